@@ -1,0 +1,157 @@
+/*
+ * timebill.h -- C ABI of the MI355X (gfx950) eviction + decode hot path of
+ * TimeBill (time-budgeted LLM inference, arXiv 2512.21859).
+ *
+ * TimeBill picks a KV-cache eviction ratio alpha per request so that the
+ * predicted worst-case time fits a budget (Sec. 5.1, Eq. alpha_with_predictor).
+ * After the prefill phase a fraction alpha of the prompt's KV cache is
+ * evicted once, and decoding runs over the retained cache, whose length at
+ * decode step i is (1 - alpha) N_x + i - 1 (Sec. 4.2, Eq. N_kv; Sec. 5.2).
+ * The paper evicts with SnapKV (Sec. 6.1).  This library provides that path:
+ *
+ *   tb_score_window  observation-window scores (softmax of the last w queries
+ *                    against the prompt keys, summed per KV head, max-pooled);
+ *   tb_select_topk   per-KV-head top-k of the scores keeping n_keep positions;
+ *   tb_compact_kv    gather of the kept K/V rows into a compact cache;
+ *   tb_decode_attn   single-token grouped-query decode attention over the
+ *                    compact cache, with the new token's K/V appended first
+ *                    (attention definition: Sec. 4.2, FLOPs-based Modeling;
+ *                    in a decoding step Q has length 1, K has length N_kv).
+ *
+ * Conventions
+ * -----------
+ * - Every pointer is a DEVICE pointer unless marked [host].  The caller owns
+ *   all buffers; the library never allocates, frees or synchronises.  Work is
+ *   enqueued on `stream`; TB_OK means "validated and enqueued".
+ * - Every argument is validated on the host before any HIP call; on error
+ *   nothing is launched and tb_last_error() describes the problem.
+ *   C++ exceptions never cross this boundary.
+ * - Layouts ("ragged lengths, padded strides"), all row-major:
+ *     q_win      [B][Hq][w][d]     window queries of the last w prompt positions
+ *     k, v       [B][Hkv][Lmax][d] prompt keys / values; sequence b valid for j < L[b]
+ *     scores     [B][Hkv][Lmax]    fp32; entries j >= L[b] - w are left untouched
+ *     keep_idx   [B][Hkv][Lmax]    int32; the first n_keep[b] entries are valid
+ *     k/v_cache  [B][Hkv][cap][d]  compact caches
+ *     kv_len     [B]               int32 current cache length per sequence (device)
+ *     q, out     [B][Hq][d];  k_new, v_new [B][Hkv][d]
+ *   Query head h uses KV head h / (Hq / Hkv).  The logit scale is 1/sqrt(d).
+ *   Rows of k / v at j >= L[b] are never read.
+ * - Supported: dtype fp32 or bf16, d in {64, 128}, B <= 64.  Scoring needs
+ *   (Hq/Hkv) * w <= 1024; decoding needs Hq/Hkv <= 8.
+ * - Retained length: n_keep = L - floor(alpha * L) in IEEE double, at least w.
+ *   The w window positions are always kept and count toward n_keep; ties in
+ *   the pooled score go to the lower position; kept positions are ascending
+ *   with the window last.
+ * - Re-entrant; the library keeps no device state.  Calls that share a
+ *   workspace must be ordered (same stream).
+ */
+#ifndef TIMEBILL_H
+#define TIMEBILL_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TB_OK = 0,
+  TB_EINVAL = 1,        /* bad argument (null pointer, size, ratio, length) */
+  TB_EUNSUPPORTED = 2,  /* valid but not supported (d, dtype, group size, B) */
+  TB_EWORKSPACE = 3,    /* ws_bytes smaller than tb_workspace_bytes() */
+  TB_EHIP = 4,          /* a HIP launch reported an error */
+  TB_EINTERNAL = 5      /* unexpected internal failure */
+} tb_status;
+
+typedef enum { TB_F32 = 0, TB_BF16 = 1 } tb_dtype;
+
+typedef enum {
+  TB_OP_SCORE = 0,
+  TB_OP_SELECT = 1,
+  TB_OP_COMPACT = 2,
+  TB_OP_DECODE = 3
+} tb_op;
+
+/* [host] Retained positions after evicting a fraction alpha of L prompt
+ * positions with a window of w (Eq. N_kv made integral): L - floor(alpha*L),
+ * at least w.  Returns -1 unless 0 < w < L and 0 <= alpha < 1. */
+int32_t tb_keep_count(int32_t L, double alpha, int32_t w);
+
+/* [host] Message describing the last error on the calling thread ("" if none).
+ * The pointer stays valid until the thread's next tb_* call. */
+const char* tb_last_error(void);
+
+/* [host] Workspace bytes the operation `op` needs for these sizes (0 if none).
+ * `cap` is used by TB_OP_DECODE only; arguments an op does not use are
+ * ignored.  Returns 0 and sets the error for invalid sizes. */
+size_t tb_workspace_bytes(int32_t op, int32_t B, int32_t Lmax, int32_t Hq,
+                          int32_t Hkv, int32_t d, int32_t w, int32_t cap);
+
+/* Observation-window scores (SnapKV eviction as used in Sec. 6.1; window
+ * queries against all prompt keys under the causal attention of Sec. 4.2).
+ * For KV head g of sequence b and prefix position j < L[b] - w:
+ *   A[j] = sum over the G query heads of group g and window rows i < w of
+ *          softmax_j'(q_win[h][i] . k[j'] / sqrt(d)),  j' <= L[b] - w + i,
+ *   scores[j] = max of A over |j - j'| <= pool/2 within the prefix.
+ * raw_scores (nullable, same layout) receives A before pooling.
+ * Arithmetic: float64 dot products, exponentials and sums; fp32 output.
+ * L: [host][B].  Requires w >= 1, odd pool >= 1, w < L[b] <= Lmax.
+ * ws: tb_workspace_bytes(TB_OP_SCORE, B, Lmax, Hq, Hkv, d, w, 0) bytes. */
+tb_status tb_score_window(const void* q_win, const void* k, int32_t B,
+                          const int32_t* L, int32_t Lmax, int32_t Hq,
+                          int32_t Hkv, int32_t d, int32_t w, int32_t pool,
+                          tb_dtype dt, float* scores, float* raw_scores,
+                          void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Per-KV-head top-k keeping n_keep[b] = tb_keep_count(L[b], alpha[b], w)
+ * positions (Eq. N_kv: a fraction alpha of the prompt's KV is evicted once,
+ * after prefill, Sec. 4.2 and Sec. 5.2).  Selects the n_keep[b] - w prefix
+ * positions with the largest scores (ties -> lower position), writes them
+ * ascending to keep_idx followed by the window positions L[b]-w .. L[b]-1.
+ * scores must be >= 0 (as tb_score_window produces).
+ * L, alpha: [host][B] inputs.  n_keep: [host][B] output, filled before return.
+ * ws: tb_workspace_bytes(TB_OP_SELECT, ...) bytes (currently 0; may be NULL). */
+tb_status tb_select_topk(const float* scores, int32_t B, const int32_t* L,
+                         int32_t Lmax, int32_t Hkv, int32_t w,
+                         const double* alpha, int32_t* keep_idx,
+                         int32_t* n_keep, void* ws, size_t ws_bytes,
+                         hipStream_t stream);
+
+/* Compaction: k_cache[b][g][i] = k[b][g][keep_idx[b][g][i]] (same for v) for
+ * i < n_keep[b]; the retained caches are what decoding uses (Sec. 5.2).
+ * Sets kv_len[b] = n_keep[b] on the device (stream-ordered).
+ * Requires 1 <= n_keep[b] <= min(Lmax, cap).  Indices should lie in
+ * [0, Lmax); the device clamps any other index into that range rather than
+ * reading outside the prompt.  Caches must not alias k or v.
+ * n_keep: [host][B].  ws: unused (may be NULL). */
+tb_status tb_compact_kv(const void* k, const void* v, const int32_t* keep_idx,
+                        int32_t B, const int32_t* n_keep, int32_t Lmax,
+                        int32_t Hkv, int32_t d, tb_dtype dt, int32_t cap,
+                        void* k_cache, void* v_cache, int32_t* kv_len,
+                        void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* One decode step of grouped-query attention (Sec. 4.2: Q of length 1
+ * against the N_kv cached keys).  With k_new/v_new given, row kv_len[b] of
+ * the caches receives them, the query attends over kv_len[b] + 1 rows and
+ * kv_len[b] is incremented on the device; with both NULL nothing is appended.
+ *   out[b][h] = sum_j softmax_j(q[b][h] . K[j] / sqrt(d)) V[j]
+ * over the rows of KV head h / (Hq/Hkv).  fp32 accumulation; out in `dt`.
+ * Lengths live only on the device, so the call can be captured in a HIP graph.
+ * The library cannot see kv_len: the caller must keep kv_len[b] + 1 <= cap
+ * when appending (an append that would overflow is dropped on the device).
+ * ws: tb_workspace_bytes(TB_OP_DECODE, B, 0, Hq, Hkv, d, 0, cap) bytes, all
+ * zero before the first call on it; every call leaves the workspace's
+ * counters at zero again.  Calls sharing a workspace must not overlap. */
+tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new,
+                         void* k_cache, void* v_cache, int32_t* kv_len,
+                         int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
+                         int32_t cap, tb_dtype dt, void* out, void* ws,
+                         size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TIMEBILL_H */

@@ -1,0 +1,213 @@
+"""ctypes binding of libtimebill.so (the C ABI declared in include/timebill.h).
+
+Argument marshalling only: every step of the path runs in the HIP kernels.
+The functions carry the C names and take torch tensors (device memory) plus
+plain Python values; work is enqueued on the current torch stream.  There is
+no fallback: without the built library every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtimebill.so")
+
+TB_OK, TB_EINVAL, TB_EUNSUPPORTED, TB_EWORKSPACE, TB_EHIP, TB_EINTERNAL = range(6)
+TB_F32, TB_BF16 = 0, 1
+TB_OP_SCORE, TB_OP_SELECT, TB_OP_COMPACT, TB_OP_DECODE = range(4)
+
+EXPORTED = ("tb_keep_count", "tb_last_error", "tb_workspace_bytes", "tb_score_window",
+            "tb_select_topk", "tb_compact_kv", "tb_decode_attn")
+
+_lib = None
+
+
+class TimebillError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"status {status}: {msg}")
+        self.status = status
+
+
+def load() -> ctypes.CDLL:
+    """Load the library once; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, dbl, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_double, ctypes.c_size_t
+    p_i32 = ctypes.POINTER(ctypes.c_int32)
+    p_dbl = ctypes.POINTER(ctypes.c_double)
+    lib.tb_keep_count.argtypes = [i32, dbl, i32]
+    lib.tb_keep_count.restype = i32
+    lib.tb_last_error.argtypes = []
+    lib.tb_last_error.restype = ctypes.c_char_p
+    lib.tb_workspace_bytes.argtypes = [i32] * 8
+    lib.tb_workspace_bytes.restype = sz
+    lib.tb_score_window.argtypes = [vp, vp, i32, p_i32, i32, i32, i32, i32, i32, i32, i32,
+                                    vp, vp, vp, sz, vp]
+    lib.tb_score_window.restype = i32
+    lib.tb_select_topk.argtypes = [vp, i32, p_i32, i32, i32, i32, p_dbl, vp, p_i32, vp, sz, vp]
+    lib.tb_select_topk.restype = i32
+    lib.tb_compact_kv.argtypes = [vp, vp, vp, i32, p_i32, i32, i32, i32, i32, i32, vp, vp, vp,
+                                  vp, sz, vp]
+    lib.tb_compact_kv.restype = i32
+    lib.tb_decode_attn.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp,
+                                   sz, vp]
+    lib.tb_decode_attn.restype = i32
+    _lib = lib
+    return lib
+
+
+def _check(status: int) -> None:
+    if status != TB_OK:
+        raise TimebillError(status, load().tb_last_error().decode())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return TB_BF16
+    if t.dtype == torch.float32:
+        return TB_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _dev(t: Optional[torch.Tensor], name: str, dtype=None) -> int:
+    if t is None:
+        return 0
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _i32_array(vals: Sequence[int]):
+    return (ctypes.c_int32 * len(vals))(*[int(v) for v in vals])
+
+
+def tb_keep_count(L: int, alpha: float, w: int) -> int:
+    return int(load().tb_keep_count(int(L), float(alpha), int(w)))
+
+
+def tb_workspace_bytes(op: int, B: int, Lmax: int, Hq: int, Hkv: int, d: int, w: int,
+                       cap: int) -> int:
+    return int(load().tb_workspace_bytes(op, B, Lmax, Hq, Hkv, d, w, cap))
+
+
+def tb_score_window(q_win: torch.Tensor, k: torch.Tensor, L: Sequence[int], w: int, pool: int,
+                    scores: torch.Tensor, raw_scores: Optional[torch.Tensor] = None,
+                    ws: Optional[torch.Tensor] = None, stream=None) -> None:
+    """q_win [B,Hq,w,d], k [B,Hkv,Lmax,d] (bf16/fp32); scores [B,Hkv,Lmax] fp32."""
+    B, Hq, w_, d = q_win.shape
+    _, Hkv, Lmax, d2 = k.shape
+    if w_ != w or d2 != d or k.shape[0] != B or k.dtype != q_win.dtype:
+        raise ValueError("q_win / k shapes or dtypes disagree")
+    if tuple(scores.shape) != (B, Hkv, Lmax):
+        raise ValueError("scores must be [B, Hkv, Lmax]")
+    if raw_scores is not None and tuple(raw_scores.shape) != (B, Hkv, Lmax):
+        raise ValueError("raw_scores must be [B, Hkv, Lmax]")
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load().tb_score_window(
+        _dev(q_win, "q_win"), _dev(k, "k"), B, _i32_array(L), Lmax, Hq, Hkv, d, w, pool,
+        _dtype_code(k), _dev(scores, "scores", torch.float32),
+        _dev(raw_scores, "raw_scores", torch.float32), _dev(ws, "ws"), ws_bytes,
+        _stream(stream)))
+
+
+def tb_select_topk(scores: torch.Tensor, L: Sequence[int], w: int, alpha: Sequence[float],
+                   keep_idx: torch.Tensor, ws: Optional[torch.Tensor] = None,
+                   stream=None) -> List[int]:
+    """scores [B,Hkv,Lmax] fp32 -> keep_idx [B,Hkv,Lmax] int32; returns n_keep per sequence."""
+    B, Hkv, Lmax = scores.shape
+    if tuple(keep_idx.shape) != (B, Hkv, Lmax):
+        raise ValueError("keep_idx must be [B, Hkv, Lmax]")
+    n_keep = (ctypes.c_int32 * B)()
+    alphas = (ctypes.c_double * B)(*[float(a) for a in alpha])
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load().tb_select_topk(
+        _dev(scores, "scores", torch.float32), B, _i32_array(L), Lmax, Hkv, w, alphas,
+        _dev(keep_idx, "keep_idx", torch.int32), n_keep, _dev(ws, "ws"), ws_bytes,
+        _stream(stream)))
+    return list(n_keep)
+
+
+def tb_compact_kv(k: torch.Tensor, v: torch.Tensor, keep_idx: torch.Tensor,
+                  n_keep: Sequence[int], k_cache: torch.Tensor, v_cache: torch.Tensor,
+                  kv_len: torch.Tensor, stream=None) -> None:
+    """k, v [B,Hkv,Lmax,d] -> caches [B,Hkv,cap,d]; kv_len [B] int32 set to n_keep."""
+    B, Hkv, Lmax, d = k.shape
+    cap = k_cache.shape[2]
+    if v.shape != k.shape or k_cache.shape != v_cache.shape or tuple(k_cache.shape) != (B, Hkv, cap, d):
+        raise ValueError("k/v or cache shapes disagree")
+    if k_cache.dtype != k.dtype or v_cache.dtype != k.dtype or v.dtype != k.dtype:
+        raise TypeError("k, v and caches must share a dtype")
+    _check(load().tb_compact_kv(
+        _dev(k, "k"), _dev(v, "v"), _dev(keep_idx, "keep_idx", torch.int32), B,
+        _i32_array(n_keep), Lmax, Hkv, d, _dtype_code(k), cap, _dev(k_cache, "k_cache"),
+        _dev(v_cache, "v_cache"), _dev(kv_len, "kv_len", torch.int32), None, 0,
+        _stream(stream)))
+
+
+def tb_decode_attn(q: torch.Tensor, k_new: Optional[torch.Tensor], v_new: Optional[torch.Tensor],
+                   k_cache: torch.Tensor, v_cache: torch.Tensor, kv_len: torch.Tensor,
+                   out: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
+    """q, out [B,Hq,d]; k_new, v_new [B,Hkv,d] or None; caches [B,Hkv,cap,d]."""
+    B, Hq, d = q.shape
+    _, Hkv, cap, d2 = k_cache.shape
+    if d2 != d or out.shape != q.shape or k_cache.shape != v_cache.shape:
+        raise ValueError("decode shapes disagree")
+    for t, name in ((k_new, "k_new"), (v_new, "v_new")):
+        if t is not None and tuple(t.shape) != (B, Hkv, d):
+            raise ValueError(f"{name} must be [B, Hkv, d]")
+    if any(t is not None and t.dtype != q.dtype for t in (k_new, v_new, k_cache, v_cache, out)):
+        raise TypeError("decode tensors must share a dtype")
+    _check(load().tb_decode_attn(
+        _dev(q, "q"), _dev(k_new, "k_new"), _dev(v_new, "v_new"), _dev(k_cache, "k_cache"),
+        _dev(v_cache, "v_cache"), _dev(kv_len, "kv_len", torch.int32), B, Hq, Hkv, d, cap,
+        _dtype_code(q), _dev(out, "out"), _dev(ws, "ws"), ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+class KVCache:
+    """Compact caches of one layer plus the host-side lengths the library cannot see.
+
+    Allocation happens here (torch device memory); every computation is a
+    call into the library.  ``decode`` refuses an append past ``cap``.
+    """
+
+    def __init__(self, B: int, Hq: int, Hkv: int, cap: int, d: int, dtype: torch.dtype,
+                 device="cuda"):
+        self.B, self.Hq, self.Hkv, self.cap, self.d = B, Hq, Hkv, cap, d
+        self.k = torch.empty((B, Hkv, cap, d), dtype=dtype, device=device)
+        self.v = torch.empty((B, Hkv, cap, d), dtype=dtype, device=device)
+        self.kv_len = torch.zeros((B,), dtype=torch.int32, device=device)
+        nbytes = tb_workspace_bytes(TB_OP_DECODE, B, 0, Hq, Hkv, d, 0, cap)
+        self.ws = torch.zeros((max(nbytes, 1),), dtype=torch.uint8, device=device)
+        self.host_len = [0] * B
+
+    def compact_from(self, k: torch.Tensor, v: torch.Tensor, keep_idx: torch.Tensor,
+                     n_keep: Sequence[int], stream=None) -> None:
+        if max(n_keep) > self.cap:
+            raise ValueError("n_keep exceeds the cache capacity")
+        tb_compact_kv(k, v, keep_idx, n_keep, self.k, self.v, self.kv_len, stream)
+        self.host_len = list(n_keep)
+
+    def decode(self, q, k_new, v_new, out, stream=None) -> None:
+        if k_new is not None and max(self.host_len) + 1 > self.cap:
+            raise ValueError("append would exceed the cache capacity")
+        tb_decode_attn(q, k_new, v_new, self.k, self.v, self.kv_len, out, self.ws, stream)
+        if k_new is not None:
+            self.host_len = [n + 1 for n in self.host_len]

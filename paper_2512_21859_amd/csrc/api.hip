@@ -1,0 +1,267 @@
+// C ABI of libtimebill: host-side validation, workspace carving and launch
+// dispatch.  Every check happens before the first HIP call, so an invalid
+// call launches nothing.  No exception crosses the boundary.
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <exception>
+#include <string>
+
+#include "../../include/timebill.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+tb_status fail(tb_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+tb_status fail(tb_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+tb_status ok() {
+  g_err.clear();
+  return TB_OK;
+}
+
+tb_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(TB_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int32_t keep_count(int32_t L, double alpha, int32_t w) {
+  if (!(w > 0 && w < L) || !(alpha >= 0.0 && alpha < 1.0)) return -1;
+  const double ev = floor(alpha * static_cast<double>(L));
+  const int32_t n = L - static_cast<int32_t>(ev);
+  return n < w ? w : n;
+}
+
+bool dtype_ok(tb_dtype dt) { return dt == TB_F32 || dt == TB_BF16; }
+int elem_bytes(tb_dtype dt) { return dt == TB_BF16 ? 2 : 4; }
+
+tb_status check_common(int32_t B, int32_t Hq, int32_t Hkv, int32_t d, tb_dtype dt) {
+  if (B < 1) return fail(TB_EINVAL, "B must be >= 1 (got %d)", B);
+  if (B > tb::kMaxB) return fail(TB_EUNSUPPORTED, "B must be <= %d (got %d)", tb::kMaxB, B);
+  if (Hkv < 1 || Hq < 1 || Hq % Hkv != 0)
+    return fail(TB_EINVAL, "need Hq %% Hkv == 0 with Hq, Hkv >= 1 (got %d, %d)", Hq, Hkv);
+  if (d != 64 && d != 128) return fail(TB_EUNSUPPORTED, "d must be 64 or 128 (got %d)", d);
+  if (!dtype_ok(dt)) return fail(TB_EUNSUPPORTED, "dtype must be TB_F32 or TB_BF16");
+  return TB_OK;
+}
+
+size_t decode_ws(int32_t B, int32_t Hkv, int32_t G, int32_t d, int32_t cap) {
+  const int chunk = tb::decode_chunk_rows(B, Hkv, cap);
+  const size_t n_chunks = (static_cast<size_t>(cap) + chunk - 1) / chunk;
+  const size_t part = static_cast<size_t>(B) * Hkv * n_chunks * G * (d + 2) * sizeof(float);
+  return align256(part) + align256(static_cast<size_t>(B) * Hkv * sizeof(int32_t)) +
+         align256(static_cast<size_t>(B) * sizeof(int32_t));
+}
+
+}  // namespace
+
+namespace tb {
+
+// Rows per decode block: enough blocks to cover the chip (B*Hkv*chunks of a
+// few hundred or more) without making the chunk partials the dominant traffic.
+int decode_chunk_rows(int B, int Hkv, int cap) {
+  const int unit = decode_rows_per_chunk_unit();               // 64
+  const long long units = static_cast<long long>(B) * Hkv;
+  long long want = (static_cast<long long>(cap) * units + 511) / 512;   // ~512 blocks
+  want = std::max<long long>(want, unit);
+  want = std::min<long long>(want, 1024);
+  return static_cast<int>((want + unit - 1) / unit * unit);
+}
+
+}  // namespace tb
+
+extern "C" {
+
+int32_t tb_keep_count(int32_t L, double alpha, int32_t w) { return keep_count(L, alpha, w); }
+
+const char* tb_last_error(void) { return g_err.c_str(); }
+
+size_t tb_workspace_bytes(int32_t op, int32_t B, int32_t Lmax, int32_t Hq, int32_t Hkv,
+                          int32_t d, int32_t w, int32_t cap) {
+  try {
+    switch (op) {
+      case TB_OP_SCORE: {
+        if (B < 1 || Lmax < 1 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0 || w < 1) {
+          fail(TB_EINVAL, "tb_workspace_bytes(SCORE): bad sizes");
+          return 0;
+        }
+        return tb::score_ws_bytes(B, Lmax, Hkv, (Hq / Hkv) * w);
+      }
+      case TB_OP_SELECT:
+      case TB_OP_COMPACT:
+        return 0;
+      case TB_OP_DECODE: {
+        if (B < 1 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0 || cap < 1 || d < 1) {
+          fail(TB_EINVAL, "tb_workspace_bytes(DECODE): bad sizes");
+          return 0;
+        }
+        return decode_ws(B, Hkv, Hq / Hkv, d, cap);
+      }
+      default:
+        fail(TB_EINVAL, "tb_workspace_bytes: unknown op %d", op);
+        return 0;
+    }
+  } catch (...) {
+    fail(TB_EINTERNAL, "tb_workspace_bytes: internal error");
+    return 0;
+  }
+}
+
+tb_status tb_score_window(const void* q_win, const void* k, int32_t B, const int32_t* L,
+                          int32_t Lmax, int32_t Hq, int32_t Hkv, int32_t d, int32_t w,
+                          int32_t pool, tb_dtype dt, float* scores, float* raw_scores,
+                          void* ws, size_t ws_bytes, hipStream_t stream) {
+  try {
+    if (!q_win || !k || !L || !scores) return fail(TB_EINVAL, "tb_score_window: null pointer");
+    tb_status st = check_common(B, Hq, Hkv, d, dt);
+    if (st != TB_OK) return st;
+    if (w < 1) return fail(TB_EINVAL, "w must be >= 1 (got %d)", w);
+    if (pool < 1 || pool % 2 == 0) return fail(TB_EINVAL, "pool must be odd and >= 1 (got %d)", pool);
+    if (pool > 129) return fail(TB_EUNSUPPORTED, "pool must be <= 129 (got %d)", pool);
+    const int R = (Hq / Hkv) * w;
+    if (R > 1024) return fail(TB_EUNSUPPORTED, "(Hq/Hkv)*w must be <= 1024 (got %d)", R);
+    for (int b = 0; b < B; ++b)
+      if (!(L[b] > w && L[b] <= Lmax))
+        return fail(TB_EINVAL, "need w < L[%d] <= Lmax (w=%d, L=%d, Lmax=%d)", b, w, L[b], Lmax);
+    const size_t need = tb::score_ws_bytes(B, Lmax, Hkv, R);
+    if (ws_bytes < need || (need > 0 && !ws))
+      return fail(TB_EWORKSPACE, "tb_score_window: workspace %zu < %zu bytes", ws_bytes, need);
+
+    tb::ScoreArgs a{};
+    a.q_win = q_win; a.k = k; a.scores = scores; a.raw_scores = raw_scores;
+    a.B = B; a.Lmax = Lmax; a.Hq = Hq; a.Hkv = Hkv; a.w = w; a.pool = pool; a.R = R;
+    a.n_tiles = (Lmax + tb::kScoreTile - 1) / tb::kScoreTile;
+    a.row_chunks = (R + tb::kScoreRows - 1) / tb::kScoreRows;
+    a.scale = 1.0 / sqrt(static_cast<double>(d));
+    for (int b = 0; b < B; ++b) a.L[b] = L[b];
+    const size_t units = static_cast<size_t>(B) * Hkv;
+    char* p = static_cast<char*>(ws);
+    a.e = reinterpret_cast<float*>(p);
+    p += align256(units * a.n_tiles * R * tb::kScoreTile * sizeof(float));
+    a.tile_m = reinterpret_cast<double*>(p);
+    p += align256(units * a.n_tiles * R * sizeof(double));
+    a.tile_z = reinterpret_cast<double*>(p);
+    p += align256(units * a.n_tiles * R * sizeof(double));
+    a.row_M = reinterpret_cast<double*>(p);
+    p += align256(units * R * sizeof(double));
+    a.row_Z = reinterpret_cast<double*>(p);
+    return hip_status(tb::launch_score(a, d, dt == TB_BF16, stream), "tb_score_window launch");
+  } catch (const std::exception& e) {
+    return fail(TB_EINTERNAL, "tb_score_window: %s", e.what());
+  } catch (...) {
+    return fail(TB_EINTERNAL, "tb_score_window: internal error");
+  }
+}
+
+tb_status tb_select_topk(const float* scores, int32_t B, const int32_t* L, int32_t Lmax,
+                         int32_t Hkv, int32_t w, const double* alpha, int32_t* keep_idx,
+                         int32_t* n_keep, void* ws, size_t ws_bytes, hipStream_t stream) {
+  (void)ws; (void)ws_bytes;
+  try {
+    if (!scores || !L || !alpha || !keep_idx || !n_keep)
+      return fail(TB_EINVAL, "tb_select_topk: null pointer");
+    if (B < 1) return fail(TB_EINVAL, "B must be >= 1 (got %d)", B);
+    if (B > tb::kMaxB) return fail(TB_EUNSUPPORTED, "B must be <= %d (got %d)", tb::kMaxB, B);
+    if (Hkv < 1) return fail(TB_EINVAL, "Hkv must be >= 1");
+    if (w < 1) return fail(TB_EINVAL, "w must be >= 1 (got %d)", w);
+    tb::SelectArgs a{};
+    for (int b = 0; b < B; ++b) {
+      if (!(L[b] > w && L[b] <= Lmax))
+        return fail(TB_EINVAL, "need w < L[%d] <= Lmax (w=%d, L=%d, Lmax=%d)", b, w, L[b], Lmax);
+      if (!(alpha[b] >= 0.0 && alpha[b] < 1.0))
+        return fail(TB_EINVAL, "alpha[%d] must be in [0, 1) (got %g)", b, alpha[b]);
+      a.L[b] = L[b];
+      a.n_keep[b] = keep_count(L[b], alpha[b], w);
+    }
+    a.scores = scores; a.keep_idx = keep_idx;
+    a.B = B; a.Lmax = Lmax; a.Hkv = Hkv; a.w = w;
+    for (int b = 0; b < B; ++b) n_keep[b] = a.n_keep[b];
+    return hip_status(tb::launch_select(a, stream), "tb_select_topk launch");
+  } catch (...) {
+    return fail(TB_EINTERNAL, "tb_select_topk: internal error");
+  }
+}
+
+tb_status tb_compact_kv(const void* k, const void* v, const int32_t* keep_idx, int32_t B,
+                        const int32_t* n_keep, int32_t Lmax, int32_t Hkv, int32_t d,
+                        tb_dtype dt, int32_t cap, void* k_cache, void* v_cache,
+                        int32_t* kv_len, void* ws, size_t ws_bytes, hipStream_t stream) {
+  (void)ws; (void)ws_bytes;
+  try {
+    if (!k || !v || !keep_idx || !n_keep || !k_cache || !v_cache || !kv_len)
+      return fail(TB_EINVAL, "tb_compact_kv: null pointer");
+    tb_status st = check_common(B, Hkv, Hkv, d, dt);
+    if (st != TB_OK) return st;
+    if (Lmax < 1 || cap < 1) return fail(TB_EINVAL, "Lmax and cap must be >= 1");
+    tb::CompactArgs a{};
+    int max_keep = 0;
+    for (int b = 0; b < B; ++b) {
+      if (!(n_keep[b] >= 1 && n_keep[b] <= Lmax && n_keep[b] <= cap))
+        return fail(TB_EINVAL, "need 1 <= n_keep[%d] <= min(Lmax, cap) (n_keep=%d, Lmax=%d, cap=%d)",
+                    b, n_keep[b], Lmax, cap);
+      a.n_keep[b] = n_keep[b];
+      max_keep = std::max(max_keep, n_keep[b]);
+    }
+    a.k = k; a.v = v; a.keep_idx = keep_idx; a.k_cache = k_cache; a.v_cache = v_cache;
+    a.kv_len = kv_len; a.B = B; a.Lmax = Lmax; a.Hkv = Hkv; a.cap = cap;
+    return hip_status(tb::launch_compact(a, d, elem_bytes(dt), max_keep, stream),
+                      "tb_compact_kv launch");
+  } catch (...) {
+    return fail(TB_EINTERNAL, "tb_compact_kv: internal error");
+  }
+}
+
+tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new, void* k_cache,
+                         void* v_cache, int32_t* kv_len, int32_t B, int32_t Hq, int32_t Hkv,
+                         int32_t d, int32_t cap, tb_dtype dt, void* out, void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  try {
+    if (!q || !k_cache || !v_cache || !kv_len || !out || !ws)
+      return fail(TB_EINVAL, "tb_decode_attn: null pointer");
+    if ((k_new == nullptr) != (v_new == nullptr))
+      return fail(TB_EINVAL, "tb_decode_attn: k_new and v_new must both be given or both NULL");
+    tb_status st = check_common(B, Hq, Hkv, d, dt);
+    if (st != TB_OK) return st;
+    const int G = Hq / Hkv;
+    if (G > 8) return fail(TB_EUNSUPPORTED, "Hq/Hkv must be <= 8 for decoding (got %d)", G);
+    if (cap < 1) return fail(TB_EINVAL, "cap must be >= 1");
+    const size_t need = decode_ws(B, Hkv, G, d, cap);
+    if (ws_bytes < need)
+      return fail(TB_EWORKSPACE, "tb_decode_attn: workspace %zu < %zu bytes", ws_bytes, need);
+    tb::DecodeArgs a{};
+    a.q = q; a.k_new = k_new; a.v_new = v_new; a.k_cache = k_cache; a.v_cache = v_cache;
+    a.kv_len = kv_len; a.out = out;
+    a.B = B; a.Hkv = Hkv; a.cap = cap;
+    a.chunk = tb::decode_chunk_rows(B, Hkv, cap);
+    a.n_chunks = (cap + a.chunk - 1) / a.chunk;
+    a.append = k_new != nullptr;
+    a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(d)));
+    char* p = static_cast<char*>(ws);
+    a.part = reinterpret_cast<float*>(p);
+    p += align256(static_cast<size_t>(B) * Hkv * a.n_chunks * G * (d + 2) * sizeof(float));
+    a.head_ctr = reinterpret_cast<int32_t*>(p);
+    p += align256(static_cast<size_t>(B) * Hkv * sizeof(int32_t));
+    a.seq_ctr = reinterpret_cast<int32_t*>(p);
+    return hip_status(tb::launch_decode(a, G, d, dt == TB_BF16, stream), "tb_decode_attn launch");
+  } catch (...) {
+    return fail(TB_EINTERNAL, "tb_decode_attn: internal error");
+  }
+}
+
+}  // extern "C"

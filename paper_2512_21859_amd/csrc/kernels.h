@@ -1,0 +1,76 @@
+// Launch-argument structs and launchers of the gfx950 kernels.  The C ABI in
+// api.hip validates every argument before calling these.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tb {
+
+constexpr int kMaxB = 64;        // per-sequence values travel in kernel arguments
+constexpr int kScoreTile = 64;   // keys per scoring tile
+constexpr int kScoreRows = 256;  // window rows per scoring block
+
+// ---------------------------------------------------------------- scoring
+struct ScoreArgs {
+  const void* q_win;      // [B][Hq][w][d]
+  const void* k;          // [B][Hkv][Lmax][d]
+  float* scores;          // [B][Hkv][Lmax]
+  float* raw_scores;      // nullable, same layout
+  float* e;               // ws: [B][Hkv][n_tiles][R][64] exp(s - tile max), fp32
+  double* tile_m;         // ws: [B][Hkv][n_tiles][R]
+  double* tile_z;         // ws: [B][Hkv][n_tiles][R]
+  double* row_M;          // ws: [B][Hkv][R]
+  double* row_Z;          // ws: [B][Hkv][R]
+  int32_t B, Lmax, Hq, Hkv, w, pool, R, n_tiles, row_chunks;
+  double scale;           // 1/sqrt(d)
+  int32_t L[kMaxB];
+};
+size_t score_ws_bytes(int B, int Lmax, int Hkv, int R);
+hipError_t launch_score(const ScoreArgs& a, int d, bool bf16, hipStream_t st);
+
+// ---------------------------------------------------------------- selection
+struct SelectArgs {
+  const float* scores;    // [B][Hkv][Lmax]
+  int32_t* keep_idx;      // [B][Hkv][Lmax]
+  int32_t B, Lmax, Hkv, w;
+  int32_t L[kMaxB];
+  int32_t n_keep[kMaxB];
+};
+hipError_t launch_select(const SelectArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- compaction
+struct CompactArgs {
+  const void* k;          // [B][Hkv][Lmax][d]
+  const void* v;
+  const int32_t* keep_idx;  // [B][Hkv][Lmax]
+  void* k_cache;          // [B][Hkv][cap][d]
+  void* v_cache;
+  int32_t* kv_len;        // [B]
+  int32_t B, Lmax, Hkv, cap, rows_per_block;
+  int32_t n_keep[kMaxB];
+};
+hipError_t launch_compact(const CompactArgs& a, int d, int elem_bytes, int max_keep,
+                          hipStream_t st);
+
+// ---------------------------------------------------------------- decode
+struct DecodeArgs {
+  const void* q;          // [B][Hq][d]
+  const void* k_new;      // [B][Hkv][d] (unused when append == 0)
+  const void* v_new;
+  void* k_cache;          // [B][Hkv][cap][d]
+  void* v_cache;
+  int32_t* kv_len;        // [B]
+  void* out;              // [B][Hq][d]
+  float* part;            // ws: [B][Hkv][n_chunks][G*(d+2)]
+  int32_t* head_ctr;      // ws: [B*Hkv], zero between launches
+  int32_t* seq_ctr;       // ws: [B], zero between launches
+  int32_t B, Hkv, cap, chunk, n_chunks, append;
+  float scale_log2;       // log2(e)/sqrt(d)
+};
+int decode_rows_per_chunk_unit();
+int decode_chunk_rows(int B, int Hkv, int cap);
+size_t decode_ws_bytes(int B, int Hkv, int G, int d, int cap);
+hipError_t launch_decode(const DecodeArgs& a, int G, int d, bool bf16, hipStream_t st);
+
+}  // namespace tb

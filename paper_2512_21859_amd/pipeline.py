@@ -1,0 +1,54 @@
+"""Orchestration of the eviction + decode path over the C ABI.
+
+Eviction happens once per request and layer after the prefill phase
+(score -> select -> compact), then every decode step appends the new token's
+K/V and attends over the retained cache (TimeBill Sec. 5.2 deployment; the
+retained length follows Eq. N_kv).  This module only allocates device buffers
+(torch) and sequences library calls; all arithmetic runs in the kernels.
+"""
+from __future__ import annotations
+
+from typing import Optional, Sequence
+
+import torch
+
+from . import _lib
+
+
+class Evictor:
+    """Score / select buffers and workspace for one layer shape."""
+
+    def __init__(self, B: int, Lmax: int, Hq: int, Hkv: int, d: int, w: int, pool: int,
+                 device="cuda", keep_raw: bool = False):
+        self.B, self.Lmax, self.Hq, self.Hkv, self.d, self.w, self.pool = B, Lmax, Hq, Hkv, d, w, pool
+        self.scores = torch.empty((B, Hkv, Lmax), dtype=torch.float32, device=device)
+        self.raw = (torch.empty((B, Hkv, Lmax), dtype=torch.float32, device=device)
+                    if keep_raw else None)
+        self.keep_idx = torch.empty((B, Hkv, Lmax), dtype=torch.int32, device=device)
+        nbytes = _lib.tb_workspace_bytes(_lib.TB_OP_SCORE, B, Lmax, Hq, Hkv, d, w, 0)
+        self.ws = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=device)
+
+    def score(self, q_win: torch.Tensor, k: torch.Tensor, L: Sequence[int], stream=None) -> None:
+        _lib.tb_score_window(q_win, k, L, self.w, self.pool, self.scores, self.raw, self.ws,
+                             stream)
+
+    def select(self, L: Sequence[int], alphas: Sequence[float], stream=None):
+        return _lib.tb_select_topk(self.scores, L, self.w, alphas, self.keep_idx, None, stream)
+
+    def evict(self, q_win, k, v, L, alphas, cache: "_lib.KVCache", stream=None):
+        """Score, select and compact into ``cache``; returns n_keep per sequence."""
+        self.score(q_win, k, L, stream)
+        n_keep = self.select(L, alphas, stream)
+        cache.compact_from(k, v, self.keep_idx, n_keep, stream)
+        return n_keep
+
+
+def run_decode(cache: "_lib.KVCache", q: torch.Tensor, k_new: torch.Tensor,
+               v_new: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+    """Decode T steps: q [T,B,Hq,d], k_new/v_new [T,B,Hkv,d] -> out [T,B,Hq,d]."""
+    T = q.shape[0]
+    if out is None:
+        out = torch.empty_like(q)
+    for t in range(T):
+        cache.decode(q[t], k_new[t], v_new[t], out[t], stream)
+    return out

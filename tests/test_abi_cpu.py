@@ -1,0 +1,152 @@
+"""C ABI checks that need no GPU: the library loads, exports every declared
+symbol, computes n_keep like the oracle, sizes workspaces, and rejects bad
+arguments before any HIP call (only calls that fail validation are made)."""
+import ctypes
+import json
+import os
+import re
+import subprocess
+
+import pytest
+
+from oracle import timebill_oracle as O
+from paper_2512_21859_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "timebill.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def _declared():
+    text = open(HEADER).read()
+    decl = r"^(?:int32_t|size_t|tb_status|const char\*)\s+(tb_[a-z_]+)\("
+    return sorted(set(re.findall(decl, text, re.M)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert set(names) == set(_lib.EXPORTED), names
+    nm = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True,
+                        text=True, check=True).stdout
+    exported = set(re.findall(r" T (tb_[a-z_]+)$", nm, re.M))
+    for n in names:
+        assert n in exported, f"{n} not exported"
+        assert hasattr(lib, n)
+
+
+def test_keep_count_matches_oracle_and_table(lib):
+    with open(os.path.join(ROOT, "tests", "golden", "n_keep_table.json")) as f:
+        tab = json.load(f)
+    for case in tab["cases"]:
+        alphas = case.get("alphas") or [k / 20 for k in case["alphas_k_over_20"]]
+        assert [_lib.tb_keep_count(case["n_x"], a, case["w"]) for a in alphas] == case["n_keep"]
+    for L in (2, 3, 17, 1000, 131072):
+        for a in (0.0, 0.05, 0.3333, 0.5, 0.9, 0.999):
+            for w in (1, 2, 16):
+                if w < L:
+                    assert _lib.tb_keep_count(L, a, w) == O.keep_count(L, a, w)
+    assert _lib.tb_keep_count(10, 1.0, 2) == -1
+    assert _lib.tb_keep_count(10, -0.5, 2) == -1
+    assert _lib.tb_keep_count(10, 0.5, 10) == -1
+
+
+def test_workspace_sizes(lib):
+    s = _lib.tb_workspace_bytes(_lib.TB_OP_SCORE, 1, 8192, 28, 4, 128, 32, 0)
+    assert s >= 4 * 128 * 224 * 64 * 4                     # the per-tile exponentials
+    assert _lib.tb_workspace_bytes(_lib.TB_OP_SELECT, 1, 8192, 28, 4, 128, 32, 0) == 0
+    d = _lib.tb_workspace_bytes(_lib.TB_OP_DECODE, 1, 0, 28, 4, 128, 0, 8448)
+    assert d > 8 and d % 256 == 0
+    assert _lib.tb_workspace_bytes(_lib.TB_OP_DECODE, 1, 0, 28, 5, 128, 0, 8448) == 0
+    assert b"bad sizes" in lib.tb_last_error()
+    assert _lib.tb_workspace_bytes(9, 1, 1, 1, 1, 64, 1, 1) == 0
+
+
+FAKE = ctypes.c_void_p(0x1000)     # never dereferenced: every call below fails validation
+
+
+def _i32(*v):
+    return (ctypes.c_int32 * len(v))(*v)
+
+
+def _score(lib, **kw):
+    a = dict(q=FAKE, k=FAKE, B=1, L=_i32(100), Lmax=100, Hq=4, Hkv=2, d=128, w=8, pool=7,
+             dt=_lib.TB_BF16, sc=FAKE, raw=None, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    return lib.tb_score_window(a["q"], a["k"], a["B"], a["L"], a["Lmax"], a["Hq"], a["Hkv"],
+                               a["d"], a["w"], a["pool"], a["dt"], a["sc"], a["raw"], a["ws"],
+                               a["wsb"], None)
+
+
+def test_score_validation(lib):
+    E = _lib
+    assert _score(lib, q=None) == E.TB_EINVAL
+    assert _score(lib, B=0) == E.TB_EINVAL
+    assert _score(lib, B=65, L=_i32(*([100] * 65))) == E.TB_EUNSUPPORTED
+    assert _score(lib, Hq=5) == E.TB_EINVAL
+    assert _score(lib, d=96) == E.TB_EUNSUPPORTED
+    assert _score(lib, dt=7) == E.TB_EUNSUPPORTED
+    assert _score(lib, w=0) == E.TB_EINVAL
+    assert _score(lib, pool=4) == E.TB_EINVAL
+    assert _score(lib, pool=131) == E.TB_EUNSUPPORTED
+    assert _score(lib, w=100) == E.TB_EINVAL            # w must be < L
+    assert _score(lib, L=_i32(101)) == E.TB_EINVAL      # L > Lmax
+    assert _score(lib, Hq=40, Hkv=1, w=32) == E.TB_EUNSUPPORTED   # G*w > 1024
+    assert _score(lib, wsb=16) == E.TB_EWORKSPACE
+    assert b"workspace" in lib.tb_last_error()
+
+
+def test_select_validation(lib):
+    E = _lib
+    n_keep = (ctypes.c_int32 * 1)()
+
+    def call(alpha=0.5, L=100, Lmax=100, w=8, B=1, keep=FAKE):
+        a = (ctypes.c_double * 1)(alpha)
+        return lib.tb_select_topk(FAKE, B, _i32(L), Lmax, 2, w, a, keep, n_keep, None, 0, None)
+
+    assert call(alpha=1.0) == E.TB_EINVAL
+    assert call(alpha=-0.1) == E.TB_EINVAL
+    assert call(alpha=float("nan")) == E.TB_EINVAL
+    assert call(L=101) == E.TB_EINVAL
+    assert call(w=100) == E.TB_EINVAL
+    assert call(B=0) == E.TB_EINVAL
+    assert call(keep=None) == E.TB_EINVAL
+
+
+def test_compact_validation(lib):
+    E = _lib
+
+    def call(n=50, cap=60, Lmax=100, d=128, dt=_lib.TB_BF16, kc=FAKE):
+        return lib.tb_compact_kv(FAKE, FAKE, FAKE, 1, _i32(n), Lmax, 2, d, dt, cap, kc, FAKE,
+                                 FAKE, None, 0, None)
+
+    assert call(n=61) == E.TB_EINVAL          # beyond cap
+    assert call(n=0) == E.TB_EINVAL
+    assert call(n=101, cap=200) == E.TB_EINVAL  # beyond Lmax
+    assert call(d=32) == E.TB_EUNSUPPORTED
+    assert call(kc=None) == E.TB_EINVAL
+
+
+def test_decode_validation(lib):
+    E = _lib
+
+    def call(Hq=28, Hkv=4, d=128, cap=100, wsb=1 << 30, kn=FAKE, vn=FAKE, ws=FAKE):
+        return lib.tb_decode_attn(FAKE, kn, vn, FAKE, FAKE, FAKE, 1, Hq, Hkv, d, cap,
+                                  _lib.TB_BF16, FAKE, ws, wsb, None)
+
+    assert call(kn=None) == E.TB_EINVAL       # k_new without v_new
+    assert call(Hq=36, Hkv=4) == E.TB_EUNSUPPORTED   # G = 9
+    assert call(Hq=30) == E.TB_EINVAL
+    assert call(d=256) == E.TB_EUNSUPPORTED
+    assert call(cap=0) == E.TB_EINVAL
+    assert call(wsb=8) == E.TB_EWORKSPACE
+    assert call(ws=None) == E.TB_EINVAL
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        _lib._dev(torch.zeros(3), "x")

@@ -1,0 +1,351 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle.
+
+Every case prints its name before touching the GPU.  Inputs come from the
+seeded generators; expected values come only from the oracle.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import timebill_oracle as O
+from paper_2512_21859_amd import _lib, synth
+from paper_2512_21859_amd.pipeline import Evictor, run_decode
+from tests.parity_util import DECODE_TOL, check_keep, f64, score_rel_err
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+SCORE_REL_TOL = 5e-7
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU in this container")
+    _lib.load()          # raises if the library was not built
+    torch.cuda.init()
+
+
+def case(msg):
+    print(f"\n[case] {msg}", flush=True)
+
+
+# ------------------------------------------------------------------ decode only
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("G", [1, 2, 3, 4, 7, 8])
+@pytest.mark.parametrize("cap,lens", [(700, [1, 523]), (20000, [19990, 4097])])
+def test_decode_only(dtype, d, G, cap, lens):
+    case(f"decode_only dtype={dtype} d={d} G={G} cap={cap} lens={lens}")
+    B, Hkv, T = 2, 2, 3
+    Hq = G * Hkv
+    g = torch.Generator().manual_seed(1234 + G + d + cap)
+    kc = torch.randn((B, Hkv, cap, d), generator=g).to(dtype)
+    vc = torch.randn((B, Hkv, cap, d), generator=g).to(dtype)
+    q = torch.randn((T + 1, B, Hq, d), generator=g).to(dtype)
+    kn = torch.randn((T, B, Hkv, d), generator=g).to(dtype)
+    vn = torch.randn((T, B, Hkv, d), generator=g).to(dtype)
+    cache = _lib.KVCache(B, Hq, Hkv, cap, d, dtype)
+    cache.k.copy_(kc)
+    cache.v.copy_(vc)
+    cache.kv_len.copy_(torch.tensor(lens, dtype=torch.int32))
+    cache.host_len = list(lens)
+    qd, knd, vnd = q.to(DEV), kn.to(DEV), vn.to(DEV)
+    out = torch.empty((T + 1, B, Hq, d), dtype=dtype, device=DEV)
+    for t in range(T):
+        cache.decode(qd[t], knd[t], vnd[t], out[t])
+    cache.decode(qd[T], None, None, out[T])            # no append
+    torch.cuda.synchronize()
+    assert cache.kv_len.cpu().tolist() == [n + T for n in lens]
+    got = f64(out)
+    tol = DECODE_TOL[dtype]
+    kc64, vc64, kn64, vn64, q64 = f64(kc), f64(vc), f64(kn), f64(vn), f64(q)
+    for b in range(B):
+        for gg in range(Hkv):
+            for t in range(T + 1):
+                n = lens[b] + min(t + 1, T)
+                rows_k = np.concatenate([kc64[b, gg, :lens[b]], kn64[:min(t + 1, T), b, gg]])
+                rows_v = np.concatenate([vc64[b, gg, :lens[b]], vn64[:min(t + 1, T), b, gg]])
+                assert rows_k.shape[0] == n
+                ref = O.decode_step(q64[t, b, gg * G:(gg + 1) * G], rows_k, rows_v)
+                err = np.abs(got[t, b, gg * G:(gg + 1) * G] - ref).max()
+                assert err <= tol, f"b={b} g={gg} t={t}: max abs err {err}"
+    # the appended rows landed in the caches
+    for t in range(T):
+        for b in range(B):
+            assert torch.equal(cache.k[b, :, lens[b] + t].cpu(), kn[t, b])
+            assert torch.equal(cache.v[b, :, lens[b] + t].cpu(), vn[t, b])
+
+
+# ------------------------------------------------------------------ compaction
+@pytest.mark.parametrize("dtype,d", [(torch.bfloat16, 128), (torch.bfloat16, 64),
+                                     (torch.float32, 64), (torch.float32, 128)])
+def test_compact_exact(dtype, d):
+    case(f"compact dtype={dtype} d={d}")
+    B, Hkv, Lmax = 3, 2, 1000
+    g = torch.Generator().manual_seed(99 + d)
+    k = torch.randn((B, Hkv, Lmax, d), generator=g).to(dtype)
+    v = torch.randn((B, Hkv, Lmax, d), generator=g).to(dtype)
+    n_keep = [1, 517, 1000]
+    cap = 1100
+    keep = torch.zeros((B, Hkv, Lmax), dtype=torch.int32)
+    for b in range(B):
+        for gg in range(Hkv):
+            sel = torch.sort(torch.randperm(Lmax, generator=g)[: n_keep[b]]).values
+            keep[b, gg, : n_keep[b]] = sel.to(torch.int32)
+    kd, vd = k.to(DEV), v.to(DEV)
+    kc = torch.zeros((B, Hkv, cap, d), dtype=dtype, device=DEV)
+    vc = torch.zeros_like(kc)
+    kv_len = torch.zeros((B,), dtype=torch.int32, device=DEV)
+    _lib.tb_compact_kv(kd, vd, keep.to(DEV), n_keep, kc, vc, kv_len)
+    torch.cuda.synchronize()
+    assert kv_len.cpu().tolist() == n_keep
+    for b in range(B):
+        for gg in range(Hkv):
+            idx = keep[b, gg, : n_keep[b]].long()
+            assert torch.equal(kc[b, gg, : n_keep[b]].cpu(), k[b, gg, idx])
+            assert torch.equal(vc[b, gg, : n_keep[b]].cpu(), v[b, gg, idx])
+            assert torch.count_nonzero(kc[b, gg, n_keep[b]:]).item() == 0
+
+
+# ------------------------------------------------------------------ selection
+def _select_case(pooled64: np.ndarray, L, w, alphas, where):
+    """pooled64 [B, Hkv, Lmax] float64 (prefix entries valid); GPU selects on fp32."""
+    B, Hkv, Lmax = pooled64.shape
+    p32 = torch.from_numpy(pooled64).to(torch.float32)
+    keep = torch.full((B, Hkv, Lmax), -1, dtype=torch.int32, device=DEV)
+    n_keep = _lib.tb_select_topk(p32.to(DEV), L, w, alphas, keep)
+    torch.cuda.synchronize()
+    kk = keep.cpu().numpy()
+    p32_64 = p32.to(torch.float64).numpy()
+    for b in range(B):
+        assert n_keep[b] == O.keep_count(L[b], alphas[b], w)
+        for gg in range(Hkv):
+            ref = O.select_keep(p32_64[b, gg, : L[b] - w], L[b], w, n_keep[b])
+            assert np.array_equal(kk[b, gg, : n_keep[b]], ref), f"{where} b={b} g={gg}"
+
+
+def test_select_exact_on_oracle_scores():
+    case("select on oracle pooled scores (fp32), ties by position")
+    wl = synth.custom(901, torch.bfloat16, 3, [300, 4099, 9000], 8, 2, 64, 8, 7, 1)
+    pr = synth.make_prompt(wl, L=[300, 4099, 9000])
+    L, w = pr["L"], wl.w
+    Lmax = max(L)
+    pooled = np.zeros((wl.B, wl.Hkv, Lmax))
+    for b in range(wl.B):
+        raw = O.window_scores(f64(pr["q_win"][b]), f64(pr["k"][b]), L[b], w)
+        pooled[b, :, : L[b] - w] = O.max_pool(raw, 7)
+    for alphas in ([0.0, 0.0, 0.0], [0.3, 0.5, 0.7], [0.99, 0.95, 0.9], [0.1, 0.05, 0.995]):
+        _select_case(pooled, L, w, alphas, f"alphas={alphas}")
+
+
+@pytest.mark.parametrize("levels", [1, 2, 3, 17])
+def test_select_exact_plateaus(levels):
+    case(f"select with heavy ties, {levels} distinct levels")
+    rng = np.random.default_rng(levels)
+    B, Hkv, w = 2, 3, 4
+    L = [5, 20000]
+    pooled = np.zeros((B, Hkv, max(L)))
+    for b in range(B):
+        pooled[b, :, : L[b] - w] = rng.integers(0, levels, (Hkv, L[b] - w)) / 8.0 + 0.5
+    for alphas in ([0.0, 0.1], [0.2, 0.5], [0.5, 0.999], [0.79, 0.25]):
+        _select_case(pooled, L, w, alphas, f"levels={levels} alphas={alphas}")
+
+
+# ------------------------------------------------------------------ scoring
+@pytest.mark.parametrize("dtype,d,G,w,pool,L", [
+    (torch.float32, 64, 2, 16, 5, [512]),
+    (torch.float32, 128, 1, 5, 3, [70, 333]),
+    (torch.bfloat16, 128, 7, 32, 7, [1000, 65, 4097]),
+    (torch.bfloat16, 64, 4, 64, 1, [129, 3000]),
+    (torch.bfloat16, 128, 8, 40, 9, [2100]),          # 320 rows: two row chunks
+    (torch.bfloat16, 128, 16, 64, 7, [700]),          # 1024 rows: four row chunks
+])
+def test_score_matches_oracle(dtype, d, G, w, pool, L):
+    case(f"score dtype={dtype} d={d} G={G} w={w} pool={pool} L={L}")
+    Hkv = 2
+    wl = synth.custom(700 + d + G + w, dtype, len(L), L, G * Hkv, Hkv, d, w, pool, 1)
+    pr = synth.make_prompt(wl, L=L, pad_value=float("nan"))    # padding must never be read
+    ev = Evictor(len(L), max(L), G * Hkv, Hkv, d, w, pool, keep_raw=True)
+    ev.scores.fill_(-7.0)
+    ev.score(pr["q_win"].to(DEV), pr["k"].to(DEV), L)
+    torch.cuda.synchronize()
+    sc, raw = ev.scores.cpu().numpy(), ev.raw.cpu().numpy()
+    worst = 0.0
+    for b in range(len(L)):
+        ref_raw = O.window_scores(f64(pr["q_win"][b]), f64(pr["k"][b]), L[b], w)
+        ref = O.max_pool(ref_raw, pool)
+        pref = L[b] - w
+        worst = max(worst, score_rel_err(raw[b, :, :pref], ref_raw),
+                    score_rel_err(sc[b, :, :pref], ref))
+        assert np.all(sc[b, :, pref:] == -7.0), "scores beyond the prefix were written"
+    print(f"max relative score error {worst:.3e}", flush=True)
+    assert worst <= SCORE_REL_TOL
+
+
+# ------------------------------------------------------------------ full chains
+_POOLED = {}
+
+
+def _oracle_pooled(wl, layer, b, q64, k64, n_x):
+    key = (wl.wid, layer, b, n_x)
+    if key not in _POOLED:
+        _POOLED.clear() if len(_POOLED) > 64 else None
+        _POOLED[key] = O.max_pool(O.window_scores(q64, k64, n_x, wl.w), wl.pool)
+    return _POOLED[key]
+
+
+def _run_layer(wl, layer, L, alphas, T, check_steps, prompt=None, dec=None):
+    """GPU eviction + decode for one layer; checked against the oracle."""
+    pr = prompt or synth.make_prompt(wl, layer, L=L)
+    dc = dec or synth.make_decode(wl, layer, T=T)
+    B, Hq, Hkv, d, w = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w
+    Lmax = max(L)
+    ev = Evictor(B, Lmax, Hq, Hkv, d, w, wl.pool)
+    n_keep_host = [O.keep_count(L[b], alphas[b], w) for b in range(B)]
+    cache = _lib.KVCache(B, Hq, Hkv, max(n_keep_host) + T, d, wl.dtype)
+    n_keep = ev.evict(pr["q_win"].to(DEV), pr["k"].to(DEV), pr["v"].to(DEV), L, alphas, cache)
+    assert n_keep == n_keep_host
+    out = run_decode(cache, dc["q"].to(DEV), dc["k_new"].to(DEV), dc["v_new"].to(DEV))
+    torch.cuda.synchronize()
+    keep = ev.keep_idx.cpu().numpy()
+    sc = ev.scores.cpu().numpy()
+    got = f64(out)
+    excused, worst_score, worst_dec = 0, 0.0, 0.0
+    for b in range(B):
+        q64, k64, v64 = f64(pr["q_win"][b]), f64(pr["k"][b]), f64(pr["v"][b])
+        pooled = _oracle_pooled(wl, layer, b, q64, k64, L[b])
+        pref = L[b] - w
+        worst_score = max(worst_score, score_rel_err(sc[b, :, :pref], pooled))
+        kc = np.empty((Hkv, n_keep[b], d))
+        vc = np.empty((Hkv, n_keep[b], d))
+        for g in range(Hkv):
+            gk = keep[b, g, : n_keep[b]]
+            excused += check_keep(gk, pooled[g], L[b], w, n_keep[b],
+                                  f"{wl.name} layer={layer} b={b} g={g} alpha={alphas[b]}")
+            kc[g], vc[g] = k64[g, gk], v64[g, gk]
+        ref = O.decode_sequence(f64(dc["q"][:, b]), f64(dc["k_new"][:, b]),
+                                f64(dc["v_new"][:, b]), kc, vc, steps=check_steps)
+        for t, o in ref.items():
+            worst_dec = max(worst_dec, float(np.abs(got[t, b] - o).max()))
+    print(f"{wl.name} layer={layer} alphas={[round(a, 4) for a in alphas]}: "
+          f"excused={excused} max score rel err={worst_score:.2e} "
+          f"max decode abs err={worst_dec:.2e}", flush=True)
+    assert worst_score <= SCORE_REL_TOL
+    assert worst_dec <= DECODE_TOL[wl.dtype]
+    return out
+
+
+def _steps(T, every=16):
+    return sorted(set([0, 1, T - 1] + list(range(0, T, every))))
+
+
+def test_workload1_tiny_fp32():
+    wl = synth.WORKLOADS[1]
+    case(wl.name)
+    _run_layer(wl, 0, [wl.L], [0.5], wl.T, range(wl.T))
+
+
+@pytest.mark.parametrize("alpha", synth.WORKLOADS[2].alphas)
+def test_workload2_single_layer(alpha):
+    wl = synth.WORKLOADS[2]
+    case(f"{wl.name} alpha={alpha}")
+    _run_layer(wl, 0, [wl.L], [alpha], wl.T, _steps(wl.T))
+
+
+def test_workload4_ragged():
+    wl = synth.WORKLOADS[4]
+    L, alphas = synth.lengths_and_alphas(wl)
+    case(f"{wl.name} L={L}")
+    _run_layer(wl, 0, L, alphas, wl.T, _steps(wl.T, 64))
+
+
+def test_workload3_layers_and_sweep():
+    wl = synth.WORKLOADS[3]
+    case(f"{wl.name}: eviction on every layer at 5 ratios, decode checked on 3 layers")
+    for layer in range(wl.layers):
+        pr = synth.make_prompt(wl, layer)
+        dc = synth.make_decode(wl, layer)
+        alphas = wl.alphas[::4] if layer not in (0, 13, 27) else wl.alphas[::2]
+        for a in alphas:
+            steps = [0, wl.T - 1] if layer in (0, 13, 27) else []
+            _run_layer(wl, layer, [wl.L], [a], wl.T, steps, prompt=pr, dec=dc)
+
+
+@pytest.mark.parametrize("alpha", synth.WORKLOADS[5].alphas)
+def test_workload5_long_context(alpha):
+    wl = synth.WORKLOADS[5]
+    case(f"{wl.name} alpha={alpha}")
+    _run_layer(wl, 0, [wl.L], [alpha], wl.T, [0, 255, wl.T - 1])
+
+
+# ------------------------------------------------------------------ properties
+def test_determinism_and_alpha0_identity():
+    wl = synth.WORKLOADS[2]
+    case(f"{wl.name}: run twice bit-identical; alpha=0 compacted == raw cache")
+    pr = synth.make_prompt(wl)
+    dc = synth.make_decode(wl, T=16)
+    qd, kd, vd = pr["q_win"].to(DEV), pr["k"].to(DEV), pr["v"].to(DEV)
+    res = []
+    for _ in range(2):
+        ev = Evictor(1, wl.L, wl.Hq, wl.Hkv, wl.d, wl.w, wl.pool, keep_raw=True)
+        cache = _lib.KVCache(1, wl.Hq, wl.Hkv, wl.L + 16, wl.d, wl.dtype)
+        ev.evict(qd, kd, vd, [wl.L], [0.5], cache)
+        out = run_decode(cache, dc["q"].to(DEV), dc["k_new"].to(DEV), dc["v_new"].to(DEV))
+        torch.cuda.synchronize()
+        res.append((ev.scores.clone(), ev.raw.clone(), ev.keep_idx.clone(), out.clone()))
+    for x, y in zip(res[0], res[1]):
+        assert torch.equal(x, y)
+    # alpha = 0: the compacted cache is the prompt cache itself
+    ev = Evictor(1, wl.L, wl.Hq, wl.Hkv, wl.d, wl.w, wl.pool)
+    c0 = _lib.KVCache(1, wl.Hq, wl.Hkv, wl.L + 16, wl.d, wl.dtype)
+    ev.evict(qd, kd, vd, [wl.L], [0.0], c0)
+    c1 = _lib.KVCache(1, wl.Hq, wl.Hkv, wl.L + 16, wl.d, wl.dtype)
+    c1.k[:, :, : wl.L].copy_(kd)
+    c1.v[:, :, : wl.L].copy_(vd)
+    c1.kv_len.fill_(wl.L)
+    c1.host_len = [wl.L]
+    o0 = run_decode(c0, dc["q"].to(DEV), dc["k_new"].to(DEV), dc["v_new"].to(DEV))
+    o1 = run_decode(c1, dc["q"].to(DEV), dc["k_new"].to(DEV), dc["v_new"].to(DEV))
+    torch.cuda.synchronize()
+    assert torch.equal(ev.keep_idx[0, :, : wl.L].cpu(),
+                       torch.arange(wl.L, dtype=torch.int32).expand(wl.Hkv, wl.L))
+    assert torch.equal(o0, o1)
+
+
+def test_decode_graph_replay():
+    wl = synth.WORKLOADS[2]
+    case(f"{wl.name}: 8 decode steps captured in a graph, replayed 3 times")
+    T = 8
+    pr = synth.make_prompt(wl)
+    dc = synth.make_decode(wl, T=T)
+    qd, knd, vnd = dc["q"].to(DEV), dc["k_new"].to(DEV), dc["v_new"].to(DEV)
+    ev = Evictor(1, wl.L, wl.Hq, wl.Hkv, wl.d, wl.w, wl.pool)
+    cache = _lib.KVCache(1, wl.Hq, wl.Hkv, 8192, wl.d, wl.dtype)
+    ev.evict(pr["q_win"].to(DEV), pr["k"].to(DEV), pr["v"].to(DEV), [wl.L], [0.75], cache)
+    torch.cuda.synchronize()
+    len0 = cache.kv_len.clone()
+    eager = torch.empty_like(qd)
+    for t in range(T):
+        _lib.tb_decode_attn(qd[t], knd[t], vnd[t], cache.k, cache.v, cache.kv_len, eager[t],
+                            cache.ws)
+    torch.cuda.synchronize()
+    graph_out = torch.empty_like(qd)
+    s = torch.cuda.Stream()
+    cache.kv_len.copy_(len0)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for t in range(T):
+            _lib.tb_decode_attn(qd[t], knd[t], vnd[t], cache.k, cache.v, cache.kv_len,
+                                graph_out[t], cache.ws, stream=s)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        cache.kv_len.copy_(len0)
+        graph_out.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(graph_out, eager), f"replay {rep} differs from eager"
+        assert torch.equal(cache.kv_len, len0 + T)
