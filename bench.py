@@ -1,0 +1,254 @@
+"""Benchmark of the eviction + decode hot path on one MI355X.
+
+Workload: one bf16 layer with a prompt of L = 8192 tokens, 28 query / 4 KV
+heads of dimension 128, observation window 32, max-pool 7, swept over the
+eviction ratios alpha in {0, 0.25, 0.5, 0.75, 0.95} (no eviction plus the
+paper's fixed-ratio arms), 256 decode steps per ratio.  Inputs are seeded
+synthetic tensors already resident in HBM when timing starts.
+
+One step = for every alpha: score the window, select, compact (one eviction,
+as after a prefill), then 256 decode steps (append + attention), replayed
+from a HIP graph captured once.  The metric is decode tokens per second over
+the whole step (eviction time included); per-alpha rows give the decode time
+per token and the achieved bandwidth.
+
+The roofline entry is for the decode-attention kernel, the dominant one:
+algorithmic bytes per launch (K and V rows of the cache plus q, the new K/V
+row and the output) divided by its average launch duration, measured with
+HIP events recorded on the stream the graphs replay on.  The CPU baseline is
+the float64 oracle on this host, on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def _parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-steps", type=int, default=2,
+                    help="decode every n-th step in the CPU-baseline sample")
+    return ap.parse_args()
+
+
+def _decode_bytes(Hq, Hkv, d, n_rows, esz=2):
+    """Algorithmic HBM bytes of one decode launch over n_rows cached rows."""
+    return (2 * Hkv * n_rows * d + 2 * Hq * d + 2 * Hkv * d) * esz
+
+
+def _evict_bytes(Hq, Hkv, d, L, w, n_keep, esz=2):
+    score = Hkv * L * d * esz + Hq * w * d * esz + Hkv * (L - w) * 4
+    select = Hkv * (L - w) * 4 + Hkv * n_keep * 4
+    compact = 2 * 2 * Hkv * n_keep * d * esz + Hkv * n_keep * 4
+    return score + select + compact
+
+
+def cpu_baseline(wl, pr, dc, every):
+    """The float64 oracle on this host: eviction + every n-th decode step per alpha."""
+    import numpy as np
+    from oracle import timebill_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:       # pragma: no cover - reporting only
+        threads = len(os.sched_getaffinity(0))
+    q64 = pr["q_win"][0].double().numpy()
+    k64 = pr["k"][0].double().numpy()
+    v64 = pr["v"][0].double().numpy()
+    qs = dc["q"][:, 0].double().numpy()
+    kn = dc["k_new"][:, 0].double().numpy()
+    vn = dc["v_new"][:, 0].double().numpy()
+    t_total = 0.0
+    tokens = 0
+    t0 = time.perf_counter()
+    for a in wl.alphas:
+        te = time.perf_counter()
+        r = O.evict_sequence(q64, k64, v64, wl.L, wl.w, wl.pool, a)
+        t_ev = time.perf_counter() - te
+        steps = list(range(0, wl.T, every))
+        td = time.perf_counter()
+        O.decode_sequence(qs, kn, vn, r["k_cache"], r["v_cache"], steps=steps)
+        t_dec = (time.perf_counter() - td) * wl.T / len(steps)   # extrapolated to all steps
+        t_total += t_ev + t_dec
+        tokens += wl.T
+    wall = time.perf_counter() - t0
+    return {"value": tokens / t_total, "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": (f"float64 numpy oracle on the host: full eviction at each of the "
+                       f"{len(wl.alphas)} ratios plus every {every}-th of the {wl.T} decode steps, "
+                       f"decode time scaled to all steps; {wall:.1f} s of CPU work")}
+
+
+def main():
+    args = _parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not "
+              f"supported (the path shards by sequence / KV head with no exchange).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2512_21859_amd import _lib, synth
+    from paper_2512_21859_amd.pipeline import Evictor
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    _lib.load()
+    wl = synth.WORKLOADS[2]
+    B, Hq, Hkv, d, w, L, T = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L, wl.T
+    pr = synth.make_prompt(wl)
+    dc = synth.make_decode(wl)
+    q_win, k, v = (pr[x].to(dev) for x in ("q_win", "k", "v"))
+    qd, knd, vnd = (dc[x].to(dev) for x in ("q", "k_new", "v_new"))
+
+    ev = Evictor(B, L, Hq, Hkv, d, w, wl.pool, device=dev)
+    stream = torch.cuda.current_stream()
+    n_keep = {a: _lib.tb_keep_count(L, a, w) for a in wl.alphas}
+    caches = {a: _lib.KVCache(B, Hq, Hkv, n_keep[a] + T, d, wl.dtype, device=dev)
+              for a in wl.alphas}
+    outs = {a: torch.empty((T, B, Hq, d), dtype=wl.dtype, device=dev) for a in wl.alphas}
+
+    def evict(a):
+        ev.evict(q_win, k, v, [L], [a], caches[a], stream)
+
+    # One graph per ratio with the T decode launches (lengths live on the device).
+    graphs = {}
+    cap_stream = torch.cuda.Stream()
+    for a in wl.alphas:
+        evict(a)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        c = caches[a]
+        with torch.cuda.graph(g, stream=cap_stream):
+            for t in range(T):
+                _lib.tb_decode_attn(qd[t], knd[t], vnd[t], c.k, c.v, c.kv_len, outs[a][t],
+                                    c.ws, stream=cap_stream)
+        graphs[a] = g
+    torch.cuda.synchronize()
+
+    n_al = len(wl.alphas)
+
+    def step(evs=None):
+        for i, a in enumerate(wl.alphas):
+            if evs is not None:
+                evs[3 * i].record(stream)
+            evict(a)
+            if evs is not None:
+                evs[3 * i + 1].record(stream)
+            graphs[a].replay()
+            if evs is not None:
+                evs[3 * i + 2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3 * n_al)]
+              for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for s in range(args.steps):
+        step(events[s])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_end)
+
+    per_alpha = []
+    dec_bytes_total, dec_ms_total, launches = 0.0, 0.0, 0
+    for i, a in enumerate(wl.alphas):
+        ev_ms = [events[s][3 * i].elapsed_time(events[s][3 * i + 1]) for s in range(args.steps)]
+        de_ms = [events[s][3 * i + 1].elapsed_time(events[s][3 * i + 2]) for s in range(args.steps)]
+        ev_ms.sort()
+        de_ms.sort()
+        e_med, d_med = ev_ms[len(ev_ms) // 2], de_ms[len(de_ms) // 2]
+        nk = n_keep[a]
+        dbytes = sum(_decode_bytes(Hq, Hkv, d, nk + t + 1) for t in range(T))
+        ebytes = _evict_bytes(Hq, Hkv, d, L, w, nk)
+        dec_bytes_total += dbytes * args.steps
+        dec_ms_total += sum(de_ms)
+        launches += T * args.steps
+        per_alpha.append({
+            "alpha": a, "n_keep": nk,
+            "evict_us": round(e_med * 1e3, 2),
+            "decode_us_per_token": round(d_med * 1e3 / T, 3),
+            "decode_GBps": round(dbytes / (d_med * 1e-3) / 1e9, 1),
+            "evict_plus_decode_GBps": round((dbytes + ebytes) / ((d_med + e_med) * 1e-3) / 1e9, 1),
+            "tokens_per_s": round(T / ((d_med + e_med) * 1e-3), 1),
+        })
+    # decode time per token against retained length: least-squares line (Eq. decoding-step form)
+    xs = [p["n_keep"] + T / 2 for p in per_alpha]
+    ys = [p["decode_us_per_token"] for p in per_alpha]
+    mx, my = sum(xs) / len(xs), sum(ys) / len(ys)
+    sxx = sum((x - mx) ** 2 for x in xs)
+    slope = sum((x - mx) * (y - my) for x, y in zip(xs, ys)) / sxx
+    icpt = my - slope * mx
+    ss_res = sum((y - (icpt + slope * x)) ** 2 for x, y in zip(xs, ys))
+    ss_tot = sum((y - my) ** 2 for y in ys)
+
+    tokens = n_al * T * args.steps
+    value = tokens / (total_ms * 1e-3)
+    avg_launch_us = dec_ms_total * 1e3 / launches
+    achieved = dec_bytes_total / (dec_ms_total * 1e-3) / 1e9
+    result = {
+        "metric": "decode tokens/s and HBM GB/s (evict+decode attn) vs eviction ratio α, 1 GPU",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "single layer bf16, B=1, L=8192, 28 q / 4 kv heads, d=128, w=32, "
+                        "pool 7, alpha sweep 0/0.25/0.5/0.75/0.95, 256 decode steps each",
+            "B": B, "L": L, "Hq": Hq, "Hkv": Hkv, "d": d, "w": w, "pool": wl.pool,
+            "alphas": list(wl.alphas), "decode_steps": T,
+            "parallelism": "none (1 GPU)",
+        },
+        "roofline": {
+            "kernel": "decode_kernel (split-K GQA decode attention with append)",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "avg_launch_us": round(avg_launch_us, 3),
+            "bytes_per_launch": round(dec_bytes_total / launches),
+            "timing": "HIP events around each ratio's graph of decode launches, "
+                      "divided by the launch count (inter-kernel gaps included)",
+        },
+        "per_alpha": per_alpha,
+        "decode_time_fit": {"us_per_token_per_kv_row": slope, "intercept_us": icpt,
+                            "r2": 1 - ss_res / ss_tot if ss_tot > 0 else 1.0},
+        "wall_s": round(wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, pr, dc, args.cpu_sample_steps)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

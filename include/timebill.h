@@ -31,7 +31,10 @@
  *     k, v       [B][Hkv][Lmax][d] prompt keys / values; sequence b valid for j < L[b]
  *     scores     [B][Hkv][Lmax]    fp32; entries j >= L[b] - w are left untouched
  *     keep_idx   [B][Hkv][Lmax]    int32; the first n_keep[b] entries are valid
- *     k/v_cache  [B][Hkv][cap][d]  compact caches
+ *     k_cache    [B][Hkv][cap][d]  compact K cache, row-major
+ *     v_cache    [B][Hkv][cap/32][d][32]  compact V cache, transposed per tile
+ *                of 32 rows (element (j, e) at tile j/32, column e, slot j%32);
+ *                cap must be a multiple of 32
  *     kv_len     [B]               int32 current cache length per sequence (device)
  *     q, out     [B][Hq][d];  k_new, v_new [B][Hkv][d]
  *   Query head h uses KV head h / (Hq / Hkv).  The logit scale is 1/sqrt(d).
@@ -122,7 +125,9 @@ tb_status tb_select_topk(const float* scores, int32_t B, const int32_t* L,
 /* Compaction: k_cache[b][g][i] = k[b][g][keep_idx[b][g][i]] (same for v) for
  * i < n_keep[b]; the retained caches are what decoding uses (Sec. 5.2).
  * Sets kv_len[b] = n_keep[b] on the device (stream-ordered).
- * Requires 1 <= n_keep[b] <= min(Lmax, cap).  Indices should lie in
+ * V rows are written transposed into 32-row tiles; the slots of the last
+ * tile past n_keep[b] are zero-filled.
+ * Requires 1 <= n_keep[b] <= min(Lmax, cap), cap % 32 == 0.  Indices should lie in
  * [0, Lmax); the device clamps any other index into that range rather than
  * reading outside the prompt.  Caches must not alias k or v.
  * n_keep: [host][B].  ws: unused (may be NULL). */
@@ -139,11 +144,13 @@ tb_status tb_compact_kv(const void* k, const void* v, const int32_t* keep_idx,
  *   out[b][h] = sum_j softmax_j(q[b][h] . K[j] / sqrt(d)) V[j]
  * over the rows of KV head h / (Hq/Hkv).  fp32 accumulation; out in `dt`.
  * Lengths live only on the device, so the call can be captured in a HIP graph.
+ * bf16 uses the matrix cores (P rounded to bf16 for the PV product); fp32
+ * keeps fp32 products.  Requires cap % 32 == 0.
  * The library cannot see kv_len: the caller must keep kv_len[b] + 1 <= cap
  * when appending (an append that would overflow is dropped on the device).
- * ws: tb_workspace_bytes(TB_OP_DECODE, B, 0, Hq, Hkv, d, 0, cap) bytes, all
- * zero before the first call on it; every call leaves the workspace's
- * counters at zero again.  Calls sharing a workspace must not overlap. */
+ * Two kernels are enqueued (chunk partials, then their merge).
+ * ws: tb_workspace_bytes(TB_OP_DECODE, B, 0, Hq, Hkv, d, 0, cap) bytes (no
+ * initialisation needed).  Calls sharing a workspace must not overlap. */
 tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new,
                          void* k_cache, void* v_cache, int32_t* kv_len,
                          int32_t B, int32_t Hq, int32_t Hkv, int32_t d,

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libtimebill.so")
 TB_OK, TB_EINVAL, TB_EUNSUPPORTED, TB_EWORKSPACE, TB_EHIP, TB_EINTERNAL = range(6)
 TB_F32, TB_BF16 = 0, 1
 TB_OP_SCORE, TB_OP_SELECT, TB_OP_COMPACT, TB_OP_DECODE = range(4)
+V_TILE = 32          # the compact V cache is stored as transposed tiles of 32 rows
 
 EXPORTED = ("tb_keep_count", "tb_last_error", "tb_workspace_bytes", "tb_score_window",
             "tb_select_topk", "tb_compact_kv", "tb_decode_attn")
@@ -144,14 +145,36 @@ def tb_select_topk(scores: torch.Tensor, L: Sequence[int], w: int, alpha: Sequen
     return list(n_keep)
 
 
+def v_rows_to_tiles(v_rows: torch.Tensor) -> torch.Tensor:
+    """Layout helper: V rows [..., cap, d] -> V^T tiles [..., cap/32, d, 32]."""
+    *lead, cap, d = v_rows.shape
+    return v_rows.reshape(*lead, cap // V_TILE, V_TILE, d).transpose(-1, -2).contiguous()
+
+
+def v_tiles_to_rows(v_tiles: torch.Tensor) -> torch.Tensor:
+    """Layout helper: V^T tiles [..., cap/32, d, 32] -> V rows [..., cap, d]."""
+    *lead, nt, d, t = v_tiles.shape
+    return v_tiles.transpose(-1, -2).reshape(*lead, nt * t, d)
+
+
+def _check_caches(k_cache, v_cache, B, Hkv, d):
+    cap = k_cache.shape[2]
+    if tuple(k_cache.shape) != (B, Hkv, cap, d):
+        raise ValueError("k_cache must be [B, Hkv, cap, d]")
+    if cap % V_TILE or tuple(v_cache.shape) != (B, Hkv, cap // V_TILE, d, V_TILE):
+        raise ValueError("v_cache must be [B, Hkv, cap/32, d, 32] with cap a multiple of 32")
+    return cap
+
+
 def tb_compact_kv(k: torch.Tensor, v: torch.Tensor, keep_idx: torch.Tensor,
                   n_keep: Sequence[int], k_cache: torch.Tensor, v_cache: torch.Tensor,
                   kv_len: torch.Tensor, stream=None) -> None:
-    """k, v [B,Hkv,Lmax,d] -> caches [B,Hkv,cap,d]; kv_len [B] int32 set to n_keep."""
+    """k, v [B,Hkv,Lmax,d] -> k_cache [B,Hkv,cap,d], v_cache [B,Hkv,cap/32,d,32];
+    kv_len [B] int32 set to n_keep."""
     B, Hkv, Lmax, d = k.shape
-    cap = k_cache.shape[2]
-    if v.shape != k.shape or k_cache.shape != v_cache.shape or tuple(k_cache.shape) != (B, Hkv, cap, d):
-        raise ValueError("k/v or cache shapes disagree")
+    if v.shape != k.shape:
+        raise ValueError("k and v shapes disagree")
+    cap = _check_caches(k_cache, v_cache, B, Hkv, d)
     if k_cache.dtype != k.dtype or v_cache.dtype != k.dtype or v.dtype != k.dtype:
         raise TypeError("k, v and caches must share a dtype")
     _check(load().tb_compact_kv(
@@ -164,11 +187,12 @@ def tb_compact_kv(k: torch.Tensor, v: torch.Tensor, keep_idx: torch.Tensor,
 def tb_decode_attn(q: torch.Tensor, k_new: Optional[torch.Tensor], v_new: Optional[torch.Tensor],
                    k_cache: torch.Tensor, v_cache: torch.Tensor, kv_len: torch.Tensor,
                    out: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
-    """q, out [B,Hq,d]; k_new, v_new [B,Hkv,d] or None; caches [B,Hkv,cap,d]."""
+    """q, out [B,Hq,d]; k_new, v_new [B,Hkv,d] or None; caches as in tb_compact_kv."""
     B, Hq, d = q.shape
-    _, Hkv, cap, d2 = k_cache.shape
-    if d2 != d or out.shape != q.shape or k_cache.shape != v_cache.shape:
-        raise ValueError("decode shapes disagree")
+    Hkv = k_cache.shape[1]
+    cap = _check_caches(k_cache, v_cache, B, Hkv, d)
+    if out.shape != q.shape:
+        raise ValueError("out must match q")
     for t, name in ((k_new, "k_new"), (v_new, "v_new")):
         if t is not None and tuple(t.shape) != (B, Hkv, d):
             raise ValueError(f"{name} must be [B, Hkv, d]")
@@ -185,14 +209,16 @@ class KVCache:
     """Compact caches of one layer plus the host-side lengths the library cannot see.
 
     Allocation happens here (torch device memory); every computation is a
-    call into the library.  ``decode`` refuses an append past ``cap``.
+    call into the library.  ``cap`` is rounded up to whole 32-row V^T tiles;
+    ``v`` holds V transposed per tile.  ``decode`` refuses an append past ``cap``.
     """
 
     def __init__(self, B: int, Hq: int, Hkv: int, cap: int, d: int, dtype: torch.dtype,
                  device="cuda"):
+        cap = -(-cap // V_TILE) * V_TILE          # whole V^T tiles
         self.B, self.Hq, self.Hkv, self.cap, self.d = B, Hq, Hkv, cap, d
         self.k = torch.empty((B, Hkv, cap, d), dtype=dtype, device=device)
-        self.v = torch.empty((B, Hkv, cap, d), dtype=dtype, device=device)
+        self.v = torch.empty((B, Hkv, cap // V_TILE, d, V_TILE), dtype=dtype, device=device)
         self.kv_len = torch.zeros((B,), dtype=torch.int32, device=device)
         nbytes = tb_workspace_bytes(TB_OP_DECODE, B, 0, Hq, Hkv, d, 0, cap)
         self.ws = torch.zeros((max(nbytes, 1),), dtype=torch.uint8, device=device)

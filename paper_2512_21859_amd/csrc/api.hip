@@ -61,26 +61,26 @@ tb_status check_common(int32_t B, int32_t Hq, int32_t Hkv, int32_t d, tb_dtype d
   return TB_OK;
 }
 
-size_t decode_ws(int32_t B, int32_t Hkv, int32_t G, int32_t d, int32_t cap) {
-  const int chunk = tb::decode_chunk_rows(B, Hkv, cap);
+size_t decode_ws(int32_t B, int32_t Hkv, int32_t G, int32_t d, int32_t cap, bool bf16) {
+  const int chunk = tb::decode_chunk_rows(B, Hkv, cap, bf16);
   const size_t n_chunks = (static_cast<size_t>(cap) + chunk - 1) / chunk;
-  const size_t part = static_cast<size_t>(B) * Hkv * n_chunks * G * (d + 2) * sizeof(float);
-  return align256(part) + align256(static_cast<size_t>(B) * Hkv * sizeof(int32_t)) +
-         align256(static_cast<size_t>(B) * sizeof(int32_t));
+  const size_t part = static_cast<size_t>(B) * Hkv * n_chunks * G * (d + 4) * sizeof(float);
+  return align256(part) + align256(static_cast<size_t>(B) * sizeof(int32_t));
 }
 
 }  // namespace
 
 namespace tb {
 
-// Rows per decode block: enough blocks to cover the chip (B*Hkv*chunks of a
-// few hundred or more) without making the chunk partials the dominant traffic.
-int decode_chunk_rows(int B, int Hkv, int cap) {
-  const int unit = decode_rows_per_chunk_unit();               // 64
+// Rows per decode block: about 512 blocks over the chip (two per CU at the
+// decode kernel's occupancy), at least one wave iteration per block, and few
+// enough chunks for the merge kernel's weight table.
+int decode_chunk_rows(int B, int Hkv, int cap, bool bf16) {
+  const long long unit = decode_chunk_unit(bf16);
   const long long units = static_cast<long long>(B) * Hkv;
-  long long want = (static_cast<long long>(cap) * units + 511) / 512;   // ~512 blocks
-  want = std::max<long long>(want, unit);
-  want = std::min<long long>(want, 1024);
+  long long want = (static_cast<long long>(cap) * units + 511) / 512;
+  want = std::min<long long>(std::max<long long>(want, unit), 1024);
+  want = std::max<long long>(want, (cap + decode_max_chunks() - 1) / decode_max_chunks());
   return static_cast<int>((want + unit - 1) / unit * unit);
 }
 
@@ -111,7 +111,9 @@ size_t tb_workspace_bytes(int32_t op, int32_t B, int32_t Lmax, int32_t Hq, int32
           fail(TB_EINVAL, "tb_workspace_bytes(DECODE): bad sizes");
           return 0;
         }
-        return decode_ws(B, Hkv, Hq / Hkv, d, cap);
+        // sized for the larger of the two dtype decompositions
+        return std::max(decode_ws(B, Hkv, Hq / Hkv, d, cap, true),
+                        decode_ws(B, Hkv, Hq / Hkv, d, cap, false));
       }
       default:
         fail(TB_EINVAL, "tb_workspace_bytes: unknown op %d", op);
@@ -209,6 +211,8 @@ tb_status tb_compact_kv(const void* k, const void* v, const int32_t* keep_idx, i
     tb_status st = check_common(B, Hkv, Hkv, d, dt);
     if (st != TB_OK) return st;
     if (Lmax < 1 || cap < 1) return fail(TB_EINVAL, "Lmax and cap must be >= 1");
+    if (cap % tb::kVTile != 0)
+      return fail(TB_EINVAL, "cap must be a multiple of %d (got %d)", tb::kVTile, cap);
     tb::CompactArgs a{};
     int max_keep = 0;
     for (int b = 0; b < B; ++b) {
@@ -241,24 +245,25 @@ tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new, vo
     const int G = Hq / Hkv;
     if (G > 8) return fail(TB_EUNSUPPORTED, "Hq/Hkv must be <= 8 for decoding (got %d)", G);
     if (cap < 1) return fail(TB_EINVAL, "cap must be >= 1");
-    const size_t need = decode_ws(B, Hkv, G, d, cap);
+    if (cap % tb::kVTile != 0)
+      return fail(TB_EINVAL, "cap must be a multiple of %d (got %d)", tb::kVTile, cap);
+    const bool bf16 = dt == TB_BF16;
+    const size_t need = decode_ws(B, Hkv, G, d, cap, bf16);
     if (ws_bytes < need)
       return fail(TB_EWORKSPACE, "tb_decode_attn: workspace %zu < %zu bytes", ws_bytes, need);
     tb::DecodeArgs a{};
     a.q = q; a.k_new = k_new; a.v_new = v_new; a.k_cache = k_cache; a.v_cache = v_cache;
     a.kv_len = kv_len; a.out = out;
     a.B = B; a.Hkv = Hkv; a.cap = cap;
-    a.chunk = tb::decode_chunk_rows(B, Hkv, cap);
+    a.chunk = tb::decode_chunk_rows(B, Hkv, cap, bf16);
     a.n_chunks = (cap + a.chunk - 1) / a.chunk;
     a.append = k_new != nullptr;
     a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(d)));
     char* p = static_cast<char*>(ws);
     a.part = reinterpret_cast<float*>(p);
-    p += align256(static_cast<size_t>(B) * Hkv * a.n_chunks * G * (d + 2) * sizeof(float));
-    a.head_ctr = reinterpret_cast<int32_t*>(p);
-    p += align256(static_cast<size_t>(B) * Hkv * sizeof(int32_t));
-    a.seq_ctr = reinterpret_cast<int32_t*>(p);
-    return hip_status(tb::launch_decode(a, G, d, dt == TB_BF16, stream), "tb_decode_attn launch");
+    p += align256(static_cast<size_t>(B) * Hkv * a.n_chunks * G * (d + 4) * sizeof(float));
+    a.seq_len = reinterpret_cast<int32_t*>(p);
+    return hip_status(tb::launch_decode(a, G, d, bf16, stream), "tb_decode_attn launch");
   } catch (...) {
     return fail(TB_EINTERNAL, "tb_decode_attn: internal error");
   }

@@ -1,11 +1,14 @@
 // Gather of the kept K/V rows into the compact caches.
 //
-// grid = (ceil(max n_keep / rows_per_block), Hkv, B), block = 256 threads.
-// A row of d elements is split over d*elem/16 lanes, 16 bytes each, so each
-// wave instruction moves whole contiguous rows; every thread issues all of its
-// K and V loads before its stores to keep many requests in flight.  The
-// kernel is pure data movement: HBM traffic is one read and one write of each
-// kept row of K and V.
+// grid = (ceil(max n_keep / 32), Hkv, B), block = 256 threads; block t fills
+// destination rows [32t, 32t + 32) of one (sequence, KV head):
+//   K rows are copied row-major: each row is split into 16-byte pieces, one
+//     per lane, so a wave instruction moves whole contiguous rows;
+//   V rows are gathered into LDS, then written as one transposed 32-row tile
+//     [d][32] (contiguous 16-byte stores of 8 (bf16) or 4 (fp32) keys of one
+//     column); slots past n_keep are zero-filled.
+// All loads of a thread are issued before its stores.  HBM traffic is one read
+// and one write of each kept row of K and V.
 
 #include "common.h"
 #include "kernels.h"
@@ -14,16 +17,21 @@ namespace tb {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kVT = kVTile;
 
-template <int ROW_BYTES, int RPB>
+template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
-  constexpr int LPR = ROW_BYTES / 16;              // lanes per row
+  constexpr int ROW_BYTES = D * sizeof(T);
+  constexpr int LPR = ROW_BYTES / 16;                 // lanes per row
   constexpr int ROWS_PER_PASS = kThreads / LPR;
-  constexpr int PASSES = RPB / ROWS_PER_PASS;
-  const int g = blockIdx.y, b = blockIdx.z;
+  constexpr int PASSES = kVT / ROWS_PER_PASS;
+  constexpr int EPV = 16 / sizeof(T);                 // elements per 16 bytes
+  constexpr int TILE_VECS = D * kVT / EPV;            // 16-byte pieces per V^T tile
+  static_assert(PASSES >= 1 && TILE_VECS % kThreads == 0, "tile shape");
+  const int tile = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int n = a.n_keep[b];
-  const int i0 = blockIdx.x * RPB;
-  if (blockIdx.x == 0 && g == 0 && threadIdx.x == 0) a.kv_len[b] = n;
+  const int i0 = tile * kVT;
+  if (tile == 0 && g == 0 && threadIdx.x == 0) a.kv_len[b] = n;
   if (i0 >= n) return;
   const int part = threadIdx.x % LPR, r0 = threadIdx.x / LPR;
   const size_t bg = static_cast<size_t>(b) * a.Hkv + g;
@@ -31,11 +39,16 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   const char* ks = static_cast<const char*>(a.k) + bg * a.Lmax * ROW_BYTES + part * 16;
   const char* vs = static_cast<const char*>(a.v) + bg * a.Lmax * ROW_BYTES + part * 16;
   char* kd = static_cast<char*>(a.k_cache) + bg * a.cap * ROW_BYTES + part * 16;
-  char* vd = static_cast<char*>(a.v_cache) + bg * a.cap * ROW_BYTES + part * 16;
+  T* vtile = static_cast<T*>(a.v_cache) + bg * a.cap * D + static_cast<size_t>(tile) * D * kVT;
+
+  __shared__ T s_v[kVT][D + EPV];                     // padded rows
+
   uint4 kr[PASSES], vr[PASSES];
 #pragma unroll
   for (int p = 0; p < PASSES; ++p) {
     const int i = i0 + r0 + p * ROWS_PER_PASS;
+    kr[p] = make_uint4(0u, 0u, 0u, 0u);
+    vr[p] = make_uint4(0u, 0u, 0u, 0u);
     if (i < n) {
       // indices are clamped into the prompt so a bad index cannot fault
       const int j = min(max(keep[i], 0), a.Lmax - 1);
@@ -46,20 +59,27 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   }
 #pragma unroll
   for (int p = 0; p < PASSES; ++p) {
-    const int i = i0 + r0 + p * ROWS_PER_PASS;
-    if (i < n) {
-      const size_t dst = static_cast<size_t>(i) * ROW_BYTES;
-      stg16(kd + dst, kr[p]);
-      stg16(vd + dst, vr[p]);
-    }
+    const int rr = r0 + p * ROWS_PER_PASS;
+    if (i0 + rr < n) stg16(kd + static_cast<size_t>(i0 + rr) * ROW_BYTES, kr[p]);
+    *reinterpret_cast<uint4*>(&s_v[rr][part * EPV]) = vr[p];   // zero past n_keep
+  }
+  __syncthreads();
+  // V^T tile: piece v covers column d = v / (32/EPV), keys (v % (32/EPV))*EPV ..
+#pragma unroll
+  for (int v = threadIdx.x; v < TILE_VECS; v += kThreads) {
+    const int d = v / (kVT / EPV), k0 = (v % (kVT / EPV)) * EPV;
+    T vals[EPV];
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) vals[e] = s_v[k0 + e][d];
+    *reinterpret_cast<uint4*>(vtile + static_cast<size_t>(d) * kVT + k0) =
+        *reinterpret_cast<const uint4*>(vals);
   }
 }
 
-template <int ROW_BYTES>
-hipError_t launch_rb(const CompactArgs& a, int max_keep, hipStream_t st) {
-  constexpr int RPB = 64;
-  const dim3 grid((max_keep + RPB - 1) / RPB, a.Hkv, a.B);
-  compact_kernel<ROW_BYTES, RPB><<<grid, kThreads, 0, st>>>(a);
+template <typename T, int D>
+hipError_t launch_t(const CompactArgs& a, int max_keep, hipStream_t st) {
+  const dim3 grid((max_keep + kVT - 1) / kVT, a.Hkv, a.B);
+  compact_kernel<T, D><<<grid, kThreads, 0, st>>>(a);
   return hipGetLastError();
 }
 
@@ -67,12 +87,9 @@ hipError_t launch_rb(const CompactArgs& a, int max_keep, hipStream_t st) {
 
 hipError_t launch_compact(const CompactArgs& a, int d, int elem_bytes, int max_keep,
                           hipStream_t st) {
-  switch (d * elem_bytes) {
-    case 128: return launch_rb<128>(a, max_keep, st);
-    case 256: return launch_rb<256>(a, max_keep, st);
-    case 512: return launch_rb<512>(a, max_keep, st);
-    default: return hipErrorInvalidValue;
-  }
+  if (elem_bytes == 2) return d == 128 ? launch_t<uint16_t, 128>(a, max_keep, st)
+                                       : launch_t<uint16_t, 64>(a, max_keep, st);
+  return d == 128 ? launch_t<float, 128>(a, max_keep, st) : launch_t<float, 64>(a, max_keep, st);
 }
 
 }  // namespace tb

@@ -1,23 +1,33 @@
 // Single-token grouped-query decode attention over the compact KV cache,
-// with the new token's K/V appended in the same launch.
+// with the new token's K/V appended in the same step.
 //
-// Work decomposition (one launch per decode step and layer):
-//   grid  = (n_chunks, Hkv, B), block = 256 threads (4 waves).
-//   Block (c, g, b) handles key rows [c*chunk, (c+1)*chunk) of KV head g of
-//   sequence b for all G = Hq/Hkv query heads of that group, so every K/V
-//   byte is read from HBM exactly once per step.
-//   Inside a wave, a 16-lane row group owns one key row at a time; each lane
-//   holds d/16 consecutive elements (16 bytes for bf16 d=128 and fp32 d=64),
-//   so a wave instruction reads 4 whole rows.  Dot products are reduced over
-//   the 16 lanes with DPP (fixed order); the softmax is online (running max
-//   and sum per head) in the exp2 domain, with q pre-scaled by log2(e)/sqrt(d).
-//   The four row groups and then the four waves are merged in a fixed order,
-//   giving one partial (m, l, o[G][d]) per block.
-//   The block that takes the last ticket of (b, g) merges the chunk partials
-//   in chunk order (log-sum-exp), writes out[b][g*G .. g*G+G-1] and re-arms
-//   its counter; the last head merger of sequence b then advances kv_len[b].
-// Lengths are read on the device only, so the launch is graph-capturable.
-// No floating-point atomics are used: results are bit-reproducible.
+// Cache layout: K rows are row-major [B][Hkv][cap][d]; V is stored
+// transposed in tiles of 32 rows, [B][Hkv][cap/32][d][32], so that the
+// matrix-core operand "8 consecutive keys of one V column" is one contiguous
+// 16-byte load.
+//
+// Two launches per decode step and layer (both capturable in a HIP graph):
+//   partial kernel, grid = (n_chunks, Hkv, B): block (c, g, b) covers key
+//     rows [c*chunk, (c+1)*chunk) of KV head g of sequence b for all
+//     G = Hq/Hkv query heads of the group, so every K/V byte is read from HBM
+//     once per step, and writes one partial (m, l, o[G][d]).
+//   merge kernel, grid = (Hq, B): combines a query head's chunk partials by
+//     log-sum-exp in a fixed order, writes the output; the block of query
+//     head 0 advances kv_len[b].
+// bf16 runs on the matrix cores (v_mfma_f32_16x16x32_bf16), one wave per
+// 32-key block at a time:
+//   S^T[32 keys x 16 heads] = K[32 x d] . Q^T[d x 16]   (heads padded to 16)
+//   O^T[d x 16 heads]      += V^T[d x 32] . P^T[32 x 16]
+// The K tile rows are permuted so that lane group q of the S^T result holds
+// keys 8q..8q+7 of the block, exactly the k-slots the P^T operand needs: the
+// softmax and the bf16 packing of P stay in the lane, and the per-head
+// rescale of O^T is lane-local too (head = lane % 16 in both layouts).
+// fp32 inputs keep fp32 arithmetic on the vector ALUs (16 lanes per key row,
+// DPP row reductions).
+// The appended row is read from k_new/v_new by the block that owns it (and
+// stored into the caches there), so no block reads a row written in the same
+// launch.  Lengths are read on the device only.  No atomics; every reduction
+// has a fixed order, so results are bit-reproducible.
 
 #include "common.h"
 #include "kernels.h"
@@ -25,76 +35,253 @@
 namespace tb {
 namespace {
 
-template <int WORDS>
-struct Raw {
-  uint32_t w[WORDS];
-};
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
-template <int WORDS>
-__device__ __forceinline__ Raw<WORDS> ld_raw(const void* p) {
-  Raw<WORDS> r;
-  if constexpr (WORDS == 2) {
-    const uint2 v = *reinterpret_cast<const uint2*>(p);
-    r.w[0] = v.x; r.w[1] = v.y;
-  } else {
+constexpr int kVT = kVTile;           // rows per V^T tile (32)
+
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// --------------------------------------------------------------------------
+// bf16: matrix-core partial kernel.
+// --------------------------------------------------------------------------
+template <int D, int G, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, 2) void decode_mfma_kernel(DecodeArgs a) {
+  static_assert(G >= 1 && G <= 16, "query heads per KV head must fit 16 columns");
+  constexpr int KC = D / 32;            // k-chunks of the QK^T product
+  constexpr int NC = D / 16;            // d-blocks of the PV product
+  const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);    // wave-uniform
+  const int q4 = lane >> 4, r16 = lane & 15;
+  const int Hkv = a.Hkv, Hq = Hkv * G;
+
+  __shared__ float4 s_o[WAVES][G][D / 4 + 1];     // +1: spreads heads over banks
+  __shared__ float s_ml[WAVES][16][2];
+
+  const size_t bg = static_cast<size_t>(b) * Hkv + g;
+  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache) + bg * a.cap * D;
+  const uint16_t* vt = static_cast<const uint16_t*>(a.v_cache) + bg * a.cap * D;
+  const uint16_t* kn = static_cast<const uint16_t*>(a.k_new) + bg * D;
+  const uint16_t* vn = static_cast<const uint16_t*>(a.v_new) + bg * D;
+  const int cap = a.cap;
+  const int lo = c * a.chunk;
+  const int per_wave = a.chunk / WAVES;          // multiple of 32
+  const int wlo = lo + wave * per_wave;
+  const int wend = min(wlo + per_wave, cap);     // static bound: no length needed
+  // K tile row permutation: MFMA row r of tile t <-> key 8*(r/4) + 4*t + r%4.
+  const int krow0 = 8 * (r16 >> 2) + (r16 & 3);
+
+  // Everything below up to the length check is issued without waiting for
+  // kv_len: the first block's K/V loads only need rows < cap, so the length
+  // load and the data loads are in flight together.
+  u32x4 kr[2][KC], vr[NC];
+  auto load_block = [&](int base) {
 #pragma unroll
-    for (int i = 0; i < WORDS / 4; ++i) {
-      const uint4 v = reinterpret_cast<const uint4*>(p)[i];
-      r.w[4 * i] = v.x; r.w[4 * i + 1] = v.y; r.w[4 * i + 2] = v.z; r.w[4 * i + 3] = v.w;
+    for (int t = 0; t < 2; ++t) {
+      const int key = base + krow0 + 4 * t;
+      const uint16_t* src = kc + static_cast<size_t>(min(key, cap - 1)) * D;
+#pragma unroll
+      for (int k = 0; k < KC; ++k) kr[t][k] = ld16(src + 32 * k + 8 * q4);
+    }
+    const uint16_t* vtile = vt + static_cast<size_t>(base / kVT) * D * kVT;
+#pragma unroll
+    for (int n = 0; n < NC; ++n) vr[n] = ld16(vtile + (16 * n + r16) * kVT + 8 * q4);
+  };
+  int n0 = a.kv_len[b];
+  if (wlo < wend) load_block(wlo);
+
+  // Q^T operand: lane holds head r16, d = 32*kc + 8*q4 .. +8 (zero past G).
+  bf16x8 qB[KC];
+  {
+    const uint16_t* qh = static_cast<const uint16_t*>(a.q) + (static_cast<size_t>(b) * Hq + g * G) * D;
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      // unconditional load of a valid head, zeroed past G
+      u32x4 v = ld16(qh + min(r16, G - 1) * D + 32 * k + 8 * q4);
+      if (r16 >= G) v = u32x4{0u, 0u, 0u, 0u};
+      qB[k] = as_bf16x8(v);
     }
   }
-  return r;
-}
-
-template <int WORDS>
-__device__ __forceinline__ void st_raw(void* p, const Raw<WORDS>& r) {
-  if constexpr (WORDS == 2) {
-    *reinterpret_cast<uint2*>(p) = make_uint2(r.w[0], r.w[1]);
-  } else {
+  // the appended row, as the lanes use it: K slices and the V^T column values
+  u32x4 knew[KC];
+  uint16_t vnew[NC];
+  if (a.append) {
 #pragma unroll
-    for (int i = 0; i < WORDS / 4; ++i)
-      reinterpret_cast<uint4*>(p)[i] =
-          make_uint4(r.w[4 * i], r.w[4 * i + 1], r.w[4 * i + 2], r.w[4 * i + 3]);
+    for (int k = 0; k < KC; ++k) knew[k] = ld16(kn + 32 * k + 8 * q4);
+#pragma unroll
+    for (int n = 0; n < NC; ++n) vnew[n] = vn[16 * n + r16];
   }
-}
 
-template <typename T, int WORDS>
-__device__ __forceinline__ void widen(const Raw<WORDS>& r, float* out) {
-  if constexpr (sizeof(T) == 2) {
+  n0 = n0 < 0 ? 0 : (n0 > cap ? cap : n0);
+  const int app = (a.append && n0 < cap) ? 1 : 0;
+  const int N = n0 + app;
+  const int hi = min(lo + a.chunk, N);
+  const int whi = min(wend, N);
+
+  // The block owning row n0 stores the appended row (K row, V^T column) from
+  // the registers that already hold it: no reload, nothing waits on it.
+  if (app && n0 >= lo && n0 < hi && wave == 0) {
+    if (r16 == 0) {
+      uint16_t* kd = static_cast<uint16_t*>(a.k_cache) + (bg * cap + n0) * D;
 #pragma unroll
-    for (int i = 0; i < WORDS; ++i) {
-      out[2 * i] = __uint_as_float(r.w[i] << 16);
-      out[2 * i + 1] = __uint_as_float(r.w[i] & 0xffff0000u);
+      for (int k = 0; k < KC; ++k) *reinterpret_cast<u32x4*>(kd + 32 * k + 8 * q4) = knew[k];
     }
-  } else {
+    if (q4 == 0) {
+      uint16_t* vd = static_cast<uint16_t*>(a.v_cache) + bg * cap * D +
+                     static_cast<size_t>(n0 / kVT) * D * kVT + (n0 % kVT);
 #pragma unroll
-    for (int i = 0; i < WORDS; ++i) out[i] = __uint_as_float(r.w[i]);
+      for (int n = 0; n < NC; ++n) vd[(16 * n + r16) * kVT] = vnew[n];
+    }
   }
+
+  f32x4 accO[NC];
+#pragma unroll
+  for (int n = 0; n < NC; ++n) accO[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY;   // running max of head r16 (same in the 4 lane groups)
+  float l_part = 0.f;        // this lane's share of the running sum of head r16
+
+  for (int base = wlo; base < whi; base += kVT) {
+    u32x4 ck[2][KC], cv[NC];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int k = 0; k < KC; ++k) ck[t][k] = kr[t][k];
+#pragma unroll
+    for (int n = 0; n < NC; ++n) cv[n] = vr[n];
+    if (base + kVT < whi) load_block(base + kVT);     // prefetch the next block
+
+    // wave-uniform: does this block hold the appended row, or run past the end?
+    const bool has_new = app && n0 >= base && n0 < base + kVT;
+    const bool tail = base + kVT > whi;
+    // ---- the appended row's K slices replace the (stale) cache rows
+    if (has_new) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const bool hit = base + krow0 + 4 * t == n0;
+#pragma unroll
+        for (int k = 0; k < KC; ++k) ck[t][k] = hit ? knew[k] : ck[t][k];
+      }
+    }
+    // ---- S^T = K Q^T: lane holds keys base + 8*q4 + 4*t + i, head r16
+    f32x4 S[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < KC; ++k)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ck[t][k]), qB[k], acc, 0, 0, 0);
+      S[t] = acc;
+    }
+    float s[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s[j] = S[j >> 2][j & 3] * a.scale_log2;
+    if (tail) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (base + 8 * q4 + j >= whi) s[j] = -INFINITY;
+    }
+    float mt = s[0];
+#pragma unroll
+    for (int j = 1; j < 8; ++j) mt = fmaxf(mt, s[j]);
+    mt = fmaxf(mt, __shfl_xor(mt, 16));
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    const float m_new = fmaxf(m_run, mt);
+    // m_new is finite: every block has at least one valid key (base < whi)
+    const float corr = exp2f(m_run - m_new);
+    m_run = m_new;
+    float p[8];
+    float psum = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) { p[j] = exp2f(s[j] - m_new); psum += p[j]; }
+    l_part = l_part * corr + psum;
+    bf16x8 pB;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) pB[j] = static_cast<__bf16>(p[j]);
+
+    // ---- V^T operand: zero keys past the end, patch the appended row
+    // (branch-free word masks over this lane's 8 keys)
+    if (tail || has_new) {
+      const int kq = base + 8 * q4;               // first key of this lane's 8
+      const int cnt = min(max(whi - kq, 0), 8);   // valid keys among the 8
+      const int pos = n0 - kq;                    // slot of the appended row
+      const bool inr = app && pos >= 0 && pos < cnt;
+      const int pw = pos >> 1;
+      const uint32_t sh = (pos & 1) * 16u;
+#pragma unroll
+      for (int n = 0; n < NC; ++n) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t keep = cnt >= 2 * w + 2 ? 0xffffffffu : (cnt == 2 * w + 1 ? 0xffffu : 0u);
+          uint32_t x = cv[n][w] & keep;
+          const uint32_t patched = (x & ~(0xffffu << sh)) | (static_cast<uint32_t>(vnew[n]) << sh);
+          cv[n][w] = (inr && w == pw) ? patched : x;
+        }
+      }
+    }
+#pragma unroll
+    for (int n = 0; n < NC; ++n) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) accO[n][i] *= corr;
+      accO[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(cv[n]), pB, accO[n], 0, 0, 0);
+    }
+  }
+
+  // ---- merge the lane groups' sums, then the waves, into this block's partial
+  float l_tot = l_part + __shfl_xor(l_part, 16);
+  l_tot += __shfl_xor(l_tot, 32);
+  if (r16 < G) {
+#pragma unroll
+    for (int n = 0; n < NC; ++n)
+      s_o[wave][r16][4 * n + q4] = make_float4(accO[n][0], accO[n][1], accO[n][2], accO[n][3]);
+  }
+  if (q4 == 0) { s_ml[wave][r16][0] = m_run; s_ml[wave][r16][1] = l_tot; }
+  __syncthreads();
+
+  float* part = a.part + (bg * a.n_chunks + c) * G * (D + 4);
+  for (int idx = tid; idx < G * (D / 4); idx += 64 * WAVES) {
+    const int h = idx / (D / 4), e4 = idx % (D / 4);
+    float M = -INFINITY;
+#pragma unroll
+    for (int wv = 0; wv < WAVES; ++wv) M = fmaxf(M, s_ml[wv][h][0]);
+    float L = 0.f;
+    float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int wv = 0; wv < WAVES; ++wv) {
+        const float sc = exp2f(s_ml[wv][h][0] - M);
+        const float4 x = s_o[wv][h][e4];
+        L += s_ml[wv][h][1] * sc;
+        O.x += x.x * sc; O.y += x.y * sc; O.z += x.z * sc; O.w += x.w * sc;
+      }
+    }
+    *reinterpret_cast<float4*>(part + h * (D + 4) + 4 * e4) = O;
+    if (e4 == 0) *reinterpret_cast<float2*>(part + h * (D + 4) + D) = make_float2(M, L);
+  }
+  if (c == 0 && g == 0 && tid == 0) a.seq_len[b] = N;
 }
 
-__device__ __forceinline__ float exp2_guarded(float x) {
-  // exp2(-inf) = 0 is what we want; the only guard needed is against
-  // (-inf) - (-inf), which callers avoid by checking the running max.
-  return exp2f(x);
-}
-
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / 64;
-constexpr int kUnroll = 4;                  // rows per row group per iteration
+// --------------------------------------------------------------------------
+// fp32: vector-ALU partial kernel (keeps fp32 products; no narrowing).
+// --------------------------------------------------------------------------
+constexpr int kValuThreads = 256;
+constexpr int kValuWaves = kValuThreads / 64;
+constexpr int kUnroll = 4;                  // rows per 16-lane row group per iteration
 constexpr int kRowsPerIter = 4 * kUnroll;   // rows per wave per iteration
 
-template <typename T, int D, int G>
-__global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
+template <int D, int G>
+__global__ __launch_bounds__(kValuThreads) void decode_valu_kernel(DecodeArgs a) {
   constexpr int DPL = D / 16;                     // elements per lane
-  constexpr int WORDS = DPL * sizeof(T) / 4;      // 32-bit words per lane
   const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int grp = lane >> 4, sub = lane & 15;
   const int Hkv = a.Hkv, Hq = Hkv * G;
 
-  __shared__ float s_o[kWaves][G][D];
-  __shared__ float s_ml[kWaves][G][2];
-  __shared__ int s_last;
+  __shared__ float s_o[kValuWaves][G][D];
+  __shared__ float s_ml[kValuWaves][G][2];
 
   int n0 = a.kv_len[b];
   n0 = n0 < 0 ? 0 : (n0 > a.cap ? a.cap : n0);
@@ -103,33 +290,39 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
   const int lo = c * a.chunk;
   const int hi = min(lo + a.chunk, N);
 
-  const size_t head_off = (static_cast<size_t>(b) * Hkv + g) * a.cap;
-  const T* kc = static_cast<const T*>(a.k_cache) + head_off * D;
-  const T* vc = static_cast<const T*>(a.v_cache) + head_off * D;
-  const T* kn = static_cast<const T*>(a.k_new) + (static_cast<size_t>(b) * Hkv + g) * D;
-  const T* vn = static_cast<const T*>(a.v_new) + (static_cast<size_t>(b) * Hkv + g) * D;
+  const size_t bg = static_cast<size_t>(b) * Hkv + g;
+  const float* kc = static_cast<const float*>(a.k_cache) + bg * a.cap * D;
+  const float* vt = static_cast<const float*>(a.v_cache) + bg * a.cap * D;
+  const float* kn = static_cast<const float*>(a.k_new) + bg * D;
+  const float* vn = static_cast<const float*>(a.v_new) + bg * D;
 
-  // The block whose chunk holds row n0 stores the appended row.  No other
-  // block of this launch reads that row from the cache.
-  if (app && n0 >= lo && n0 < hi && wave == 0 && grp == 0) {
-    st_raw<WORDS>(static_cast<T*>(a.k_cache) + (head_off + n0) * D + sub * DPL,
-                  ld_raw<WORDS>(kn + sub * DPL));
-    st_raw<WORDS>(static_cast<T*>(a.v_cache) + (head_off + n0) * D + sub * DPL,
-                  ld_raw<WORDS>(vn + sub * DPL));
-  }
-
-  // q slice of every head of the group, pre-scaled into the exp2 domain.
-  float qf[G][DPL];
-  {
-    const T* qb = static_cast<const T*>(a.q) + (static_cast<size_t>(b) * Hq + g * G) * D;
+  if (app && n0 >= lo && n0 < hi && wave == 0) {
+    float* kd = static_cast<float*>(a.k_cache) + (bg * a.cap + n0) * D;
+    float* vd = static_cast<float*>(a.v_cache) + bg * a.cap * D +
+                static_cast<size_t>(n0 / kVT) * D * kVT + (n0 % kVT);
+    constexpr int PER = (D + 63) / 64;
+    float kx[PER], vx[PER];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      widen<T, WORDS>(ld_raw<WORDS>(qb + h * D + sub * DPL), qf[h]);
+    for (int i = 0; i < PER; ++i) {
+      const int e = lane + 64 * i;
+      kx[i] = e < D ? kn[e] : 0.f;
+      vx[i] = e < D ? vn[e] : 0.f;
+    }
 #pragma unroll
-      for (int e = 0; e < DPL; ++e) qf[h][e] *= a.scale_log2;
+    for (int i = 0; i < PER; ++i) {
+      const int e = lane + 64 * i;
+      if (e < D) { kd[e] = kx[i]; vd[e * kVT] = vx[i]; }
     }
   }
 
+  float qf[G][DPL];
+  {
+    const float* qb = static_cast<const float*>(a.q) + (static_cast<size_t>(b) * Hq + g * G) * D;
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) qf[h][e] = qb[h * D + sub * DPL + e] * a.scale_log2;
+  }
   float m[G], l[G], o[G][DPL];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
@@ -138,53 +331,47 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
     for (int e = 0; e < DPL; ++e) o[h][e] = 0.f;
   }
 
-  const int per_wave = a.chunk / kWaves;
+  const int per_wave = a.chunk / kValuWaves;
   const int wlo = lo + wave * per_wave;
   const int whi = min(wlo + per_wave, hi);
   for (int base = wlo; base < whi; base += kRowsPerIter) {
-    Raw<WORDS> kr[kUnroll], vr[kUnroll];
+    float kf[kUnroll][DPL], vf[kUnroll][DPL];
     bool valid[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int row = base + u * 4 + grp;
       valid[u] = row < whi;
-      if (valid[u]) {
-        const bool is_new = app && row == n0;
-        kr[u] = ld_raw<WORDS>((is_new ? kn : kc + static_cast<size_t>(row) * D) + sub * DPL);
-        vr[u] = ld_raw<WORDS>((is_new ? vn : vc + static_cast<size_t>(row) * D) + sub * DPL);
-      } else {
+      const bool is_new = app && row == n0;
+      const float* vcol = vt + static_cast<size_t>(row / kVT) * D * kVT + (row % kVT);
 #pragma unroll
-        for (int i = 0; i < WORDS; ++i) { kr[u].w[i] = 0u; vr[u].w[i] = 0u; }
+      for (int e = 0; e < DPL; ++e) {
+        const int d = sub * DPL + e;
+        kf[u][e] = valid[u] ? (is_new ? kn[d] : kc[static_cast<size_t>(row) * D + d]) : 0.f;
+        vf[u][e] = valid[u] ? (is_new ? vn[d] : vcol[d * kVT]) : 0.f;
       }
     }
     float s[kUnroll][G];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      float kf[DPL];
-      widen<T, WORDS>(kr[u], kf);
+    for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
       for (int h = 0; h < G; ++h) {
         float acc = 0.f;
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) acc = fmaf(qf[h][e], kf[e], acc);
+        for (int e = 0; e < DPL; ++e) acc = fmaf(qf[h][e], kf[u][e], acc);
         acc = row16_sum(acc);
         s[u][h] = valid[u] ? acc : -INFINITY;
       }
-    }
-    float vf[kUnroll][DPL];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) widen<T, WORDS>(vr[u], vf[u]);
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       float mx = m[h];
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) mx = fmaxf(mx, s[u][h]);
-      if (mx == -INFINITY) continue;               // nothing valid yet
-      const float corr = exp2_guarded(m[h] - mx);  // m = -inf gives 0
+      if (mx == -INFINITY) continue;
+      const float corr = exp2f(m[h] - mx);
       float p[kUnroll];
       float psum = 0.f;
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) { p[u] = exp2_guarded(s[u][h] - mx); psum += p[u]; }
+      for (int u = 0; u < kUnroll; ++u) { p[u] = exp2f(s[u][h] - mx); psum += p[u]; }
       l[h] = l[h] * corr + psum;
 #pragma unroll
       for (int e = 0; e < DPL; ++e) {
@@ -197,12 +384,11 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
     }
   }
 
-  // Merge the four row groups of the wave (lanes sub, sub+16, sub+32, sub+48).
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     float M = fmaxf(m[h], __shfl_xor(m[h], 16));
     M = fmaxf(M, __shfl_xor(M, 32));
-    const float sc = (M == -INFINITY) ? 0.f : exp2_guarded(m[h] - M);
+    const float sc = (M == -INFINITY) ? 0.f : exp2f(m[h] - M);
     float lh = l[h] * sc;
     lh += __shfl_xor(lh, 16);
     lh += __shfl_xor(lh, 32);
@@ -226,85 +412,151 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
   }
   __syncthreads();
 
-  // Merge the waves in a fixed order and write this block's partial.
-  const size_t bg = static_cast<size_t>(b) * Hkv + g;
-  float* part = a.part + (bg * a.n_chunks + c) * (G * (D + 2));
-  for (int idx = tid; idx < G * D; idx += kThreads) {
+  float* part = a.part + (bg * a.n_chunks + c) * G * (D + 4);
+  for (int idx = tid; idx < G * D; idx += kValuThreads) {
     const int h = idx / D, e = idx % D;
     float M = -INFINITY;
 #pragma unroll
-    for (int wv = 0; wv < kWaves; ++wv) M = fmaxf(M, s_ml[wv][h][0]);
+    for (int wv = 0; wv < kValuWaves; ++wv) M = fmaxf(M, s_ml[wv][h][0]);
     float L = 0.f, O = 0.f;
     if (M != -INFINITY) {
 #pragma unroll
-      for (int wv = 0; wv < kWaves; ++wv) {
-        const float sc = exp2_guarded(s_ml[wv][h][0] - M);
+      for (int wv = 0; wv < kValuWaves; ++wv) {
+        const float sc = exp2f(s_ml[wv][h][0] - M);
         L += s_ml[wv][h][1] * sc;
         O += s_o[wv][h][e] * sc;
       }
     }
-    part[h * D + e] = O;
-    if (e == 0) { part[G * D + 2 * h] = M; part[G * D + 2 * h + 1] = L; }
+    part[h * (D + 4) + e] = O;
+    if (e == 0) { part[h * (D + 4) + D] = M; part[h * (D + 4) + D + 1] = L; }
   }
+  if (c == 0 && g == 0 && tid == 0) a.seq_len[b] = N;
+}
 
-  // Ticket: the last block of (b, g) merges the chunk partials.
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const int t = atomicAdd(a.head_ctr + bg, 1);
-    s_last = (t == a.n_chunks - 1);
+// --------------------------------------------------------------------------
+// Merge of the chunk partials of one query head.
+// grid = (Hq, B), block = 512 threads: thread (sp, e4) handles output
+// elements 4*e4 .. 4*e4+3 over the chunks c = sp, sp + S, ... (S = 512/(D/4)
+// interleaved splits).  Each thread issues all its partial loads before
+// combining them (online max per thread, then a fixed-order merge of the
+// splits in LDS).
+// --------------------------------------------------------------------------
+constexpr int kMergeThreads = 512;
+constexpr int kMaxPerThread = 16;      // chunk partials held in flight per thread
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeArgs a) {
+  constexpr int E4 = D / 4;
+  constexpr int S = kMergeThreads / E4;
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int Hkv = a.Hkv, Hq = Hkv * G;
+  const int g = h / G, hh = h % G;
+  const int tid = threadIdx.x, e4 = tid % E4, sp = tid / E4;
+  // Every chunk writes a partial (empty chunks carry m = -inf, l = 0), so the
+  // merge runs over all of them and never waits for the length; the length is
+  // only needed for the final kv_len store.
+  const int N = a.seq_len[b];
+  const int n_used = a.n_chunks;
+  const size_t bg = static_cast<size_t>(b) * Hkv + g;
+  const float* base = a.part + (bg * a.n_chunks * G + hh) * (D + 4);
+  constexpr size_t CSTRIDE = static_cast<size_t>(G) * (D + 4);
+
+  __shared__ float s_m[S], s_l[S];
+  __shared__ float4 s_o[S][E4];
+
+  float M = -INFINITY, L = 0.f;
+  float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int c0 = sp; c0 < n_used; c0 += S * kMaxPerThread) {
+    float mm[kMaxPerThread], ll[kMaxPerThread];
+    float4 oo[kMaxPerThread];
+    // unconditional loads (index clamped, value masked) so they issue back to back
+#pragma unroll
+    for (int k = 0; k < kMaxPerThread; ++k) {
+      const int cc = c0 + k * S;
+      const float* pc = base + min(cc, n_used - 1) * CSTRIDE;
+      const float2 ml = *reinterpret_cast<const float2*>(pc + D);
+      oo[k] = *reinterpret_cast<const float4*>(pc + 4 * e4);
+      mm[k] = cc < n_used ? ml.x : -INFINITY;
+      ll[k] = cc < n_used ? ml.y : 0.f;
+    }
+    // keep every load above this point: they must all be in flight together
+    __builtin_amdgcn_sched_barrier(0);
+    float mx = M;
+#pragma unroll
+    for (int k = 0; k < kMaxPerThread; ++k) mx = fmaxf(mx, mm[k]);
+    if (mx == -INFINITY) continue;
+    const float corr = exp2f(M - mx);
+    L *= corr; O.x *= corr; O.y *= corr; O.z *= corr; O.w *= corr;
+#pragma unroll
+    for (int k = 0; k < kMaxPerThread; ++k) {
+      const float wgt = exp2f(mm[k] - mx);
+      L += wgt * ll[k];
+      O.x += wgt * oo[k].x; O.y += wgt * oo[k].y; O.z += wgt * oo[k].z; O.w += wgt * oo[k].w;
+    }
+    M = mx;
   }
+  if (e4 == 0) { s_m[sp] = M; s_l[sp] = L; }
+  s_o[sp][e4] = O;
   __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-
-  const int n_used = (N + a.chunk - 1) / a.chunk;
-  const float* parts = a.part + bg * a.n_chunks * (G * (D + 2));
-  T* out = static_cast<T*>(a.out) + (static_cast<size_t>(b) * Hq + g * G) * D;
-  for (int idx = tid; idx < G * D; idx += kThreads) {
-    const int h = idx / D, e = idx % D;
-    float M = -INFINITY;
-    for (int cc = 0; cc < n_used; ++cc)
-      M = fmaxf(M, parts[cc * (G * (D + 2)) + G * D + 2 * h]);
-    float L = 0.f, O = 0.f;
-    if (M != -INFINITY) {
-      for (int cc = 0; cc < n_used; ++cc) {
-        const float* pc = parts + cc * (G * (D + 2));
-        const float mc = pc[G * D + 2 * h];
-        const float sc = exp2_guarded(mc - M);
-        L += pc[G * D + 2 * h + 1] * sc;
-        O += pc[h * D + e] * sc;
+  if (sp == 0) {
+    float Mg = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < S; ++q) Mg = fmaxf(Mg, s_m[q]);
+    float Lg = 0.f;
+    float4 Og = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (Mg != -INFINITY) {
+#pragma unroll
+      for (int q = 0; q < S; ++q) {
+        const float wgt = exp2f(s_m[q] - Mg);
+        const float4 x = s_o[q][e4];
+        Lg += wgt * s_l[q];
+        Og.x += wgt * x.x; Og.y += wgt * x.y; Og.z += wgt * x.z; Og.w += wgt * x.w;
       }
     }
-    Elem<T>::store1(out + h * D + e, L > 0.f ? O / L : 0.f);
-  }
-  __syncthreads();
-  if (tid == 0) {
-    a.head_ctr[bg] = 0;                 // re-arm for the next launch
-    __threadfence();
-    const int t = atomicAdd(a.seq_ctr + b, 1);
-    if (t == Hkv - 1) {                 // every head of b has read kv_len[b]
-      a.kv_len[b] = N;
-      a.seq_ctr[b] = 0;
+    const float inv = Lg > 0.f ? 1.f / Lg : 0.f;
+    T* out = static_cast<T*>(a.out) + (static_cast<size_t>(b) * Hq + h) * D + 4 * e4;
+    if constexpr (sizeof(T) == 2) {
+      typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+      const bf16x4 o4 = {static_cast<__bf16>(Og.x * inv), static_cast<__bf16>(Og.y * inv),
+                         static_cast<__bf16>(Og.z * inv), static_cast<__bf16>(Og.w * inv)};
+      *reinterpret_cast<bf16x4*>(out) = o4;
+    } else {
+      *reinterpret_cast<float4*>(out) = make_float4(Og.x * inv, Og.y * inv, Og.z * inv, Og.w * inv);
     }
   }
+  if (h == 0 && tid == 0) a.kv_len[b] = N;
+}
+
+constexpr int kMfmaWaves = 4;
+
+template <typename T, int D, int G>
+hipError_t launch_both(const DecodeArgs& a, hipStream_t st) {
+  const dim3 grid(a.n_chunks, a.Hkv, a.B);
+  if constexpr (sizeof(T) == 2) {
+    decode_mfma_kernel<D, G, kMfmaWaves><<<grid, 64 * kMfmaWaves, 0, st>>>(a);
+  } else {
+    decode_valu_kernel<D, G><<<grid, kValuThreads, 0, st>>>(a);
+  }
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  decode_merge_kernel<T, D, G><<<dim3(a.Hkv * G, a.B), kMergeThreads, 0, st>>>(a);
+  return hipGetLastError();
 }
 
 template <typename T, int D>
 hipError_t launch_g(const DecodeArgs& a, int G, hipStream_t st) {
-  const dim3 grid(a.n_chunks, a.Hkv, a.B);
   switch (G) {
-#define TB_CASE(GG) case GG: decode_kernel<T, D, GG><<<grid, kThreads, 0, st>>>(a); break;
+#define TB_CASE(GG) case GG: return launch_both<T, D, GG>(a, st);
     TB_CASE(1) TB_CASE(2) TB_CASE(3) TB_CASE(4) TB_CASE(5) TB_CASE(6) TB_CASE(7) TB_CASE(8)
 #undef TB_CASE
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 }  // namespace
 
-int decode_rows_per_chunk_unit() { return kWaves * kRowsPerIter; }
+int decode_chunk_unit(bool bf16) { return bf16 ? kMfmaWaves * kVT : kValuWaves * kRowsPerIter; }
+int decode_max_chunks() { return 4096; }
 
 hipError_t launch_decode(const DecodeArgs& a, int G, int d, bool bf16, hipStream_t st) {
   if (bf16) return d == 128 ? launch_g<bf16_t, 128>(a, G, st) : launch_g<bf16_t, 64>(a, G, st);

@@ -10,6 +10,7 @@ namespace tb {
 constexpr int kMaxB = 64;        // per-sequence values travel in kernel arguments
 constexpr int kScoreTile = 64;   // keys per scoring tile
 constexpr int kScoreRows = 256;  // window rows per scoring block
+constexpr int kVTile = 32;       // rows per V^T tile of the compact V cache
 
 // ---------------------------------------------------------------- scoring
 struct ScoreArgs {
@@ -45,9 +46,9 @@ struct CompactArgs {
   const void* v;
   const int32_t* keep_idx;  // [B][Hkv][Lmax]
   void* k_cache;          // [B][Hkv][cap][d]
-  void* v_cache;
+  void* v_cache;          // [B][Hkv][cap/32][d][32]
   int32_t* kv_len;        // [B]
-  int32_t B, Lmax, Hkv, cap, rows_per_block;
+  int32_t B, Lmax, Hkv, cap;
   int32_t n_keep[kMaxB];
 };
 hipError_t launch_compact(const CompactArgs& a, int d, int elem_bytes, int max_keep,
@@ -59,17 +60,17 @@ struct DecodeArgs {
   const void* k_new;      // [B][Hkv][d] (unused when append == 0)
   const void* v_new;
   void* k_cache;          // [B][Hkv][cap][d]
-  void* v_cache;
+  void* v_cache;          // [B][Hkv][cap/32][d][32]
   int32_t* kv_len;        // [B]
   void* out;              // [B][Hq][d]
-  float* part;            // ws: [B][Hkv][n_chunks][G*(d+2)]
-  int32_t* head_ctr;      // ws: [B*Hkv], zero between launches
-  int32_t* seq_ctr;       // ws: [B], zero between launches
+  float* part;            // ws: [B][Hkv][n_chunks][G][d+4] chunk partials (o, m, l)
+  int32_t* seq_len;       // ws: [B] attended length of this step
   int32_t B, Hkv, cap, chunk, n_chunks, append;
   float scale_log2;       // log2(e)/sqrt(d)
 };
-int decode_rows_per_chunk_unit();
-int decode_chunk_rows(int B, int Hkv, int cap);
+int decode_chunk_unit(bool bf16);
+int decode_max_chunks();
+int decode_chunk_rows(int B, int Hkv, int cap, bool bf16);
 size_t decode_ws_bytes(int B, int Hkv, int G, int d, int cap);
 hipError_t launch_decode(const DecodeArgs& a, int G, int d, bool bf16, hipStream_t st);
 

@@ -119,11 +119,12 @@ def test_select_validation(lib):
 def test_compact_validation(lib):
     E = _lib
 
-    def call(n=50, cap=60, Lmax=100, d=128, dt=_lib.TB_BF16, kc=FAKE):
+    def call(n=50, cap=64, Lmax=100, d=128, dt=_lib.TB_BF16, kc=FAKE):
         return lib.tb_compact_kv(FAKE, FAKE, FAKE, 1, _i32(n), Lmax, 2, d, dt, cap, kc, FAKE,
                                  FAKE, None, 0, None)
 
-    assert call(n=61) == E.TB_EINVAL          # beyond cap
+    assert call(n=65) == E.TB_EINVAL          # beyond cap
+    assert call(cap=60) == E.TB_EINVAL        # cap not a whole number of V^T tiles
     assert call(n=0) == E.TB_EINVAL
     assert call(n=101, cap=200) == E.TB_EINVAL  # beyond Lmax
     assert call(d=32) == E.TB_EUNSUPPORTED
@@ -133,7 +134,7 @@ def test_compact_validation(lib):
 def test_decode_validation(lib):
     E = _lib
 
-    def call(Hq=28, Hkv=4, d=128, cap=100, wsb=1 << 30, kn=FAKE, vn=FAKE, ws=FAKE):
+    def call(Hq=28, Hkv=4, d=128, cap=128, wsb=1 << 30, kn=FAKE, vn=FAKE, ws=FAKE):
         return lib.tb_decode_attn(FAKE, kn, vn, FAKE, FAKE, FAKE, 1, Hq, Hkv, d, cap,
                                   _lib.TB_BF16, FAKE, ws, wsb, None)
 
@@ -142,6 +143,7 @@ def test_decode_validation(lib):
     assert call(Hq=30) == E.TB_EINVAL
     assert call(d=256) == E.TB_EUNSUPPORTED
     assert call(cap=0) == E.TB_EINVAL
+    assert call(cap=100) == E.TB_EINVAL       # cap not a whole number of V^T tiles
     assert call(wsb=8) == E.TB_EWORKSPACE
     assert call(ws=None) == E.TB_EINVAL
 

@@ -35,7 +35,7 @@ def case(msg):
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
 @pytest.mark.parametrize("d", [64, 128])
 @pytest.mark.parametrize("G", [1, 2, 3, 4, 7, 8])
-@pytest.mark.parametrize("cap,lens", [(700, [1, 523]), (20000, [19990, 4097])])
+@pytest.mark.parametrize("cap,lens", [(704, [1, 523]), (20000, [19990, 4097])])
 def test_decode_only(dtype, d, G, cap, lens):
     case(f"decode_only dtype={dtype} d={d} G={G} cap={cap} lens={lens}")
     B, Hkv, T = 2, 2, 3
@@ -48,7 +48,7 @@ def test_decode_only(dtype, d, G, cap, lens):
     vn = torch.randn((T, B, Hkv, d), generator=g).to(dtype)
     cache = _lib.KVCache(B, Hq, Hkv, cap, d, dtype)
     cache.k.copy_(kc)
-    cache.v.copy_(vc)
+    cache.v.copy_(_lib.v_rows_to_tiles(vc))
     cache.kv_len.copy_(torch.tensor(lens, dtype=torch.int32))
     cache.host_len = list(lens)
     qd, knd, vnd = q.to(DEV), kn.to(DEV), vn.to(DEV)
@@ -72,10 +72,11 @@ def test_decode_only(dtype, d, G, cap, lens):
                 err = np.abs(got[t, b, gg * G:(gg + 1) * G] - ref).max()
                 assert err <= tol, f"b={b} g={gg} t={t}: max abs err {err}"
     # the appended rows landed in the caches
+    v_rows = _lib.v_tiles_to_rows(cache.v).cpu()
     for t in range(T):
         for b in range(B):
             assert torch.equal(cache.k[b, :, lens[b] + t].cpu(), kn[t, b])
-            assert torch.equal(cache.v[b, :, lens[b] + t].cpu(), vn[t, b])
+            assert torch.equal(v_rows[b, :, lens[b] + t], vn[t, b])
 
 
 # ------------------------------------------------------------------ compaction
@@ -88,7 +89,7 @@ def test_compact_exact(dtype, d):
     k = torch.randn((B, Hkv, Lmax, d), generator=g).to(dtype)
     v = torch.randn((B, Hkv, Lmax, d), generator=g).to(dtype)
     n_keep = [1, 517, 1000]
-    cap = 1100
+    cap = 1120
     keep = torch.zeros((B, Hkv, Lmax), dtype=torch.int32)
     for b in range(B):
         for gg in range(Hkv):
@@ -96,17 +97,22 @@ def test_compact_exact(dtype, d):
             keep[b, gg, : n_keep[b]] = sel.to(torch.int32)
     kd, vd = k.to(DEV), v.to(DEV)
     kc = torch.zeros((B, Hkv, cap, d), dtype=dtype, device=DEV)
-    vc = torch.zeros_like(kc)
+    vc = torch.full((B, Hkv, cap // 32, d, 32), 3.0, dtype=dtype, device=DEV)
     kv_len = torch.zeros((B,), dtype=torch.int32, device=DEV)
     _lib.tb_compact_kv(kd, vd, keep.to(DEV), n_keep, kc, vc, kv_len)
     torch.cuda.synchronize()
     assert kv_len.cpu().tolist() == n_keep
+    v_rows = _lib.v_tiles_to_rows(vc).cpu()
     for b in range(B):
         for gg in range(Hkv):
-            idx = keep[b, gg, : n_keep[b]].long()
-            assert torch.equal(kc[b, gg, : n_keep[b]].cpu(), k[b, gg, idx])
-            assert torch.equal(vc[b, gg, : n_keep[b]].cpu(), v[b, gg, idx])
-            assert torch.count_nonzero(kc[b, gg, n_keep[b]:]).item() == 0
+            n = n_keep[b]
+            idx = keep[b, gg, :n].long()
+            assert torch.equal(kc[b, gg, :n].cpu(), k[b, gg, idx])
+            assert torch.equal(v_rows[b, gg, :n], v[b, gg, idx])
+            assert torch.count_nonzero(kc[b, gg, n:]).item() == 0
+            tail = -(-n // 32) * 32          # rest of the last tile is zero-filled
+            assert torch.count_nonzero(v_rows[b, gg, n:tail]).item() == 0
+            assert bool((v_rows[b, gg, tail:] == 3.0).all())
 
 
 # ------------------------------------------------------------------ selection
@@ -294,8 +300,11 @@ def test_determinism_and_alpha0_identity():
         ev.evict(qd, kd, vd, [wl.L], [0.5], cache)
         out = run_decode(cache, dc["q"].to(DEV), dc["k_new"].to(DEV), dc["v_new"].to(DEV))
         torch.cuda.synchronize()
-        res.append((ev.scores.clone(), ev.raw.clone(), ev.keep_idx.clone(), out.clone()))
-    for x, y in zip(res[0], res[1]):
+        n_keep = cache.host_len[0] - 16
+        pref = wl.L - wl.w
+        res.append((ev.scores[:, :, :pref].clone(), ev.raw[:, :, :pref].clone(),
+                    ev.keep_idx[:, :, :n_keep].clone(), out.clone()))
+    for x, y in zip(res[0], res[1]):     # entries beyond these are unspecified
         assert torch.equal(x, y)
     # alpha = 0: the compacted cache is the prompt cache itself
     ev = Evictor(1, wl.L, wl.Hq, wl.Hkv, wl.d, wl.w, wl.pool)
@@ -303,7 +312,9 @@ def test_determinism_and_alpha0_identity():
     ev.evict(qd, kd, vd, [wl.L], [0.0], c0)
     c1 = _lib.KVCache(1, wl.Hq, wl.Hkv, wl.L + 16, wl.d, wl.dtype)
     c1.k[:, :, : wl.L].copy_(kd)
-    c1.v[:, :, : wl.L].copy_(vd)
+    v_rows = torch.zeros((1, wl.Hkv, c1.cap, wl.d), dtype=wl.dtype, device=DEV)
+    v_rows[:, :, : wl.L] = vd
+    c1.v.copy_(_lib.v_rows_to_tiles(v_rows))
     c1.kv_len.fill_(wl.L)
     c1.host_len = [wl.L]
     o0 = run_decode(c0, dc["q"].to(DEV), dc["k_new"].to(DEV), dc["v_new"].to(DEV))
