@@ -40,8 +40,8 @@ def _parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-steps", type=int, default=2,
-                    help="decode every n-th step in the CPU-baseline sample")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum CPU time of the oracle baseline sample")
     return ap.parse_args()
 
 
@@ -57,9 +57,9 @@ def _evict_bytes(Hq, Hkv, d, L, w, n_keep, esz=2):
     return score + select + compact
 
 
-def cpu_baseline(wl, pr, dc, every):
-    """The float64 oracle on this host: eviction + every n-th decode step per alpha."""
-    import numpy as np
+def cpu_baseline(wl, pr, dc, min_seconds):
+    """The float64 oracle on this host: whole passes of the step (eviction and
+    every decode step at each ratio), repeated until min_seconds have passed."""
     from oracle import timebill_oracle as O
     try:
         from threadpoolctl import threadpool_info
@@ -72,25 +72,22 @@ def cpu_baseline(wl, pr, dc, every):
     qs = dc["q"][:, 0].double().numpy()
     kn = dc["k_new"][:, 0].double().numpy()
     vn = dc["v_new"][:, 0].double().numpy()
-    t_total = 0.0
-    tokens = 0
+    tokens, passes = 0, 0
     t0 = time.perf_counter()
-    for a in wl.alphas:
-        te = time.perf_counter()
-        r = O.evict_sequence(q64, k64, v64, wl.L, wl.w, wl.pool, a)
-        t_ev = time.perf_counter() - te
-        steps = list(range(0, wl.T, every))
-        td = time.perf_counter()
-        O.decode_sequence(qs, kn, vn, r["k_cache"], r["v_cache"], steps=steps)
-        t_dec = (time.perf_counter() - td) * wl.T / len(steps)   # extrapolated to all steps
-        t_total += t_ev + t_dec
-        tokens += wl.T
-    wall = time.perf_counter() - t0
-    return {"value": tokens / t_total, "unit": "tokens/s", "cores": int(threads),
+    while True:
+        for a in wl.alphas:
+            r = O.evict_sequence(q64, k64, v64, wl.L, wl.w, wl.pool, a)
+            O.decode_sequence(qs, kn, vn, r["k_cache"], r["v_cache"])
+            tokens += wl.T
+        passes += 1
+        wall = time.perf_counter() - t0
+        if wall >= min_seconds:
+            break
+    return {"value": tokens / wall, "unit": "tokens/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": (f"float64 numpy oracle on the host: full eviction at each of the "
-                       f"{len(wl.alphas)} ratios plus every {every}-th of the {wl.T} decode steps, "
-                       f"decode time scaled to all steps; {wall:.1f} s of CPU work")}
+            "sample": (f"float64 numpy oracle on the host: {passes} whole pass(es) of the step "
+                       f"(eviction plus all {wl.T} decode steps at each of the "
+                       f"{len(wl.alphas)} ratios), {wall:.1f} s of CPU work")}
 
 
 def main():
@@ -246,7 +243,7 @@ def main():
         "wall_s": round(wall, 3),
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, pr, dc, args.cpu_sample_steps)
+        result["cpu_baseline"] = cpu_baseline(wl, pr, dc, args.cpu_seconds)
     print(json.dumps(result), flush=True)
 
 

@@ -435,43 +435,44 @@ __global__ __launch_bounds__(kValuThreads) void decode_valu_kernel(DecodeArgs a)
 
 // --------------------------------------------------------------------------
 // Merge of the chunk partials of one query head.
-// grid = (Hq, B), block = 512 threads: thread (sp, e4) handles output
-// elements 4*e4 .. 4*e4+3 over the chunks c = sp, sp + S, ... (S = 512/(D/4)
-// interleaved splits).  Each thread issues all its partial loads before
-// combining them (online max per thread, then a fixed-order merge of the
-// splits in LDS).
+// grid = (Hq, B), block = 256 threads: thread (sp, e4) handles output
+// elements 4*e4 .. 4*e4+3 over the chunks c = sp, sp + S, ... (S = 256/(d/4)
+// interleaved splits, up to 8 chunks per thread per round).  A thread issues
+// all of a round's partial loads before using them (online max per thread),
+// then the splits are combined by a fixed-order tree in LDS.
+// Every chunk writes a partial (empty chunks carry m = -inf, l = 0), so the
+// merge runs over all of them and never waits for the length; the length is
+// only needed for the final kv_len store.
 // --------------------------------------------------------------------------
-constexpr int kMergeThreads = 512;
-constexpr int kMaxPerThread = 16;      // chunk partials held in flight per thread
+constexpr int kMergeThreads = 256;
+constexpr int kMergePerThread = 8;
 
 template <typename T, int D, int G>
 __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeArgs a) {
   constexpr int E4 = D / 4;
   constexpr int S = kMergeThreads / E4;
+  constexpr int KPT = kMergePerThread;
   const int h = blockIdx.x, b = blockIdx.y;
   const int Hkv = a.Hkv, Hq = Hkv * G;
   const int g = h / G, hh = h % G;
   const int tid = threadIdx.x, e4 = tid % E4, sp = tid / E4;
-  // Every chunk writes a partial (empty chunks carry m = -inf, l = 0), so the
-  // merge runs over all of them and never waits for the length; the length is
-  // only needed for the final kv_len store.
   const int N = a.seq_len[b];
   const int n_used = a.n_chunks;
   const size_t bg = static_cast<size_t>(b) * Hkv + g;
   const float* base = a.part + (bg * a.n_chunks * G + hh) * (D + 4);
   constexpr size_t CSTRIDE = static_cast<size_t>(G) * (D + 4);
 
-  __shared__ float s_m[S], s_l[S];
+  __shared__ float2 s_ml[S][E4];
   __shared__ float4 s_o[S][E4];
 
   float M = -INFINITY, L = 0.f;
   float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int c0 = sp; c0 < n_used; c0 += S * kMaxPerThread) {
-    float mm[kMaxPerThread], ll[kMaxPerThread];
-    float4 oo[kMaxPerThread];
+  for (int c0 = sp; c0 < n_used; c0 += S * KPT) {
+    float mm[KPT], ll[KPT];
+    float4 oo[KPT];
     // unconditional loads (index clamped, value masked) so they issue back to back
 #pragma unroll
-    for (int k = 0; k < kMaxPerThread; ++k) {
+    for (int k = 0; k < KPT; ++k) {
       const int cc = c0 + k * S;
       const float* pc = base + min(cc, n_used - 1) * CSTRIDE;
       const float2 ml = *reinterpret_cast<const float2*>(pc + D);
@@ -483,45 +484,47 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeArgs 
     __builtin_amdgcn_sched_barrier(0);
     float mx = M;
 #pragma unroll
-    for (int k = 0; k < kMaxPerThread; ++k) mx = fmaxf(mx, mm[k]);
+    for (int k = 0; k < KPT; ++k) mx = fmaxf(mx, mm[k]);
     if (mx == -INFINITY) continue;
     const float corr = exp2f(M - mx);
     L *= corr; O.x *= corr; O.y *= corr; O.z *= corr; O.w *= corr;
 #pragma unroll
-    for (int k = 0; k < kMaxPerThread; ++k) {
+    for (int k = 0; k < KPT; ++k) {
       const float wgt = exp2f(mm[k] - mx);
       L += wgt * ll[k];
       O.x += wgt * oo[k].x; O.y += wgt * oo[k].y; O.z += wgt * oo[k].z; O.w += wgt * oo[k].w;
     }
     M = mx;
   }
-  if (e4 == 0) { s_m[sp] = M; s_l[sp] = L; }
-  s_o[sp][e4] = O;
-  __syncthreads();
-  if (sp == 0) {
-    float Mg = -INFINITY;
+  // fixed-order tree over the S splits
 #pragma unroll
-    for (int q = 0; q < S; ++q) Mg = fmaxf(Mg, s_m[q]);
-    float Lg = 0.f;
-    float4 Og = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (Mg != -INFINITY) {
-#pragma unroll
-      for (int q = 0; q < S; ++q) {
-        const float wgt = exp2f(s_m[q] - Mg);
-        const float4 x = s_o[q][e4];
-        Lg += wgt * s_l[q];
-        Og.x += wgt * x.x; Og.y += wgt * x.y; Og.z += wgt * x.z; Og.w += wgt * x.w;
+  for (int half = S / 2; half >= 1; half >>= 1) {
+    if (sp >= half && sp < 2 * half) { s_ml[sp][e4] = make_float2(M, L); s_o[sp][e4] = O; }
+    __syncthreads();
+    if (sp < half) {
+      const float2 ml2 = s_ml[sp + half][e4];
+      const float4 o2 = s_o[sp + half][e4];
+      const float Mn = fmaxf(M, ml2.x);
+      if (Mn != -INFINITY) {
+        const float w1 = exp2f(M - Mn), w2 = exp2f(ml2.x - Mn);
+        L = L * w1 + ml2.y * w2;
+        O.x = O.x * w1 + o2.x * w2; O.y = O.y * w1 + o2.y * w2;
+        O.z = O.z * w1 + o2.z * w2; O.w = O.w * w1 + o2.w * w2;
+        M = Mn;
       }
     }
-    const float inv = Lg > 0.f ? 1.f / Lg : 0.f;
+    __syncthreads();
+  }
+  if (sp == 0) {
+    const float inv = L > 0.f ? 1.f / L : 0.f;
     T* out = static_cast<T*>(a.out) + (static_cast<size_t>(b) * Hq + h) * D + 4 * e4;
     if constexpr (sizeof(T) == 2) {
       typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
-      const bf16x4 o4 = {static_cast<__bf16>(Og.x * inv), static_cast<__bf16>(Og.y * inv),
-                         static_cast<__bf16>(Og.z * inv), static_cast<__bf16>(Og.w * inv)};
-      *reinterpret_cast<bf16x4*>(out) = o4;
+      *reinterpret_cast<bf16x4*>(out) =
+          bf16x4{static_cast<__bf16>(O.x * inv), static_cast<__bf16>(O.y * inv),
+                 static_cast<__bf16>(O.z * inv), static_cast<__bf16>(O.w * inv)};
     } else {
-      *reinterpret_cast<float4*>(out) = make_float4(Og.x * inv, Og.y * inv, Og.z * inv, Og.w * inv);
+      *reinterpret_cast<float4*>(out) = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
     }
   }
   if (h == 0 && tid == 0) a.kv_len[b] = N;
