@@ -42,6 +42,9 @@ def _parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum CPU time of the oracle baseline sample")
+    ap.add_argument("--pmc-calibration", action="store_true",
+                    help="first copy 512 MiB device-to-device twice (a kernel of known "
+                         "traffic for scaling hardware byte counters)")
     return ap.parse_args()
 
 
@@ -55,6 +58,21 @@ def _evict_bytes(Hq, Hkv, d, L, w, n_keep, esz=2):
     select = Hkv * (L - w) * 4 + Hkv * n_keep * 4
     compact = 2 * 2 * Hkv * n_keep * d * esz + Hkv * n_keep * 4
     return score + select + compact
+
+
+def measured_traffic():
+    """HBM bytes per decode launch from the committed counter runs, or None when
+    the decode kernel source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "decode_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        with open(os.path.join(ROOT, rec["source"]), "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, KeyError, ValueError):
+        return None
+    return rec["traffic_bytes_per_launch"] if sha == rec["source_sha256"] else None
 
 
 def cpu_baseline(wl, pr, dc, min_seconds):
@@ -105,6 +123,13 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     _lib.load()
+    if args.pmc_calibration:
+        src = torch.ones((256 << 20,), dtype=torch.bfloat16, device=dev)   # 512 MiB
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     wl = synth.WORKLOADS[2]
     B, Hq, Hkv, d, w, L, T = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L, wl.T
     pr = synth.make_prompt(wl)
@@ -231,7 +256,10 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(),
+            "traffic_note": "HBM bytes per decode launch (FETCH_SIZE x2 + WRITE_SIZE, scaled "
+                            "by a 512 MiB copy; profiles/pmc_bf16_L8192_sweep.md); null if "
+                            "the decode kernel changed since",
             "avg_launch_us": round(avg_launch_us, 3),
             "bytes_per_launch": round(dec_bytes_total / launches),
             "timing": "HIP events around each ratio's graph of decode launches, "
