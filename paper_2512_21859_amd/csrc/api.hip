@@ -163,6 +163,8 @@ tb_status tb_score_window(const void* q_win, const void* k, int32_t B, const int
     a.row_M = reinterpret_cast<double*>(p);
     p += align256(units * R * sizeof(double));
     a.row_Z = reinterpret_cast<double*>(p);
+    p += align256(units * R * sizeof(double));
+    a.raw = raw_scores ? raw_scores : reinterpret_cast<float*>(p);
     return hip_status(tb::launch_score(a, d, dt == TB_BF16, stream), "tb_score_window launch");
   } catch (const std::exception& e) {
     return fail(TB_EINTERNAL, "tb_score_window: %s", e.what());

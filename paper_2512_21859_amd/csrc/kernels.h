@@ -19,10 +19,11 @@ struct ScoreArgs {
   float* scores;          // [B][Hkv][Lmax]
   float* raw_scores;      // nullable, same layout
   float* e;               // ws: [B][Hkv][n_tiles][R][64] exp(s - tile max), fp32
-  double* tile_m;         // ws: [B][Hkv][n_tiles][R]
-  double* tile_z;         // ws: [B][Hkv][n_tiles][R]
+  double* tile_m;         // ws: [B][Hkv][R][n_tiles]
+  double* tile_z;         // ws: [B][Hkv][R][n_tiles]
   double* row_M;          // ws: [B][Hkv][R]
   double* row_Z;          // ws: [B][Hkv][R]
+  float* raw;             // raw scores: raw_scores if given, else ws [B][Hkv][Lmax]
   int32_t B, Lmax, Hq, Hkv, w, pool, R, n_tiles, row_chunks;
   double scale;           // 1/sqrt(d)
   int32_t L[kMaxB];

@@ -4,27 +4,31 @@
 // Precision.  The selection that follows is compared position by position, so
 // scores are kept to ~1e-7 relative: dot products of the (exact) bf16/fp32
 // inputs are accumulated in float64, exponentials are float64, and sums are
-// float64.  Only the per-tile exponentials are stored as fp32 (relative
-// rounding 6e-8) and the final scores are rounded to fp32 once.
+// float64.  Only the per-tile exponentials and the raw scores are stored as
+// fp32 (relative rounding 6e-8 each); pooling is a max, so it is exact.
 //
-// Three kernels, all with fixed-order reductions (no atomics):
-//   K1 score_tiles: block = (64-key tile, <=256 window rows) of one KV head.
-//      Stages the window queries (transposed, fp32) and the key tile (fp64)
-//      in LDS in 32-wide d chunks; each thread computes a 4-row x 16-key
-//      micro-tile of float64 dot products (the 16 keys are a wave-uniform LDS
-//      broadcast).  Applies the causal mask, takes the tile max m per row,
-//      stores e = exp(s - m) as fp32 and z = sum(e) per row.
-//   K2 row_stats: one wave per window row merges the tiles' (m, z) into the
+// Four kernels, all with fixed-order reductions (no atomics):
+//   K1 score_tiles: block = (64-key tile, <=256 window rows) of one KV head;
+//      wave w owns 64 rows x the 64 keys.  Window queries and keys are staged
+//      in LDS in 32-wide d chunks; the float64 dot products run on the matrix
+//      cores (v_mfma_f64_16x16x4_f64, 4 x 4 tiles of 16 x 16 per wave).  Each
+//      row's 64 logits sit in one 16-lane DPP row, so the causal mask, the tile
+//      max m and z = sum exp(s - m) need no LDS.  Stores e = exp(s - m) (fp32)
+//      and (m, z) per (row, tile).
+//   K2 row_stats: one wave per window row merges its tiles' (m, z) into the
 //      row's global max M and normaliser Z.
-//   K3 score_accum: block = 64 prefix columns (+ pool halo).  For each column
-//      j, A[j] = sum_r e[r][j] * exp(m[r][tile(j)] - M[r]) / Z[r] in float64,
-//      then the max-pool over |j - j'| <= pool/2 within the prefix.
+//   K3 score_accum: block = 64 prefix columns; A[j] = sum_r e[r][j] *
+//      exp(m[r][tile] - M[r]) / Z[r] in float64 (four row groups, four
+//      independent accumulators each, combined in a fixed order); raw A as fp32.
+//   K4 pool: max of the raw scores over |j - j'| <= pool/2 within the prefix.
 
 #include "common.h"
 #include "kernels.h"
 
 namespace tb {
 namespace {
+
+typedef __attribute__((ext_vector_type(4))) double f64x4;
 
 constexpr int kThreads = 256;
 constexpr int kT = kScoreTile;     // keys per tile (64)
@@ -43,31 +47,57 @@ __device__ __forceinline__ void load8<float>(const float* p, float* out) {
   Elem<float>::widen(ldg16(p + 4), out + 4);
 }
 
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const uint64_t u = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_update_dpp(0, static_cast<int>(u & 0xffffffffu), CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, static_cast<int>(u >> 32), CTRL, 0xF, 0xF, false);
+  return __longlong_as_double((static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) |
+                              static_cast<uint32_t>(lo));
+}
+// Max / sum over the 16 lanes of a DPP row; every lane gets the result, in a
+// fixed order (deterministic).
+__device__ __forceinline__ double row16_max_f64(double x) {
+  x = fmax(x, dpp_f64<kDppQuadXor1>(x));
+  x = fmax(x, dpp_f64<kDppQuadXor2>(x));
+  x = fmax(x, dpp_f64<kDppRowHalfMirror>(x));
+  x = fmax(x, dpp_f64<kDppRowMirror>(x));
+  return x;
+}
+__device__ __forceinline__ double row16_sum_f64(double x) {
+  x += dpp_f64<kDppQuadXor1>(x);
+  x += dpp_f64<kDppQuadXor2>(x);
+  x += dpp_f64<kDppRowHalfMirror>(x);
+  x += dpp_f64<kDppRowMirror>(x);
+  return x;
+}
+
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void score_tiles_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(kThreads, 2) void score_tiles_kernel(ScoreArgs a) {
   const int tile = blockIdx.x / a.row_chunks, rc = blockIdx.x % a.row_chunks;
   const int g = blockIdx.y, b = blockIdx.z;
   const int L = a.L[b];
-  const int kbase_tile = tile * kT;
-  if (kbase_tile >= L) return;
+  const int kbase = tile * kT;
+  if (kbase >= L) return;
   const int G = a.Hq / a.Hkv, R = a.R, w = a.w;
   const int row0 = rc * kRows;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int q4 = lane >> 4, r16 = lane & 15;
 
-  __shared__ float qT[kDC][kRows];                 // 32 KB
-  __shared__ double kT_[kDC][kT];                  // 16 KB
-  __shared__ double red[4][kRows];                 // 8 KB
+  __shared__ float qs[kRows][kDC + 1];             // +1: conflict-free column reads
+  __shared__ float ks[kT][kDC + 1];
 
-  double acc[4][16];
+  f64x4 acc[4][4];
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+  for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
-    for (int c = 0; c < 16; ++c) acc[r][c] = 0.0;
+    for (int kt = 0; kt < 4; ++kt) acc[rt][kt] = f64x4{0.0, 0.0, 0.0, 0.0};
 
   const T* kh = static_cast<const T*>(a.k) + (static_cast<size_t>(b) * a.Hkv + g) * a.Lmax * D;
+#pragma unroll 1
   for (int dc = 0; dc < D; dc += kDC) {
-    // Stage the window queries of this d chunk, transposed: qT[dd][row].
-    {
+    {   // window queries of this d chunk: thread = row
       const int r = row0 + tid;
       float qv[kDC];
       if (r < R) {
@@ -81,12 +111,11 @@ __global__ __launch_bounds__(kThreads) void score_tiles_kernel(ScoreArgs a) {
         for (int e = 0; e < kDC; ++e) qv[e] = 0.f;
       }
 #pragma unroll
-      for (int e = 0; e < kDC; ++e) qT[e][tid] = qv[e];
+      for (int e = 0; e < kDC; ++e) qs[tid][e] = qv[e];
     }
-    // Stage the key tile of this d chunk in float64: kT_[dd][key].
-    {
+    {   // key tile of this d chunk: 4 threads per key, 8 elements each
       const int kk = tid >> 2, dp = (tid & 3) * 8;
-      const int j = kbase_tile + kk;
+      const int j = kbase + kk;
       float kv[8];
       if (j < L) {
         load8<T>(kh + static_cast<size_t>(j) * D + dc + dp, kv);
@@ -95,83 +124,64 @@ __global__ __launch_bounds__(kThreads) void score_tiles_kernel(ScoreArgs a) {
         for (int e = 0; e < 8; ++e) kv[e] = 0.f;
       }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) kT_[dp + e][kk] = static_cast<double>(kv[e]);
+      for (int e = 0; e < 8; ++e) ks[kk][dp + e] = kv[e];
     }
     __syncthreads();
-#pragma unroll 4
-    for (int dd = 0; dd < kDC; ++dd) {
-      const float4 q4 = *reinterpret_cast<const float4*>(&qT[dd][4 * lane]);
-      const double q[4] = {q4.x, q4.y, q4.z, q4.w};
-      double kv[16];
 #pragma unroll
-      for (int c = 0; c < 16; c += 2) {
-        const double2 k2 = *reinterpret_cast<const double2*>(&kT_[dd][16 * wave + c]);
-        kv[c] = k2.x; kv[c + 1] = k2.y;
-      }
+    for (int k4 = 0; k4 < kDC / 4; ++k4) {
+      const int dd = 4 * k4 + q4;                  // this lane's k index
+      double av[4], bv[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
+      for (int rt = 0; rt < 4; ++rt) av[rt] = static_cast<double>(qs[64 * wave + 16 * rt + r16][dd]);
 #pragma unroll
-        for (int c = 0; c < 16; ++c) acc[r][c] = fma(q[r], kv[c], acc[r][c]);
+      for (int kt = 0; kt < 4; ++kt) bv[kt] = static_cast<double>(ks[16 * kt + r16][dd]);
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+          acc[rt][kt] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[rt], bv[kt], acc[rt][kt], 0, 0, 0);
     }
     __syncthreads();
   }
 
-  // Masked logits; tile max per row.
-  const int kbase = kbase_tile + 16 * wave;
-  double rmax[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int rg = row0 + 4 * lane + r;
-    const int lim = (rg < R) ? min(L - 1, L - w + rg % w) : -1;   // last visible key
-    double mx = -INFINITY;
-#pragma unroll
-    for (int c = 0; c < 16; ++c) {
-      const double s = (kbase + c <= lim) ? acc[r][c] * a.scale : -INFINITY;
-      acc[r][c] = s;
-      mx = fmax(mx, s);
-    }
-    rmax[r] = mx;
-    red[wave][4 * lane + r] = mx;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int rr = 4 * lane + r;
-    rmax[r] = fmax(fmax(red[0][rr], red[1][rr]), fmax(red[2][rr], red[3][rr]));
-  }
-  __syncthreads();
-
-  // e = exp(s - m) (fp32 store) and per-row partial sums.
+  // acc[rt][kt][v] = q(row 16 rt + q4 + 4 v) . k(key 16 kt + r16) of this wave
+  // (the float64 16x16x4 product returns rows interleaved: item v of lane l is
+  // row l/16 + 4v, column l%16).
   const size_t bg = static_cast<size_t>(b) * a.Hkv + g;
   float* ebase = a.e + (bg * a.n_tiles + tile) * static_cast<size_t>(R) * kT;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int rg = row0 + 4 * lane + r;
-    double zsum = 0.0;
-    float ef[16];
+  for (int rt = 0; rt < 4; ++rt) {
 #pragma unroll
-    for (int c = 0; c < 16; ++c) {
-      const double ev = (rmax[r] == -INFINITY) ? 0.0 : exp(acc[r][c] - rmax[r]);
-      zsum += ev;
-      ef[c] = static_cast<float>(ev);
-    }
-    red[wave][4 * lane + r] = zsum;
-    if (rg < R) {
-      float4* dst = reinterpret_cast<float4*>(ebase + static_cast<size_t>(rg) * kT + 16 * wave);
+    for (int v = 0; v < 4; ++v) {
+      const int rg = row0 + 64 * wave + 16 * rt + q4 + 4 * v;
+      const int lim = (rg < R) ? min(L - 1, L - w + rg % w) : -1;    // last visible key
+      double s[4];
+      double mx = -INFINITY;
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
-        dst[c] = make_float4(ef[4 * c], ef[4 * c + 1], ef[4 * c + 2], ef[4 * c + 3]);
-    }
-  }
-  __syncthreads();
-  if (wave == 0) {
+      for (int kt = 0; kt < 4; ++kt) {
+        const int key = kbase + 16 * kt + r16;
+        s[kt] = (key <= lim) ? acc[rt][kt][v] * a.scale : -INFINITY;
+        mx = fmax(mx, s[kt]);
+      }
+      mx = row16_max_f64(mx);
+      double z = 0.0;
+      float ef[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int rr = 4 * lane + r, rg = row0 + rr;
+      for (int kt = 0; kt < 4; ++kt) {
+        const double ev = (mx == -INFINITY) ? 0.0 : exp(s[kt] - mx);
+        z += ev;
+        ef[kt] = static_cast<float>(ev);
+      }
+      z = row16_sum_f64(z);
       if (rg < R) {
-        const size_t o = (bg * a.n_tiles + tile) * R + rg;
-        a.tile_m[o] = rmax[r];
-        a.tile_z[o] = ((red[0][rr] + red[1][rr]) + red[2][rr]) + red[3][rr];
+        float* dst = ebase + static_cast<size_t>(rg) * kT + r16;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) dst[16 * kt] = ef[kt];
+        if (r16 == 0) {
+          const size_t o = (bg * R + rg) * a.n_tiles + tile;
+          a.tile_m[o] = mx;
+          a.tile_z[o] = z;
+        }
       }
     }
   }
@@ -187,10 +197,10 @@ __global__ __launch_bounds__(kThreads) void row_stats_kernel(ScoreArgs a) {
   const int bg = wid / a.R;
   const int b = bg / a.Hkv;
   const int nt = (a.L[b] + kT - 1) / kT;
+  const size_t rowo = (static_cast<size_t>(bg) * a.R + r) * a.n_tiles;
   double M = -INFINITY, Z = 0.0;
   for (int t = lane; t < nt; t += 64) {
-    const size_t o = (static_cast<size_t>(bg) * a.n_tiles + t) * a.R + r;
-    const double m = a.tile_m[o], z = a.tile_z[o];
+    const double m = a.tile_m[rowo + t], z = a.tile_z[rowo + t];
     if (m == -INFINITY) continue;
     if (m > M) { Z = Z * exp(M - m) + z; M = m; }
     else       { Z += z * exp(m - M); }
@@ -213,67 +223,63 @@ __global__ __launch_bounds__(kThreads) void row_stats_kernel(ScoreArgs a) {
   }
 }
 
-constexpr int kMaxHalo = 64;
-
+// Column sums of one 64-column tile: thread (rg, col), rows r = rg + 4k.
 __global__ __launch_bounds__(kThreads) void score_accum_kernel(ScoreArgs a) {
   const int ct = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int L = a.L[b], pref = L - a.w;
   const int j0 = ct * kT;
   if (j0 >= pref) return;
-  const int R = a.R, hp = a.pool / 2;
-  const int ncols = kT + 2 * hp;
-  const int nt = (L + kT - 1) / kT;
+  const int R = a.R;
   const size_t bg = static_cast<size_t>(b) * a.Hkv + g;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, col = tid & 63, rg = tid >> 6;
 
-  __shared__ double coef[3][1024];                 // tiles ct-1, ct, ct+1
-  __shared__ double part[4][kT + 2 * kMaxHalo];
-  __shared__ double raw[kT + 2 * kMaxHalo];
+  __shared__ double coef[1024];
+  __shared__ double part[4][kT];
 
-  for (int idx = tid; idx < 3 * R; idx += kThreads) {
-    const int tt = ct - 1 + idx / R, r = idx % R;
-    double cv = 0.0;
-    if (tt >= 0 && tt < nt) {
-      const double m = a.tile_m[(bg * a.n_tiles + tt) * R + r];
-      const double M = a.row_M[bg * R + r], Z = a.row_Z[bg * R + r];
-      if (m != -INFINITY && Z > 0.0) cv = exp(m - M) / Z;
-    }
-    coef[idx / R][r] = cv;
+  for (int r = tid; r < R; r += kThreads) {
+    const double m = a.tile_m[(bg * R + r) * a.n_tiles + ct];
+    const double M = a.row_M[bg * R + r], Z = a.row_Z[bg * R + r];
+    coef[r] = (m != -INFINITY && Z > 0.0) ? exp(m - M) / Z : 0.0;
   }
   __syncthreads();
 
-  const float* ebg = a.e + bg * a.n_tiles * static_cast<size_t>(R) * kT;
-  for (int item = tid; item < 4 * ncols; item += kThreads) {
-    const int col = item % ncols, rg = item / ncols;
-    const int j = j0 - hp + col;
-    double s = 0.0;
-    if (j >= 0 && j < pref) {
-      const int tt = j / kT, jj = j % kT;
-      const float* et = ebg + static_cast<size_t>(tt) * R * kT + jj;
-      const double* cf = coef[tt - ct + 1];
-      for (int r = rg; r < R; r += 4) s = fma(static_cast<double>(et[static_cast<size_t>(r) * kT]), cf[r], s);
-    }
-    part[rg][col] = s;
+  const float* et = a.e + (bg * a.n_tiles + ct) * static_cast<size_t>(R) * kT + col;
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+  int r = rg;
+  for (; r + 12 < R; r += 16) {
+    const float e0 = et[static_cast<size_t>(r) * kT];
+    const float e1 = et[static_cast<size_t>(r + 4) * kT];
+    const float e2 = et[static_cast<size_t>(r + 8) * kT];
+    const float e3 = et[static_cast<size_t>(r + 12) * kT];
+    s0 = fma(static_cast<double>(e0), coef[r], s0);
+    s1 = fma(static_cast<double>(e1), coef[r + 4], s1);
+    s2 = fma(static_cast<double>(e2), coef[r + 8], s2);
+    s3 = fma(static_cast<double>(e3), coef[r + 12], s3);
   }
+  for (; r < R; r += 4) s0 = fma(static_cast<double>(et[static_cast<size_t>(r) * kT]), coef[r], s0);
+  part[rg][col] = (s0 + s1) + (s2 + s3);
   __syncthreads();
-  for (int col = tid; col < ncols; col += kThreads)
-    raw[col] = ((part[0][col] + part[1][col]) + part[2][col]) + part[3][col];
-  __syncthreads();
-
   if (tid < kT) {
     const int j = j0 + tid;
     if (j < pref) {
-      const int col = tid + hp;
-      double mx = raw[col];
-      for (int dj = -hp; dj <= hp; ++dj) {
-        const int jn = j + dj;
-        if (jn >= 0 && jn < pref) mx = fmax(mx, raw[col + dj]);
-      }
-      const size_t o = bg * a.Lmax + j;
-      a.scores[o] = static_cast<float>(mx);
-      if (a.raw_scores) a.raw_scores[o] = static_cast<float>(raw[col]);
+      const double A = ((part[0][tid] + part[1][tid]) + part[2][tid]) + part[3][tid];
+      a.raw[bg * a.Lmax + j] = static_cast<float>(A);
     }
   }
+}
+
+__global__ __launch_bounds__(kThreads) void pool_kernel(ScoreArgs a) {
+  const int g = blockIdx.y, b = blockIdx.z;
+  const int j = blockIdx.x * kThreads + threadIdx.x;
+  const int pref = a.L[b] - a.w;
+  if (j >= pref) return;
+  const int hp = a.pool / 2;
+  const size_t bg = static_cast<size_t>(b) * a.Hkv + g;
+  const float* raw = a.raw + bg * a.Lmax;
+  float mx = raw[j];
+  const int lo = max(j - hp, 0), hi = min(j + hp, pref - 1);
+  for (int jn = lo; jn <= hi; ++jn) mx = fmaxf(mx, raw[jn]);
+  a.scores[bg * a.Lmax + j] = mx;
 }
 
 }  // namespace
@@ -285,6 +291,7 @@ size_t score_ws_bytes(int B, int Lmax, int Hkv, int R) {
   size_t bytes = up(units * n_tiles * R * kT * sizeof(float));       // e
   bytes += 2 * up(units * n_tiles * R * sizeof(double));             // tile m, z
   bytes += 2 * up(units * R * sizeof(double));                       // row M, Z
+  bytes += up(units * Lmax * sizeof(float));                         // raw scores
   return bytes;
 }
 
@@ -305,6 +312,10 @@ hipError_t launch_score(const ScoreArgs& a, int d, bool bf16, hipStream_t st) {
   if (err != hipSuccess) return err;
   const dim3 g3((a.Lmax + kT - 1) / kT, a.Hkv, a.B);
   score_accum_kernel<<<g3, kThreads, 0, st>>>(a);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const dim3 g4((a.Lmax + kThreads - 1) / kThreads, a.Hkv, a.B);
+  pool_kernel<<<g4, kThreads, 0, st>>>(a);
   return hipGetLastError();
 }
 
