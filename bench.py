@@ -42,6 +42,8 @@ def _parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum CPU time of the oracle baseline sample")
+    ap.add_argument("--no-long-context", action="store_true",
+                    help="skip the supplementary long-context decode measurement")
     ap.add_argument("--pmc-calibration", action="store_true",
                     help="first copy 512 MiB device-to-device twice (a kernel of known "
                          "traffic for scaling hardware byte counters)")
@@ -106,6 +108,60 @@ def cpu_baseline(wl, pr, dc, min_seconds):
             "sample": (f"float64 numpy oracle on the host: {passes} whole pass(es) of the step "
                        f"(eviction plus all {wl.T} decode steps at each of the "
                        f"{len(wl.alphas)} ratios), {wall:.1f} s of CPU work")}
+
+
+def long_context(torch, _lib, synth, Evictor, dev, steps=64, alpha=0.5):
+    """Supplementary: decode at the long-context shape (L = 131072, 32 q / 8 kv
+    heads, alpha = 0.5, ~65.5k retained rows per head, ~268 MB of K/V per step),
+    where a step is bandwidth-bound rather than latency-bound."""
+    wl = synth.WORKLOADS[5]
+    B, Hq, Hkv, d, w, L = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L
+    pr = synth.make_prompt(wl)
+    dc = synth.make_decode(wl, T=steps)
+    q_win, k, v = (pr[x].to(dev) for x in ("q_win", "k", "v"))
+    qd, knd, vnd = (dc[x].to(dev) for x in ("q", "k_new", "v_new"))
+    del pr
+    stream = torch.cuda.current_stream()
+    ev = Evictor(B, L, Hq, Hkv, d, w, wl.pool, device=dev)
+    nk = _lib.tb_keep_count(L, alpha, w)
+    cache = _lib.KVCache(B, Hq, Hkv, nk + steps, d, wl.dtype, device=dev)
+    out = torch.empty((steps, B, Hq, d), dtype=wl.dtype, device=dev)
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    ev.evict(q_win, k, v, [L], [alpha], cache, stream)          # warm-up
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    cs = torch.cuda.Stream()
+    with torch.cuda.graph(g, stream=cs):
+        for t in range(steps):
+            _lib.tb_decode_attn(qd[t], knd[t], vnd[t], cache.k, cache.v, cache.kv_len, out[t],
+                                cache.ws, stream=cs)
+    torch.cuda.synchronize()
+    ev_ms, de_ms = [], []
+    for _ in range(3):
+        e0.record(stream)
+        ev.evict(q_win, k, v, [L], [alpha], cache, stream)
+        e1.record(stream)
+        g.replay()
+        e2.record(stream)
+        torch.cuda.synchronize()
+        ev_ms.append(e0.elapsed_time(e1))
+        de_ms.append(e1.elapsed_time(e2))
+    ev_t, de_t = min(ev_ms), min(de_ms)
+    dbytes = sum(_decode_bytes(Hq, Hkv, d, nk + t + 1) for t in range(steps)) / steps
+    per_step_us = de_t * 1e3 / steps
+    cbytes = 2 * 2 * Hkv * nk * d * 2
+    return {
+        "workload": "bf16, B=1, L=131072, 32 q / 8 kv heads, d=128, w=64, pool 7, "
+                    f"alpha={alpha}, {steps} decode steps",
+        "n_keep": nk,
+        "decode_us_per_step": round(per_step_us, 2),
+        "decode_GBps": round(dbytes / (per_step_us * 1e-6) / 1e9, 1),
+        "decode_frac_of_8TBps": round(dbytes / (per_step_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+        "bytes_per_step": round(dbytes),
+        "evict_us": round(ev_t * 1e3, 1),
+        "compaction_bytes": cbytes,
+        "timing": "best of 3: HIP events around the eviction and around a graph of the decode steps",
+    }
 
 
 def main():
@@ -270,6 +326,8 @@ def main():
                             "r2": 1 - ss_res / ss_tot if ss_tot > 0 else 1.0},
         "wall_s": round(wall, 3),
     }
+    if not args.no_long_context:
+        result["long_context"] = long_context(torch, _lib, synth, Evictor, dev)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, pr, dc, args.cpu_seconds)
     print(json.dumps(result), flush=True)
