@@ -271,15 +271,16 @@ def main():
             "evict_plus_decode_GBps": round((dbytes + ebytes) / ((d_med + e_med) * 1e-3) / 1e9, 1),
             "tokens_per_s": round(T / ((d_med + e_med) * 1e-3), 1),
         })
-    # decode time per token against retained length: least-squares line (Eq. decoding-step form)
-    xs = [p["n_keep"] + T / 2 for p in per_alpha]
+    # decode time per step against retained length: least-squares line t = p N_kv + q
+    # (the execution-time model's decode-step form), fitted by the library
+    xs = [p["n_keep"] + (T + 1) / 2 for p in per_alpha]
     ys = [p["decode_us_per_token"] for p in per_alpha]
-    mx, my = sum(xs) / len(xs), sum(ys) / len(ys)
-    sxx = sum((x - mx) ** 2 for x in xs)
-    slope = sum((x - mx) * (y - my) for x, y in zip(xs, ys)) / sxx
-    icpt = my - slope * mx
-    ss_res = sum((y - (icpt + slope * x)) ** 2 for x, y in zip(xs, ys))
+    slope, icpt = _lib.tb_ete_fit(xs, ys, 1)
+    pred = [slope * x + icpt for x in xs]
+    my = sum(ys) / len(ys)
+    ss_res = sum((y - f) ** 2 for y, f in zip(ys, pred))
     ss_tot = sum((y - my) ** 2 for y in ys)
+    mape = 100.0 * sum(abs(f - y) / y for y, f in zip(ys, pred)) / len(ys)
 
     tokens = n_al * T * args.steps
     value = tokens / (total_ms * 1e-3)
@@ -322,8 +323,11 @@ def main():
                       "divided by the launch count (inter-kernel gaps included)",
         },
         "per_alpha": per_alpha,
-        "decode_time_fit": {"us_per_token_per_kv_row": slope, "intercept_us": icpt,
-                            "r2": 1 - ss_res / ss_tot if ss_tot > 0 else 1.0},
+        "decode_time_fit": {"p_us_per_kv_row": slope, "q_us": icpt,
+                            "r2": 1 - ss_res / ss_tot if ss_tot > 0 else 1.0,
+                            "mape_pct": mape,
+                            "note": "least squares of per-step decode time vs mean retained "
+                                    "length over the ratio sweep (tb_ete_fit)"},
         "wall_s": round(wall, 3),
     }
     if not args.no_long_context:

@@ -157,6 +157,35 @@ tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new,
                          int32_t cap, tb_dtype dt, void* out, void* ws,
                          size_t ws_bytes, hipStream_t stream);
 
+/* ---- time-budget controller (host) ------------------------------------ */
+
+/* [host] Least-squares fit of the execution-time model from profiled pairs
+ * (Sec. 4.2, profiling-based fitting): degree 1 gives coef = {p, q} of
+ * t = p N + q (decode step vs KV length, Eq. decoding_step_time_raw); degree 2
+ * gives coef = {a, b, c} of t = a N^2 + b N + c (prefill, Eq.
+ * prefill_phase_time_raw).  Returns 0, or -1 on bad arguments / a singular
+ * system (fewer than degree + 1 distinct N). */
+int32_t tb_ete_fit(const double* n, const double* t, int32_t count, int32_t degree,
+                   double* coef);
+
+/* [host] Predicted worst-case execution time (Eq. wcet): prefill plus the
+ * decode steps i = 1 .. n_hat_w - 1 at KV length (1 - alpha) n_x + i - 1.
+ * prefill_abc = {a, b, c}, step_pq = {p, q}.  NaN on null pointers. */
+double tb_wcet(const double* prefill_abc, const double* step_pq, double n_x, double alpha,
+               int32_t n_hat_w);
+
+/* [host] Smallest eviction ratio in [0, alpha_max] with
+ * t_predict + WCET(alpha) <= budget (Sec. 5.1, Eq. problem_converted), in
+ * closed form (Eq. alpha_with_predictor with the second term read as
+ * (n_hat_w - 2) / (2 n_x); the printed version also divides it by p, which is
+ * dimensionally inconsistent).  *feasible (nullable) is 1 when the budget can
+ * be met at or below alpha_max, else 0 and alpha_max is returned.
+ * n_hat_w <= 1 (no decode step) gives 0.  NaN for n_x <= 0 or alpha_max
+ * outside [0, 1). */
+double tb_alpha_star(const double* prefill_abc, const double* step_pq, double n_x,
+                     int32_t n_hat_w, double budget, double t_predict, double alpha_max,
+                     int32_t* feasible);
+
 #ifdef __cplusplus
 }
 #endif

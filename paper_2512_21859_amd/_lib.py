@@ -22,7 +22,8 @@ TB_OP_SCORE, TB_OP_SELECT, TB_OP_COMPACT, TB_OP_DECODE = range(4)
 V_TILE = 32          # the compact V cache is stored as transposed tiles of 32 rows
 
 EXPORTED = ("tb_keep_count", "tb_last_error", "tb_workspace_bytes", "tb_score_window",
-            "tb_select_topk", "tb_compact_kv", "tb_decode_attn")
+            "tb_select_topk", "tb_compact_kv", "tb_decode_attn", "tb_ete_fit", "tb_wcet",
+            "tb_alpha_star")
 
 _lib = None
 
@@ -61,6 +62,12 @@ def load() -> ctypes.CDLL:
     lib.tb_decode_attn.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp,
                                    sz, vp]
     lib.tb_decode_attn.restype = i32
+    lib.tb_ete_fit.argtypes = [p_dbl, p_dbl, i32, i32, p_dbl]
+    lib.tb_ete_fit.restype = i32
+    lib.tb_wcet.argtypes = [p_dbl, p_dbl, dbl, dbl, i32]
+    lib.tb_wcet.restype = dbl
+    lib.tb_alpha_star.argtypes = [p_dbl, p_dbl, dbl, i32, dbl, dbl, dbl, p_i32]
+    lib.tb_alpha_star.restype = dbl
     _lib = lib
     return lib
 
@@ -143,6 +150,33 @@ def tb_select_topk(scores: torch.Tensor, L: Sequence[int], w: int, alpha: Sequen
         _dev(keep_idx, "keep_idx", torch.int32), n_keep, _dev(ws, "ws"), ws_bytes,
         _stream(stream)))
     return list(n_keep)
+
+
+def _dbl_array(vals: Sequence[float]):
+    return (ctypes.c_double * len(vals))(*[float(v) for v in vals])
+
+
+def tb_ete_fit(n: Sequence[float], t: Sequence[float], degree: int) -> List[float]:
+    """Least-squares coefficients, highest power first ({p, q} or {a, b, c})."""
+    coef = (ctypes.c_double * (degree + 1))()
+    if load().tb_ete_fit(_dbl_array(n), _dbl_array(t), len(n), degree, coef) != 0:
+        raise ValueError("tb_ete_fit: bad arguments or singular system")
+    return list(coef)
+
+
+def tb_wcet(prefill_abc: Sequence[float], step_pq: Sequence[float], n_x: float, alpha: float,
+            n_hat_w: int) -> float:
+    return float(load().tb_wcet(_dbl_array(prefill_abc), _dbl_array(step_pq), n_x, alpha,
+                                n_hat_w))
+
+
+def tb_alpha_star(prefill_abc: Sequence[float], step_pq: Sequence[float], n_x: float,
+                  n_hat_w: int, budget: float, t_predict: float, alpha_max: float):
+    """Returns (alpha*, feasible)."""
+    feas = ctypes.c_int32(0)
+    a = load().tb_alpha_star(_dbl_array(prefill_abc), _dbl_array(step_pq), n_x, n_hat_w, budget,
+                             t_predict, alpha_max, ctypes.byref(feas))
+    return float(a), bool(feas.value)
 
 
 def v_rows_to_tiles(v_rows: torch.Tensor) -> torch.Tensor:

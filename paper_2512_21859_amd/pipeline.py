@@ -52,3 +52,17 @@ def run_decode(cache: "_lib.KVCache", q: torch.Tensor, k_new: torch.Tensor,
     for t in range(T):
         cache.decode(q[t], k_new[t], v_new[t], out[t], stream)
     return out
+
+
+def choose_alpha(prefill_abc, step_pq, n_x: int, n_hat: int, bucket: int, k: int, n_max: int,
+                 budget: float, t_predict: float = 0.0, alpha_max: float = 0.95):
+    """Per-request eviction ratio (Sec. 5.2 deployment): the predicted bucket
+    n_hat gives N_hat = min(N_max, n_hat * B) (Eq. predictor_inference), the
+    pessimistic length N_hat_W = min(k * N_hat, N_max), and alpha* is the
+    smallest ratio meeting the budget (computed by tb_alpha_star).
+    Returns (alpha, feasible, N_hat_W)."""
+    n_hat_len = min(n_max, n_hat * bucket)
+    n_hat_w = min(k * n_hat_len, n_max)
+    alpha, feasible = _lib.tb_alpha_star(prefill_abc, step_pq, float(n_x), n_hat_w, budget,
+                                         t_predict, alpha_max)
+    return alpha, feasible, n_hat_w

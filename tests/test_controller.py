@@ -1,0 +1,156 @@
+"""Time-budget controller: the float64 reference pinned against the paper's
+constraint (bisection), a hand-derived example and library least squares; the
+C ABI host functions checked against the reference.  No GPU."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from oracle import controller as C
+from paper_2512_21859_amd import _lib
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "controller_example.json")
+
+
+def _ex():
+    with open(GOLDEN) as f:
+        return json.load(f)
+
+
+def _bisect_alpha(abc, pq, n_x, n_hat_w, budget, t_pred, alpha_max):
+    """Smallest alpha in [0, alpha_max] meeting t_pred + WCET <= budget, found by
+    bisection on the explicit-loop WCET (independent of the closed form)."""
+    f = lambda a: t_pred + C.t_wcet(abc, pq, n_x, a, n_hat_w) - budget
+    if f(0.0) <= 0:
+        return 0.0, True
+    if f(alpha_max) > 0:
+        return alpha_max, False
+    lo, hi = 0.0, alpha_max
+    for _ in range(200):
+        mid = 0.5 * (lo + hi)
+        lo, hi = (lo, mid) if f(mid) <= 0 else (mid, hi)
+    return hi, True
+
+
+def test_hand_example():
+    e = _ex()
+    a, feas = C.alpha_star(e["prefill_abc"], e["step_pq"], e["n_x"], e["n_hat_w"], e["budget"],
+                           e["t_predict"], e["alpha_max"])
+    assert feas and abs(a - e["alpha_star"]) < 1e-12
+    assert abs(C.t_wcet(e["prefill_abc"], e["step_pq"], e["n_x"], 0.0, e["n_hat_w"]) -
+               e["wcet_at_alpha_0"]) < 1e-9
+    assert abs(C.t_wcet(e["prefill_abc"], e["step_pq"], e["n_x"], e["alpha_star"], e["n_hat_w"]) -
+               e["budget"]) < 1e-9
+    L = e["lengths"]
+    for c in L["cases"]:
+        nh = C.predicted_length(c["n_hat"], L["bucket"], L["n_max"])
+        assert nh == c["N_hat"]
+        assert C.pessimistic_length(nh, L["k"], L["n_max"]) == c["N_hat_W"]
+
+
+@settings(max_examples=200, deadline=None)
+@given(st.floats(1e-9, 1e-6), st.floats(1e-6, 1e-3), st.floats(0.0, 1.0),
+       st.floats(1e-6, 1e-3), st.floats(1e-4, 0.1), st.integers(100, 32768),
+       st.integers(1, 600), st.floats(0.5, 60.0), st.floats(0.0, 0.5), st.floats(0.5, 0.99))
+def test_closed_form_equals_bisection(a, b, c, p, q, n_x, n_hat_w, budget, t_pred, amax):
+    abc, pq = (a, b, c), (p, q)
+    got, feas = C.alpha_star(abc, pq, n_x, n_hat_w, budget, t_pred, amax)
+    ref, rfeas = _bisect_alpha(abc, pq, n_x, n_hat_w, budget, t_pred, amax)
+    if n_hat_w <= 1:
+        assert got == 0.0
+        return
+    assert feas == rfeas
+    assert abs(got - ref) < 1e-9
+
+
+def test_printed_second_term_disagrees():
+    """The printed closed form divides (N_hat_W - 2)/2 by p N_x; it does not
+    solve the constraint, the derived (N_hat_W - 2)/(2 N_x) does."""
+    e = _ex()
+    (a, b, c), (p, q) = e["prefill_abc"], e["step_pq"]
+    n_x, nw, T = e["n_x"], e["n_hat_w"], e["budget"]
+    pre = a * n_x ** 2 + b * n_x + c
+    printed = 1 - (T - pre) / (p * n_x * (nw - 1)) + (nw - 2) / (2 * p * n_x) + q / (p * n_x)
+    derived = 1 - (T - pre) / (p * n_x * (nw - 1)) + (nw - 2) / (2 * n_x) + q / (p * n_x)
+    assert abs(derived - e["alpha_star"]) < 1e-12
+    assert abs(printed - e["alpha_star"]) > 1.0
+
+
+def test_decoding_phase_explicit_sum():
+    pq = (2e-5, 3e-3)
+    for n_x, alpha, nh in [(1000, 0.0, 1), (1000, 0.3, 2), (4096, 0.5, 65), (32768, 0.95, 257)]:
+        want = sum(pq[0] * ((1 - alpha) * n_x + i - 1) + pq[1] for i in range(1, nh))
+        assert abs(C.t_decoding_phase(pq, n_x, alpha, nh) - want) < 1e-12
+
+
+def test_fit_poly_recovers_exact_and_matches_polyfit():
+    n = np.linspace(0, 32768, 41)
+    t = 3e-9 * n ** 2 + 2e-5 * n + 0.04
+    assert np.allclose(C.fit_poly(n, t, 2), [3e-9, 2e-5, 0.04], rtol=1e-8, atol=1e-12)
+    rng = np.random.default_rng(5)
+    tn = 7e-6 * n + 0.02 + rng.normal(0, 1e-4, n.size)
+    assert np.allclose(C.fit_poly(n, tn, 1), np.polyfit(n, tn, 1), rtol=1e-9)
+
+
+# ---------------------------------------------------------------- C ABI vs reference
+@pytest.mark.parametrize("degree", [1, 2])
+def test_abi_fit_matches_reference(degree):
+    rng = np.random.default_rng(degree)
+    for _ in range(20):
+        n = np.sort(rng.uniform(0, 32768, rng.integers(degree + 1, 60)))
+        t = rng.uniform(0, 1e-9) * n ** 2 * (degree == 2) + rng.uniform(0, 1e-4) * n + \
+            rng.uniform(0, 0.1) + rng.normal(0, 1e-5, n.size)
+        got = _lib.tb_ete_fit(n.tolist(), t.tolist(), degree)
+        ref = C.fit_poly(n, t, degree)
+        V = np.vander(n, degree + 1)                                # compare the fitted curves
+        assert np.abs(V @ np.array(got) - V @ ref).max() <= 1e-9 * np.abs(t).max()
+    with pytest.raises(ValueError):
+        _lib.tb_ete_fit([1.0], [2.0], 1)
+    with pytest.raises(ValueError):
+        _lib.tb_ete_fit([3.0, 3.0, 3.0], [1.0, 2.0, 3.0], 1)
+
+
+@settings(max_examples=200, deadline=None)
+@given(st.floats(0.0, 1e-6), st.floats(0.0, 1e-3), st.floats(0.0, 1.0),
+       st.floats(1e-6, 1e-3), st.floats(1e-4, 0.1), st.integers(100, 32768),
+       st.integers(0, 600), st.floats(0.1, 60.0), st.floats(0.0, 0.5), st.floats(0.5, 0.99),
+       st.floats(0.0, 0.99))
+def test_abi_wcet_and_alpha_match_reference(a, b, c, p, q, n_x, n_hat_w, budget, t_pred, amax,
+                                            alpha):
+    abc, pq = (a, b, c), (p, q)
+    w_ref = C.t_wcet(abc, pq, n_x, alpha, n_hat_w)
+    assert math.isclose(_lib.tb_wcet(abc, pq, n_x, alpha, n_hat_w), w_ref, rel_tol=1e-10,
+                        abs_tol=1e-12)
+    got, feas = _lib.tb_alpha_star(abc, pq, n_x, n_hat_w, budget, t_pred, amax)
+    ref, rfeas = C.alpha_star(abc, pq, n_x, n_hat_w, budget, t_pred, amax)
+    assert feas == rfeas
+    assert math.isclose(got, ref, rel_tol=1e-12, abs_tol=1e-12)
+
+
+def test_abi_alpha_edges():
+    e = _ex()
+    got, feas = _lib.tb_alpha_star(e["prefill_abc"], e["step_pq"], e["n_x"], e["n_hat_w"],
+                                   e["budget"], e["t_predict"], e["alpha_max"])
+    assert feas and abs(got - e["alpha_star"]) < 1e-12
+    assert _lib.tb_alpha_star(e["prefill_abc"], e["step_pq"], e["n_x"], 101, 1e6, 0.0, 0.95) == (0.0, True)
+    assert _lib.tb_alpha_star(e["prefill_abc"], e["step_pq"], e["n_x"], 101, 5.0, 0.0, 0.95) == (0.95, False)
+    assert _lib.tb_alpha_star(e["prefill_abc"], e["step_pq"], e["n_x"], 1, 5.0, 0.0, 0.95) == (0.0, True)
+    assert math.isnan(_lib.tb_alpha_star(e["prefill_abc"], e["step_pq"], 0.0, 101, 5.0, 0.0, 0.95)[0])
+
+
+def test_choose_alpha_matches_reference():
+    from paper_2512_21859_amd.pipeline import choose_alpha
+    e = _ex()
+    L = e["lengths"]
+    for c in L["cases"]:
+        for budget in (0.5, 2.0, 5.0, 50.0):
+            got = choose_alpha(e["prefill_abc"], e["step_pq"], e["n_x"], c["n_hat"], L["bucket"],
+                               L["k"], L["n_max"], budget, 0.1, 0.95)
+            nw = C.pessimistic_length(C.predicted_length(c["n_hat"], L["bucket"], L["n_max"]),
+                                      L["k"], L["n_max"])
+            ref = C.alpha_star(e["prefill_abc"], e["step_pq"], e["n_x"], nw, budget, 0.1, 0.95)
+            assert got[2] == nw == c["N_hat_W"]
+            assert got[1] == ref[1] and abs(got[0] - ref[0]) < 1e-12
