@@ -44,6 +44,12 @@ def _parse():
                     help="minimum CPU time of the oracle baseline sample")
     ap.add_argument("--no-long-context", action="store_true",
                     help="skip the supplementary long-context decode measurement")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the cold-cache decode measurement (caches rotated over 1 GiB)")
+    ap.add_argument("--no-layer-sweep", action="store_true",
+                    help="skip the supplementary 28-layer L=32768 ratio sweep")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the 2 GiB read / copy bandwidth ceilings")
     ap.add_argument("--pmc-calibration", action="store_true",
                     help="first copy 512 MiB device-to-device twice (a kernel of known "
                          "traffic for scaling hardware byte counters)")
@@ -147,6 +153,9 @@ def long_context(torch, _lib, synth, Evictor, dev, steps=64, alpha=0.5):
         ev_ms.append(e0.elapsed_time(e1))
         de_ms.append(e1.elapsed_time(e2))
     ev_t, de_t = min(ev_ms), min(de_ms)
+    sc_t = _best_ms(torch, lambda: ev.score(q_win, k, [L], stream))
+    se_t = _best_ms(torch, lambda: ev.select([L], [alpha], stream))
+    co_t = _best_ms(torch, lambda: cache.compact_from(k, v, ev.keep_idx, [nk], stream))
     dbytes = sum(_decode_bytes(Hq, Hkv, d, nk + t + 1) for t in range(steps)) / steps
     per_step_us = de_t * 1e3 / steps
     cbytes = 2 * 2 * Hkv * nk * d * 2
@@ -159,9 +168,192 @@ def long_context(torch, _lib, synth, Evictor, dev, steps=64, alpha=0.5):
         "decode_frac_of_8TBps": round(dbytes / (per_step_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
         "bytes_per_step": round(dbytes),
         "evict_us": round(ev_t * 1e3, 1),
+        "score_us": round(sc_t * 1e3, 1),
+        "select_us": round(se_t * 1e3, 1),
+        "compact_us": round(co_t * 1e3, 1),
         "compaction_bytes": cbytes,
+        "compact_GBps": round(cbytes / (co_t * 1e-3) / 1e9, 1),
+        "compact_frac_of_8TBps": round(cbytes / (co_t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "timing": "best of 3: HIP events around the eviction and around a graph of the decode steps",
     }
+
+
+def _best_ms(torch, fn, reps=3, stream=None):
+    """Best of ``reps`` HIP-event timings of fn() on the current stream, in ms."""
+    stream = torch.cuda.current_stream() if stream is None else stream
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    best = float("inf")
+    for _ in range(reps):
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    return best
+
+
+def hbm_ceiling(torch, dev, nbytes=2 << 30):
+    """Practical bandwidth ceilings over 2 GiB buffers: a streaming read (a
+    library sum) and a device-to-device copy, best of 5."""
+    x = torch.ones((nbytes // 4,), dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+    x.sum()
+    y.copy_(x)
+    torch.cuda.synchronize()
+    rd = _best_ms(torch, lambda: x.sum(), reps=5)
+    cp = _best_ms(torch, lambda: y.copy_(x), reps=5)
+    del x, y
+    torch.cuda.empty_cache()
+    return {"read_GBps": round(nbytes / (rd * 1e-3) / 1e9, 1),
+            "copy_GBps": round(2 * nbytes / (cp * 1e-3) / 1e9, 1),
+            "bytes": nbytes,
+            "how": "torch sum (read) and copy_ (read + write) over 2 GiB fp32 buffers, "
+                   "HIP events, best of 5"}
+
+
+def cold_decode(torch, _lib, Evictor, dev, wl, q_win, k, v, qd, knd, vnd,
+                target_bytes=1 << 30):
+    """Decode at ratio 0 for the L = 8192 workload with the step's cache
+    rotated over enough copies (>= 1 GiB in total) that every step reads its
+    cache from HBM rather than the 256 MB last-level cache."""
+    B, Hq, Hkv, d, w, L, T = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L, wl.T
+    per_cache = 2 * Hkv * (L + T) * d * 2
+    R = -(-target_bytes // per_cache)
+    ev = Evictor(B, L, Hq, Hkv, d, w, wl.pool, device=dev)
+    caches = [_lib.KVCache(B, Hq, Hkv, L + T, d, wl.dtype, device=dev) for _ in range(R)]
+    out = torch.empty((T, B, Hq, d), dtype=wl.dtype, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def reset():
+        for c in caches:
+            ev.evict(q_win, k, v, [L], [0.0], c, stream)
+
+    reset()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    cs = torch.cuda.Stream()
+    with torch.cuda.graph(g, stream=cs):
+        for t in range(T):
+            c = caches[t % R]
+            _lib.tb_decode_attn(qd[t], knd[t], vnd[t], c.k, c.v, c.kv_len, out[t], c.ws,
+                                stream=cs)
+    torch.cuda.synchronize()
+    best = float("inf")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(3):
+        reset()
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    # rows attended at step t: L + (number of earlier appends to that cache) + 1
+    dbytes = sum(_decode_bytes(Hq, Hkv, d, L + t // R + 1) for t in range(T))
+    us = best * 1e3 / T
+    del caches, ev
+    torch.cuda.empty_cache()
+    return {"workload": f"bf16, B=1, L={L}, 28 q / 4 kv heads, d=128, ratio 0, {T} decode "
+                        f"steps rotating over {R} caches ({R * per_cache / 2**30:.2f} GiB)",
+            "decode_us_per_step": round(us, 3),
+            "decode_GBps": round(dbytes / T / (us * 1e-6) / 1e9, 1),
+            "decode_frac_of_8TBps": round(dbytes / T / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "timing": "best of 3: HIP events around a graph of the decode steps"}
+
+
+def layer_sweep(torch, _lib, synth, Evictor, dev, T=None):
+    """Supplementary: the 28-layer model shape at L = 32768 (28 q / 4 kv heads,
+    d = 128, w = 32, pool 7) over the ratios k/20, k = 0..19.  Per ratio: evict
+    every layer, then decode T tokens, one token being the decode step of all
+    28 layers in order, replayed from a graph.  The per-token time is fitted
+    against the retained length with the execution-time model's decode-step
+    form t = p N_kv + q (least squares, computed by tb_ete_fit)."""
+    wl = synth.WORKLOADS[3]
+    T = wl.T if T is None else T
+    B, Hq, Hkv, d, w, L, nl = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L, wl.layers
+    lay = []
+    for layer in range(nl):
+        pr = synth.make_prompt(wl, layer)
+        dc = synth.make_decode(wl, layer, T=T)
+        lay.append({x: pr[x].to(dev) for x in ("q_win", "k", "v")})
+        lay[-1].update({x: dc[x].to(dev) for x in ("q", "k_new", "v_new")})
+        del pr, dc
+    ev = Evictor(B, L, Hq, Hkv, d, w, wl.pool, device=dev)
+    stream = torch.cuda.current_stream()
+    cs = torch.cuda.Stream()
+    rows = []
+    for a in wl.alphas:
+        nk = _lib.tb_keep_count(L, a, w)
+        caches = [_lib.KVCache(B, Hq, Hkv, nk + T, d, wl.dtype, device=dev) for _ in range(nl)]
+        out = torch.empty((T, nl, B, Hq, d), dtype=wl.dtype, device=dev)
+
+        def evict_all():
+            for layer in range(nl):
+                x = lay[layer]
+                ev.evict(x["q_win"], x["k"], x["v"], [L], [a], caches[layer], stream)
+
+        evict_all()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cs):
+            for t in range(T):
+                for layer in range(nl):
+                    x, c = lay[layer], caches[layer]
+                    _lib.tb_decode_attn(x["q"][t], x["k_new"][t], x["v_new"][t], c.k, c.v,
+                                        c.kv_len, out[t, layer], c.ws, stream=cs)
+        torch.cuda.synchronize()
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        ev_best, de_best = float("inf"), float("inf")
+        for _ in range(2):
+            e0.record(stream)
+            evict_all()
+            e1.record(stream)
+            g.replay()
+            e2.record(stream)
+            torch.cuda.synchronize()
+            ev_best = min(ev_best, e0.elapsed_time(e1))
+            de_best = min(de_best, e1.elapsed_time(e2))
+        tok_us = de_best * 1e3 / T
+        dbytes = nl * sum(_decode_bytes(Hq, Hkv, d, nk + t + 1) for t in range(T)) / T
+        rows.append({"alpha": a, "n_keep": nk,
+                     "us_per_token": round(tok_us, 2),
+                     "tokens_per_s": round(1e6 / tok_us, 1),
+                     "decode_GBps": round(dbytes / (tok_us * 1e-6) / 1e9, 1),
+                     "evict_all_layers_us": round(ev_best * 1e3, 1)})
+        del g, caches, out
+        torch.cuda.empty_cache()
+    # eviction stages of one layer at ratio 0.5 (scores do not depend on the ratio)
+    a = 0.5
+    nk = _lib.tb_keep_count(L, a, w)
+    cache = _lib.KVCache(B, Hq, Hkv, nk, d, wl.dtype, device=dev)
+    x = lay[0]
+    sc_t = _best_ms(torch, lambda: ev.score(x["q_win"], x["k"], [L], stream))
+    se_t = _best_ms(torch, lambda: ev.select([L], [a], stream))
+    co_t = _best_ms(torch, lambda: cache.compact_from(x["k"], x["v"], ev.keep_idx, [nk], stream))
+    cbytes = 2 * 2 * Hkv * nk * d * 2
+    stages = {"alpha": a, "score_us": round(sc_t * 1e3, 1), "select_us": round(se_t * 1e3, 1),
+              "compact_us": round(co_t * 1e3, 1),
+              "compact_GBps": round(cbytes / (co_t * 1e-3) / 1e9, 1),
+              "score_window_flops": 2 * Hq * w * L * d,
+              "score_fp64_TFLOPs": round(2 * Hq * w * L * d / (sc_t * 1e-3) / 1e12, 2)}
+    del cache
+    xs = [r["n_keep"] + (T + 1) / 2 for r in rows]
+    ys = [r["us_per_token"] for r in rows]
+    p, q = _lib.tb_ete_fit(xs, ys, 1)
+    pred = [p * x + q for x in xs]
+    my = sum(ys) / len(ys)
+    ss_res = sum((y - f) ** 2 for y, f in zip(ys, pred))
+    ss_tot = sum((y - my) ** 2 for y in ys)
+    del lay, ev
+    torch.cuda.empty_cache()
+    return {"workload": f"bf16, B=1, {nl} layers, L={L}, 28 q / 4 kv heads, d=128, w=32, "
+                        f"pool 7, ratios k/20 (k = 0..19), {T} decode tokens per ratio",
+            "per_alpha": rows,
+            "evict_one_layer": stages,
+            "token_time_fit": {"p_us_per_kv_row": p, "q_us": q,
+                               "r2": 1 - ss_res / ss_tot if ss_tot > 0 else 1.0,
+                               "mape_pct": 100.0 * sum(abs(f - y) / y for y, f in zip(ys, pred)) / len(ys)},
+            "timing": "best of 2: HIP events around the 28 evictions and around a graph of "
+                      f"{T} x {nl} decode launches"}
 
 
 def main():
@@ -330,8 +522,17 @@ def main():
                                     "length over the ratio sweep (tb_ete_fit)"},
         "wall_s": round(wall, 3),
     }
+    if not args.no_cold:
+        result["cold_decode"] = cold_decode(torch, _lib, Evictor, dev, wl, q_win, k, v,
+                                            qd, knd, vnd)
+    del caches, graphs, outs
+    torch.cuda.empty_cache()
     if not args.no_long_context:
         result["long_context"] = long_context(torch, _lib, synth, Evictor, dev)
+    if not args.no_layer_sweep:
+        result["layer_sweep"] = layer_sweep(torch, _lib, synth, Evictor, dev)
+    if not args.no_ceiling:
+        result["hbm_ceiling"] = hbm_ceiling(torch, dev)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, pr, dc, args.cpu_seconds)
     print(json.dumps(result), flush=True)
