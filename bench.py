@@ -50,6 +50,9 @@ def _parse():
                     help="skip the supplementary 28-layer L=32768 ratio sweep")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the 2 GiB read / copy bandwidth ceilings")
+    ap.add_argument("--only", choices=("cold", "long", "layers", "ceiling"),
+                    help="run one supplementary measurement alone and print its JSON "
+                         "(for profiling that workload by itself)")
     ap.add_argument("--pmc-calibration", action="store_true",
                     help="first copy 512 MiB device-to-device twice (a kernel of known "
                          "traffic for scaling hardware byte counters)")
@@ -378,6 +381,12 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.only in ("long", "layers", "ceiling"):
+        fn = {"long": lambda: long_context(torch, _lib, synth, Evictor, dev),
+              "layers": lambda: layer_sweep(torch, _lib, synth, Evictor, dev),
+              "ceiling": lambda: hbm_ceiling(torch, dev)}[args.only]
+        print(json.dumps({"section": args.only, **fn()}), flush=True)
+        return
     wl = synth.WORKLOADS[2]
     B, Hq, Hkv, d, w, L, T = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L, wl.T
     pr = synth.make_prompt(wl)
@@ -385,6 +394,10 @@ def main():
     q_win, k, v = (pr[x].to(dev) for x in ("q_win", "k", "v"))
     qd, knd, vnd = (dc[x].to(dev) for x in ("q", "k_new", "v_new"))
 
+    if args.only == "cold":
+        print(json.dumps({"section": "cold", **cold_decode(torch, _lib, Evictor, dev, wl, q_win,
+                                                            k, v, qd, knd, vnd)}), flush=True)
+        return
     ev = Evictor(B, L, Hq, Hkv, d, w, wl.pool, device=dev)
     stream = torch.cuda.current_stream()
     n_keep = {a: _lib.tb_keep_count(L, a, w) for a in wl.alphas}

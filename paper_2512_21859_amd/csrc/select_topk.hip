@@ -4,13 +4,23 @@
 // One block of 1024 threads per (sequence, KV head).  Scores are >= 0, so
 // their IEEE bit patterns order like the values; the selection is integer
 // work and bit-exact:
-//   1. radix select (4 passes of 8 bits, LDS histograms) finds the key tau of
-//      the n_sel-th largest score and how many tau-valued positions to take;
-//   2. an ordered emit walks the prefix in tiles of 4096 positions (4 per
+//   0. one pass over the prefix finds the largest and smallest key; the bits
+//      above their highest differing bit are common to every key, so the radix
+//      search starts just below them (digits spread over bins from the first
+//      pass instead of piling into the one or two bins the exponent's top bits
+//      give, which would serialise the LDS atomics);
+//   1. radix select with digits of up to 11 bits (at most 3 passes) finds the
+//      key tau of the n_sel-th largest score and how many tau-valued positions
+//      to take (histogram bins are replicated per lane group to spread
+//      same-bin atomics over LDS banks);
+//   2. an ordered emit walks the prefix in tiles of 16384 positions (16 per
 //      thread, contiguous), with one block-wide exclusive scan of the packed
 //      counts (greater-than-tau, equal-to-tau) per tile.  Positions equal to
 //      tau are taken lowest index first, so a thread's output offset is
 //      (#greater before it) + min(#equal before it, equal-needed).
+// A prefix of up to 32768 positions is read from HBM once and kept in LDS for
+// every pass; a longer one is re-read (from L2) by each pass and staged
+// through the same LDS buffer one emit tile at a time.
 
 #include "common.h"
 #include "kernels.h"
@@ -20,8 +30,11 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
-constexpr int kPer = 4;                       // positions per thread per tile
-constexpr int kTileN = kThreads * kPer;
+constexpr int kBits = 11;
+constexpr int kBins = 1 << kBits;
+constexpr int kPer = 16;                      // positions per thread per emit tile
+constexpr int kTileN = kThreads * kPer;       // 16384
+constexpr int kCacheN = 32768;                // prefix kept in LDS when it fits
 
 __device__ __forceinline__ uint32_t key_of(float f) {
   return __float_as_uint(f) & 0x7fffffffu;    // scores are >= 0 (-0 -> 0)
@@ -57,6 +70,44 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
   return res;
 }
 
+// Block-wide max and min of 32-bit keys (every thread gets both).
+__device__ __forceinline__ void block_max_min(uint32_t& mx, uint32_t& mn, uint32_t* s_wave) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    mx = max(mx, static_cast<uint32_t>(__shfl_xor(mx, off)));
+    mn = min(mn, static_cast<uint32_t>(__shfl_xor(mn, off)));
+  }
+  if (lane == 0) { s_wave[wave] = mx; s_wave[kWaves + wave] = mn; }
+  __syncthreads();
+  mx = 0u;
+  mn = 0xffffffffu;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) { mx = max(mx, s_wave[i]); mn = min(mn, s_wave[kWaves + i]); }
+  __syncthreads();
+}
+
+// Visit every prefix position j < n once, as f(j, key): each thread takes kU
+// positions per round, strided by the block size, all loaded before any is used
+// (indices clamped, results masked) so a round's loads are in flight together.
+constexpr int kU = 16;
+template <typename Load, typename F>
+__device__ __forceinline__ void for_each_key(int n, Load load, F f) {
+  const int tid = threadIdx.x;
+  for (int j0 = 0; j0 < n; j0 += kThreads * kU) {
+    uint32_t k[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) k[u] = load(min(j0 + u * kThreads + tid, n - 1));
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int j = j0 + u * kThreads + tid;
+      if (j < n) f(j, k[u]);
+    }
+  }
+}
+
+template <bool CACHED>
 __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
   const int g = blockIdx.x, b = blockIdx.y;
   const int L = a.L[b], w = a.w, pref = L - w;
@@ -66,7 +117,11 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
   int32_t* out = a.keep_idx + bg * a.Lmax;
   const int tid = threadIdx.x;
 
-  __shared__ uint32_t hist[256];
+  // Each bin has kRep interleaved copies (lane % kRep picks one), so lanes of a
+  // wave that hit the same bin mostly update different LDS banks.
+  constexpr int kRep = CACHED ? 2 : 8;
+  __shared__ uint32_t s_keys[CACHED ? kCacheN : kTileN];   // the prefix, or one emit tile
+  __shared__ uint32_t hist[kBins * kRep];
   __shared__ uint32_t s_wave[2 * kWaves + 1];
   __shared__ uint32_t s_digit, s_rank;
 
@@ -77,45 +132,55 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
     return;
   }
 
-  // 1. radix select of the n_sel-th largest key.
-  uint32_t prefix = 0u, mask = 0u, rank = static_cast<uint32_t>(n_sel);
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int i = tid; i < 256; i += kThreads) hist[i] = 0u;
+  // 0. key range (and the LDS copy of the prefix)
+  const auto from_hbm = [&](int j) { return key_of(sc[j]); };
+  const auto from_lds = [&](int j) { return s_keys[j]; };
+  uint32_t kmax = 0u, kmin = 0xffffffffu;
+  for_each_key(pref, from_hbm, [&](int j, uint32_t k) {
+    if (CACHED) s_keys[j] = k;
+    kmax = max(kmax, k);
+    kmin = min(kmin, k);
+  });
+  block_max_min(kmax, kmin, s_wave);          // ends with a barrier
+  const uint32_t diff = kmax ^ kmin;
+  // bits [lo, 31) still to resolve; keys are < 2^31, so the common part of the
+  // keys above bit lo is kmax's
+  int lo = diff ? 32 - __clz(diff) : 1;
+  uint32_t mask = ~((1u << lo) - 1u) & 0x7fffffffu;
+  uint32_t prefix = kmax & mask;
+  uint32_t rank = static_cast<uint32_t>(n_sel);
+
+  // 1. radix select of the n_sel-th largest key among those matching prefix.
+  while (lo > 0) {
+    const int shift = max(lo - kBits, 0);
+    const uint32_t dmask = (1u << (lo - shift)) - 1u;
+    for (int i = tid; i < kBins * kRep; i += kThreads) hist[i] = 0u;
     __syncthreads();
-    for (int j = tid; j < pref; j += kThreads) {
-      const uint32_t k = key_of(sc[j]);
-      if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+    const uint32_t rep = tid % kRep;
+    const auto count = [&](int, uint32_t k) {
+      if ((k & mask) == prefix) atomicAdd(&hist[((k >> shift) & dmask) * kRep + rep], 1u);
+    };
+    if (CACHED) for_each_key(pref, from_lds, count);
+    else        for_each_key(pref, from_hbm, count);
+    __syncthreads();
+    // thread t holds bins kBins-1-2t and kBins-2-2t (descending digit order)
+    uint32_t c0 = 0u, c1 = 0u;
+#pragma unroll
+    for (int r = 0; r < kRep; ++r) {
+      c0 += hist[(kBins - 1 - 2 * tid) * kRep + r];
+      c1 += hist[(kBins - 2 - 2 * tid) * kRep + r];
     }
-    __syncthreads();
-    if (tid < 64) {
-      // lane holds digits 255-4*lane .. 252-4*lane (descending)
-      uint32_t cnt[4], local = 0u;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) { cnt[q] = hist[255 - (4 * tid + q)]; local += cnt[q]; }
-      uint32_t incl = local;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t y = __shfl_up(incl, off);
-        if (tid >= off) incl += y;
-      }
-      const uint32_t excl = incl - local;
-      if (excl < rank && rank <= incl) {
-        uint32_t accum = excl;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if (accum + cnt[q] >= rank) {
-            s_digit = 255u - static_cast<uint32_t>(4 * tid + q);
-            s_rank = rank - accum;
-            break;
-          }
-          accum += cnt[q];
-        }
-      }
+    uint32_t total;
+    const uint32_t ex = block_exclusive_scan(c0 + c1, s_wave, total);
+    if (ex < rank && rank <= ex + c0 + c1) {
+      if (ex + c0 >= rank) { s_digit = kBins - 1 - 2 * tid; s_rank = rank - ex; }
+      else                 { s_digit = kBins - 2 - 2 * tid; s_rank = rank - ex - c0; }
     }
     __syncthreads();
     prefix |= s_digit << shift;
-    mask |= 255u << shift;
+    mask |= dmask << shift;
     rank = s_rank;
+    lo = shift;
     __syncthreads();
   }
   const uint32_t tau = prefix;
@@ -124,28 +189,33 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
   // 2. ordered emit.
   uint32_t gt_run = 0u, eq_run = 0u;
   for (int base = 0; base < pref; base += kTileN) {
+    const uint32_t* tk = s_keys + (CACHED ? base : 0);
+    if (!CACHED) {
+      for_each_key(min(kTileN, pref - base), [&](int i) { return key_of(sc[base + i]); },
+                   [&](int i, uint32_t k) { s_keys[i] = k; });
+      __syncthreads();
+    }
     const int j0 = base + tid * kPer;
     uint32_t gt = 0u, eq = 0u, kk[kPer];
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
       const int j = j0 + q;
-      kk[q] = (j < pref) ? key_of(sc[j]) : 0u;
       const bool in = j < pref;
+      kk[q] = in ? tk[tid * kPer + q] : 0u;
       gt += (in && kk[q] > tau) ? 1u : 0u;
       eq += (in && kk[q] == tau) ? 1u : 0u;
     }
     uint32_t total;
+    // counts per thread <= 16 and per tile <= 16384 fit the 16-bit halves
     const uint32_t ex = block_exclusive_scan(gt | (eq << 16), s_wave, total);
-    uint32_t gt_before = gt_run + (ex & 0xffffu);
     uint32_t eq_before = eq_run + (ex >> 16);
-    uint32_t pos = gt_before + min(eq_before, need_eq);
+    uint32_t pos = gt_run + (ex & 0xffffu) + min(eq_before, need_eq);
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
       const int j = j0 + q;
-      if (j >= pref) break;
-      if (kk[q] > tau) {
+      if (j < pref && kk[q] > tau) {
         out[pos++] = j;
-      } else if (kk[q] == tau) {
+      } else if (j < pref && kk[q] == tau) {
         if (eq_before < need_eq) out[pos++] = j;
         ++eq_before;
       }
@@ -159,7 +229,10 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t st) {
   const dim3 grid(a.Hkv, a.B);
-  select_kernel<<<grid, kThreads, 0, st>>>(a);
+  int max_pref = 0;
+  for (int b = 0; b < a.B; ++b) max_pref = max(max_pref, a.L[b] - a.w);
+  if (max_pref <= kCacheN) select_kernel<true><<<grid, kThreads, 0, st>>>(a);
+  else                     select_kernel<false><<<grid, kThreads, 0, st>>>(a);
   return hipGetLastError();
 }
 

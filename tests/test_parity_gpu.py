@@ -159,6 +159,36 @@ def test_select_exact_plateaus(levels):
         _select_case(pooled, L, w, alphas, f"levels={levels} alphas={alphas}")
 
 
+def test_select_exact_long_prefix_and_wide_range():
+    case("select beyond the LDS-cached prefix length, keys over the whole float range")
+    rng = np.random.default_rng(77)
+    B, Hkv, w = 2, 2, 32
+    L = [40000, 33000]            # prefixes 39968 and 32968 (> 32768: read from L2 per pass)
+    pooled = np.zeros((B, Hkv, max(L)))
+    for b in range(B):
+        n = L[b] - w
+        x = 10.0 ** rng.uniform(-44, 3, (Hkv, n))          # includes fp32 subnormals
+        x[:, rng.integers(0, n, n // 50)] = 0.0             # exact zeros
+        x[:, 1000:1100] = x[:, 1000:1001]                   # a long plateau
+        pooled[b, :, :n] = x
+    for alphas in ([0.0, 0.3], [0.5, 0.9], [0.999, 0.01]):
+        _select_case(pooled, L, w, alphas, f"alphas={alphas}")
+
+
+def test_select_exact_narrow_range():
+    case("select on keys that share all but their lowest bits")
+    rng = np.random.default_rng(5)
+    B, Hkv, w = 1, 2, 8
+    L = [3000]
+    base = np.float32(0.125)
+    pooled = np.zeros((B, Hkv, L[0]))
+    bits = np.frombuffer(base.tobytes(), dtype=np.uint32)[0]
+    low = rng.integers(0, 4, (Hkv, L[0] - w)).astype(np.uint32)      # differ in 2 bits only
+    pooled[0, :, : L[0] - w] = (bits + low).view(np.float32).astype(np.float64)
+    for alphas in ([0.1], [0.5], [0.97]):
+        _select_case(pooled, L, w, alphas, f"alphas={alphas}")
+
+
 # ------------------------------------------------------------------ scoring
 @pytest.mark.parametrize("dtype,d,G,w,pool,L", [
     (torch.float32, 64, 2, 16, 5, [512]),
