@@ -3,24 +3,33 @@
 //
 // Precision.  The selection that follows is compared position by position, so
 // scores are kept to ~1e-7 relative: dot products of the (exact) bf16/fp32
-// inputs are accumulated in float64, exponentials are float64, and sums are
-// float64.  Only the per-tile exponentials and the raw scores are stored as
-// fp32 (relative rounding 6e-8 each); pooling is a max, so it is exact.
+// inputs are accumulated in float64, exponent arguments are reduced in float64,
+// and sums are float64.  The per-logit exponentials (fp32, within ~1.5e-7
+// relative) and the raw scores (fp32 rounding, 6e-8) are the only
+// single-precision values; pooling is a max, so it is exact.
 //
 // Four kernels, all with fixed-order reductions (no atomics):
-//   K1 score_tiles: block = (64-key tile, <=256 window rows) of one KV head;
-//      wave w owns 64 rows x the 64 keys.  Window queries and keys are staged
-//      in LDS in 32-wide d chunks; the float64 dot products run on the matrix
-//      cores (v_mfma_f64_16x16x4_f64, 4 x 4 tiles of 16 x 16 per wave).  Each
-//      row's 64 logits sit in one 16-lane DPP row, so the causal mask, the tile
-//      max m and z = sum exp(s - m) need no LDS.  Stores e = exp(s - m) (fp32)
-//      and (m, z) per (row, tile).
+//   K1 score_tiles: block = (64-key tile, <=256 window rows) of one KV head,
+//      512 threads; wave w owns 32 rows x the 64 keys (waves whose rows are all
+//      padding skip the products).  Window queries and keys are staged in LDS
+//      in 32-wide d chunks, the next chunk's global loads in flight while the
+//      current one is multiplied; the float64 dot products run on the matrix
+//      cores (v_mfma_f64_16x16x4_f64, 2 x 4 tiles of 16 x 16 per wave).  Each
+//      row's 64 logits sit in one 16-lane DPP row, so the causal mask, a tile
+//      reference m (the row's largest dot product rounded to fp32) and
+//      z = sum exp(s - m) need no LDS.  Stores e = exp(s - m) (fp32, one float4
+//      per lane and row: keys r, r+16, r+32, r+48) and (m, z) per (row, tile).
 //   K2 row_stats: one wave per window row merges its tiles' (m, z) into the
 //      row's global max M and normaliser Z.
 //   K3 score_accum: block = 64 prefix columns; A[j] = sum_r e[r][j] *
 //      exp(m[r][tile] - M[r]) / Z[r] in float64 (four row groups, four
 //      independent accumulators each, combined in a fixed order); raw A as fp32.
 //   K4 pool: max of the raw scores over |j - j'| <= pool/2 within the prefix.
+//
+// The per-logit exponential is the one place fp64 arithmetic is avoided: on
+// this part the fp64 vector instructions compete with the fp64 matrix
+// instructions for the same throughput, so K1's epilogue reduces the argument
+// in fp64 (exactly) and evaluates 2^f for |f| <= 1/2 in fp32.
 
 #include "common.h"
 #include "kernels.h"
@@ -47,6 +56,15 @@ __device__ __forceinline__ void load8<float>(const float* p, float* out) {
   Elem<float>::widen(ldg16(p + 4), out + 4);
 }
 
+// 2^t as fp32 for a float64 t >= -300: t = n + f with n = round(t) exact and
+// |f| <= 1/2, so only f is rounded to fp32 (relative effect on 2^f below
+// 3e-8); 2^f comes from the hardware base-2 exponential (about 1 ulp) and the
+// scaling by 2^n is exact (results under the smallest fp32 subnormal are 0).
+__device__ __forceinline__ float exp2_split(double t) {
+  const double n = rint(t);
+  return ldexpf(__builtin_amdgcn_exp2f(static_cast<float>(t - n)), static_cast<int>(n));
+}
+
 template <int CTRL>
 __device__ __forceinline__ double dpp_f64(double x) {
   const uint64_t u = __double_as_longlong(x);
@@ -71,9 +89,23 @@ __device__ __forceinline__ double row16_sum_f64(double x) {
   x += dpp_f64<kDppRowMirror>(x);
   return x;
 }
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row16_max_f32(float x) {
+  x = fmaxf(x, dpp_f32<kDppQuadXor1>(x));
+  x = fmaxf(x, dpp_f32<kDppQuadXor2>(x));
+  x = fmaxf(x, dpp_f32<kDppRowHalfMirror>(x));
+  x = fmaxf(x, dpp_f32<kDppRowMirror>(x));
+  return x;
+}
+
+constexpr int kTilesThreads = 512;
+constexpr int kWaveRows = 32;      // window rows per wave in score_tiles
 
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads, 2) void score_tiles_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(kTilesThreads, 2) void score_tiles_kernel(ScoreArgs a) {
   const int tile = blockIdx.x / a.row_chunks, rc = blockIdx.x % a.row_chunks;
   const int g = blockIdx.y, b = blockIdx.z;
   const int L = a.L[b];
@@ -84,102 +116,129 @@ __global__ __launch_bounds__(kThreads, 2) void score_tiles_kernel(ScoreArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q4 = lane >> 4, r16 = lane & 15;
+  const bool active = row0 + kWaveRows * wave < R;    // wave-uniform: not all padding
 
   __shared__ float qs[kRows][kDC + 1];             // +1: conflict-free column reads
   __shared__ float ks[kT][kDC + 1];
+  __shared__ int s_lim[kRows];                     // last key a row sees (-1: padding)
+  if (tid < kRows) {
+    const int r = row0 + tid;
+    s_lim[tid] = r < R ? min(L - 1, L - w + r % w) : -1;
+  }
 
-  f64x4 acc[4][4];
+  // Staging: two threads per window row (16 elements each) and, for the first
+  // 256 threads, four threads per key (8 elements each).
+  const int qrow = tid >> 1, qoff = (tid & 1) * 16;
+  const bool qvalid = row0 + qrow < R;
+  const T* qsrc = nullptr;
+  if (qvalid) {
+    const int r = row0 + qrow, h = g * G + r / w, i = r % w;
+    qsrc = static_cast<const T*>(a.q_win) + ((static_cast<size_t>(b) * a.Hq + h) * w + i) * D + qoff;
+  }
+  const int kk = (tid & 255) >> 2, kdp = (tid & 3) * 8;
+  const bool kvalid = tid < 256 && kbase + kk < L;
+  const T* ksrc = static_cast<const T*>(a.k) +
+                  ((static_cast<size_t>(b) * a.Hkv + g) * a.Lmax + kbase + kk) * D + kdp;
+  float qv[16], kv[8];
+  auto fetch = [&](int dc) {
+    if (qvalid) {
+      load8<T>(qsrc + dc, qv);
+      load8<T>(qsrc + dc + 8, qv + 8);
+    } else {
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt)
+      for (int e = 0; e < 16; ++e) qv[e] = 0.f;
+    }
+    if (kvalid) {
+      load8<T>(ksrc + dc, kv);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kv[e] = 0.f;
+    }
+  };
+  auto stage = [&]() {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) qs[qrow][qoff + e] = qv[e];
+    if (tid < 256) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ks[kk][kdp + e] = kv[e];
+    }
+  };
+
+  f64x4 acc[2][4];
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) acc[rt][kt] = f64x4{0.0, 0.0, 0.0, 0.0};
 
-  const T* kh = static_cast<const T*>(a.k) + (static_cast<size_t>(b) * a.Hkv + g) * a.Lmax * D;
+  fetch(0);
+  stage();
+  __syncthreads();
 #pragma unroll 1
   for (int dc = 0; dc < D; dc += kDC) {
-    {   // window queries of this d chunk: thread = row
-      const int r = row0 + tid;
-      float qv[kDC];
-      if (r < R) {
-        const int h = g * G + r / w, i = r % w;
-        const T* src = static_cast<const T*>(a.q_win) +
-                       ((static_cast<size_t>(b) * a.Hq + h) * w + i) * D + dc;
+    const bool more = dc + kDC < D;
+    if (more) fetch(dc + kDC);                     // in flight during the products
+    if (active) {
 #pragma unroll
-        for (int e = 0; e < kDC; e += 8) load8<T>(src + e, qv + e);
-      } else {
+      for (int k4 = 0; k4 < kDC / 4; ++k4) {
+        const int dd = 4 * k4 + q4;                // this lane's k index
+        double av[2], bv[4];
 #pragma unroll
-        for (int e = 0; e < kDC; ++e) qv[e] = 0.f;
+        for (int rt = 0; rt < 2; ++rt)
+          av[rt] = static_cast<double>(qs[kWaveRows * wave + 16 * rt + r16][dd]);
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) bv[kt] = static_cast<double>(ks[16 * kt + r16][dd]);
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt)
+            acc[rt][kt] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[rt], bv[kt], acc[rt][kt], 0, 0, 0);
       }
-#pragma unroll
-      for (int e = 0; e < kDC; ++e) qs[tid][e] = qv[e];
-    }
-    {   // key tile of this d chunk: 4 threads per key, 8 elements each
-      const int kk = tid >> 2, dp = (tid & 3) * 8;
-      const int j = kbase + kk;
-      float kv[8];
-      if (j < L) {
-        load8<T>(kh + static_cast<size_t>(j) * D + dc + dp, kv);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) kv[e] = 0.f;
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) ks[kk][dp + e] = kv[e];
     }
     __syncthreads();
-#pragma unroll
-    for (int k4 = 0; k4 < kDC / 4; ++k4) {
-      const int dd = 4 * k4 + q4;                  // this lane's k index
-      double av[4], bv[4];
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt) av[rt] = static_cast<double>(qs[64 * wave + 16 * rt + r16][dd]);
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt) bv[kt] = static_cast<double>(ks[16 * kt + r16][dd]);
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt)
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-          acc[rt][kt] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[rt], bv[kt], acc[rt][kt], 0, 0, 0);
+    if (more) {
+      stage();
+      __syncthreads();
     }
-    __syncthreads();
   }
+  if (!active) return;
 
   // acc[rt][kt][v] = q(row 16 rt + q4 + 4 v) . k(key 16 kt + r16) of this wave
   // (the float64 16x16x4 product returns rows interleaved: item v of lane l is
   // row l/16 + 4v, column l%16).
   const size_t bg = static_cast<size_t>(b) * a.Hkv + g;
   float* ebase = a.e + (bg * a.n_tiles + tile) * static_cast<size_t>(R) * kT;
+  const double c = a.scale * 1.4426950408889634;  // exp(x) = 2^(x log2 e)
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt) {
+  for (int rt = 0; rt < 2; ++rt) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int rg = row0 + 64 * wave + 16 * rt + q4 + 4 * v;
-      const int lim = (rg < R) ? min(L - 1, L - w + rg % w) : -1;    // last visible key
-      double s[4];
-      double mx = -INFINITY;
+      const int rl = kWaveRows * wave + 16 * rt + q4 + 4 * v;
+      const int lim = s_lim[rl];
+      bool ok[4];
+      float mx = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
-        const int key = kbase + 16 * kt + r16;
-        s[kt] = (key <= lim) ? acc[rt][kt][v] * a.scale : -INFINITY;
-        mx = fmax(mx, s[kt]);
+        ok[kt] = kbase + 16 * kt + r16 <= lim;
+        mx = fmaxf(mx, ok[kt] ? static_cast<float>(acc[rt][kt][v]) : -INFINITY);
       }
-      mx = row16_max_f64(mx);
-      double z = 0.0;
-      float ef[4];
+      // reference: the row's largest dot product rounded to fp32 (exact as a
+      // double); e and m below use the same value, so any nearby one is as good
+      const double md = row16_max_f32(mx);
+      const double mdc = md * c;
+      float ev[4], zs = 0.f;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
-        const double ev = (mx == -INFINITY) ? 0.0 : exp(s[kt] - mx);
-        z += ev;
-        ef[kt] = static_cast<float>(ev);
+        ev[kt] = ok[kt] ? exp2_split(fma(acc[rt][kt][v], c, -mdc)) : 0.f;
+        zs += ev[kt];
       }
-      z = row16_sum_f64(z);
+      const double z = row16_sum_f64(static_cast<double>(zs));
+      const int rg = row0 + rl;
       if (rg < R) {
-        float* dst = ebase + static_cast<size_t>(rg) * kT + r16;
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt) dst[16 * kt] = ef[kt];
+        *reinterpret_cast<float4*>(ebase + static_cast<size_t>(rg) * kT + 4 * r16) =
+            make_float4(ev[0], ev[1], ev[2], ev[3]);
         if (r16 == 0) {
           const size_t o = (bg * R + rg) * a.n_tiles + tile;
-          a.tile_m[o] = mx;
+          a.tile_m[o] = md * a.scale;       // -inf when the whole row-tile is masked
           a.tile_z[o] = z;
         }
       }
@@ -243,7 +302,9 @@ __global__ __launch_bounds__(kThreads) void score_accum_kernel(ScoreArgs a) {
   }
   __syncthreads();
 
-  const float* et = a.e + (bg * a.n_tiles + ct) * static_cast<size_t>(R) * kT + col;
+  // key col of a tile row is stored at 4 (col % 16) + col / 16
+  const float* et = a.e + (bg * a.n_tiles + ct) * static_cast<size_t>(R) * kT +
+                    4 * (col & 15) + (col >> 4);
   double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
   int r = rg;
   for (; r + 12 < R; r += 16) {
@@ -298,11 +359,11 @@ size_t score_ws_bytes(int B, int Lmax, int Hkv, int R) {
 hipError_t launch_score(const ScoreArgs& a, int d, bool bf16, hipStream_t st) {
   const dim3 g1(a.n_tiles * a.row_chunks, a.Hkv, a.B);
   if (bf16) {
-    if (d == 128) score_tiles_kernel<bf16_t, 128><<<g1, kThreads, 0, st>>>(a);
-    else          score_tiles_kernel<bf16_t, 64><<<g1, kThreads, 0, st>>>(a);
+    if (d == 128) score_tiles_kernel<bf16_t, 128><<<g1, kTilesThreads, 0, st>>>(a);
+    else          score_tiles_kernel<bf16_t, 64><<<g1, kTilesThreads, 0, st>>>(a);
   } else {
-    if (d == 128) score_tiles_kernel<float, 128><<<g1, kThreads, 0, st>>>(a);
-    else          score_tiles_kernel<float, 64><<<g1, kThreads, 0, st>>>(a);
+    if (d == 128) score_tiles_kernel<float, 128><<<g1, kTilesThreads, 0, st>>>(a);
+    else          score_tiles_kernel<float, 64><<<g1, kTilesThreads, 0, st>>>(a);
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
