@@ -62,8 +62,7 @@ tb_status check_common(int32_t B, int32_t Hq, int32_t Hkv, int32_t d, tb_dtype d
 }
 
 size_t decode_ws(int32_t B, int32_t Hkv, int32_t G, int32_t d, int32_t cap, bool bf16) {
-  const int chunk = tb::decode_chunk_rows(B, Hkv, cap, bf16);
-  const size_t n_chunks = (static_cast<size_t>(cap) + chunk - 1) / chunk;
+  const size_t n_chunks = tb::decode_plan(B, Hkv, cap, bf16).n_chunks;
   const size_t part = static_cast<size_t>(B) * Hkv * n_chunks * G * (d + 4) * sizeof(float);
   return align256(part) + align256(static_cast<size_t>(B) * sizeof(int32_t));
 }
@@ -72,17 +71,33 @@ size_t decode_ws(int32_t B, int32_t Hkv, int32_t G, int32_t d, int32_t cap, bool
 
 namespace tb {
 
-// Rows per decode block: the smallest whole number of wave iterations that
-// keeps the grid at or under one block per CU (256 CUs); a CU holding two
-// blocks streams twice the rows and sets the step time (measured: 264 blocks
-// of 128 rows take 10.6 us per step where 132 blocks of 256 take 9.4 us).
-int decode_chunk_rows(int B, int Hkv, int cap, bool bf16) {
-  const long long unit = decode_chunk_unit(bf16);
+// How a decode step splits the cache (measured on the single-layer L = 8192
+// workload, 4 KV heads):
+// * The merge reads a KV head's partials in one round of loads when there are
+//   at most 64 of them; a second round costs more than larger chunks do.
+// * Small caches (up to ~3k rows per head here) are fastest with one-wave
+//   blocks: each wave writes its own partial from registers, with no LDS
+//   combine or barrier (410 rows: 7.6 us per step vs 8.2 with 4-wave blocks).
+// * Larger caches use 4-wave blocks, with the fewest rows per block that keep
+//   the grid at one block per CU (256 CUs), since a CU holding two blocks sets
+//   the step time.
+DecodePlan decode_plan(int B, int Hkv, int cap, bool bf16) {
   const long long units = static_cast<long long>(B) * Hkv;
-  long long want = (static_cast<long long>(cap) * units + 255) / 256;
-  want = std::min<long long>(std::max<long long>(want, unit), 1024);
-  want = std::max<long long>(want, (cap + decode_max_chunks() - 1) / decode_max_chunks());
-  return static_cast<int>((want + unit - 1) / unit * unit);
+  DecodePlan p{};
+  if (bf16 && units * cap <= 12288) {
+    p.waves = 1;
+    const long long unit = decode_chunk_unit(1, true);
+    p.chunk = static_cast<int32_t>((cap + unit * 64 - 1) / (unit * 64) * unit);
+  } else {
+    p.waves = bf16 ? 4 : 1;
+    const long long unit = decode_chunk_unit(p.waves, bf16);
+    long long want = (static_cast<long long>(cap) * units + 255) / 256;
+    want = std::min<long long>(std::max<long long>(want, unit), 1024);
+    want = std::max<long long>(want, (cap + decode_max_chunks() - 1) / decode_max_chunks());
+    p.chunk = static_cast<int32_t>((want + unit - 1) / unit * unit);
+  }
+  p.n_chunks = (cap + p.chunk - 1) / p.chunk;
+  return p;
 }
 
 }  // namespace tb
@@ -258,8 +273,10 @@ tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new, vo
     a.q = q; a.k_new = k_new; a.v_new = v_new; a.k_cache = k_cache; a.v_cache = v_cache;
     a.kv_len = kv_len; a.out = out;
     a.B = B; a.Hkv = Hkv; a.cap = cap;
-    a.chunk = tb::decode_chunk_rows(B, Hkv, cap, bf16);
-    a.n_chunks = (cap + a.chunk - 1) / a.chunk;
+    const tb::DecodePlan plan = tb::decode_plan(B, Hkv, cap, bf16);
+    a.chunk = plan.chunk;
+    a.n_chunks = plan.n_chunks;
+    a.waves = plan.waves;
     a.append = k_new != nullptr;
     a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(d)));
     char* p = static_cast<char*>(ws);

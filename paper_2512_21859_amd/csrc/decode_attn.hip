@@ -10,7 +10,9 @@
 //   partial kernel, grid = (n_chunks, Hkv, B): block (c, g, b) covers key
 //     rows [c*chunk, (c+1)*chunk) of KV head g of sequence b for all
 //     G = Hq/Hkv query heads of the group, so every K/V byte is read from HBM
-//     once per step, and writes one partial (m, l, o[G][d]).
+//     once per step, and writes one partial (m, l, o[G][d]).  A block has one
+//     wave (small caches: the wave stores its partial from registers) or four
+//     (each takes a quarter of the rows; the block combines them through LDS).
 //   merge kernel, grid = (Hq, B): combines a query head's chunk partials by
 //     log-sum-exp in a fixed order, writes the output; the block of query
 //     head 0 advances kv_len[b].
@@ -48,8 +50,10 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 // --------------------------------------------------------------------------
 // bf16: matrix-core partial kernel.
 // --------------------------------------------------------------------------
+// At least two waves per SIMD (<= 256 VGPRs), whatever the block size.
 template <int D, int G, int WAVES>
-__global__ __launch_bounds__(64 * WAVES, 2) void decode_mfma_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(2)))
+void decode_mfma_kernel(DecodeArgs a) {
   static_assert(G >= 1 && G <= 16, "query heads per KV head must fit 16 columns");
   constexpr int KC = D / 32;            // k-chunks of the QK^T product
   constexpr int NC = D / 16;            // d-blocks of the PV product
@@ -233,6 +237,20 @@ __global__ __launch_bounds__(64 * WAVES, 2) void decode_mfma_kernel(DecodeArgs a
   // ---- merge the lane groups' sums, then the waves, into this block's partial
   float l_tot = l_part + __shfl_xor(l_part, 16);
   l_tot += __shfl_xor(l_tot, 32);
+  float* part = a.part + (bg * a.n_chunks + c) * G * (D + 4);
+  if constexpr (WAVES == 1) {
+    // one wave: its (o, m, l) is the block's partial, stored from registers
+    // (lane (q4, r16) holds d = 16 n + 4 q4 .. +3 of head r16)
+    if (r16 < G) {
+#pragma unroll
+      for (int n = 0; n < NC; ++n)
+        *reinterpret_cast<float4*>(part + r16 * (D + 4) + 16 * n + 4 * q4) =
+            make_float4(accO[n][0], accO[n][1], accO[n][2], accO[n][3]);
+      if (q4 == 0) *reinterpret_cast<float2*>(part + r16 * (D + 4) + D) = make_float2(m_run, l_tot);
+    }
+    if (c == 0 && g == 0 && tid == 0) a.seq_len[b] = N;
+    return;
+  }
   if (r16 < G) {
 #pragma unroll
     for (int n = 0; n < NC; ++n)
@@ -241,7 +259,6 @@ __global__ __launch_bounds__(64 * WAVES, 2) void decode_mfma_kernel(DecodeArgs a
   if (q4 == 0) { s_ml[wave][r16][0] = m_run; s_ml[wave][r16][1] = l_tot; }
   __syncthreads();
 
-  float* part = a.part + (bg * a.n_chunks + c) * G * (D + 4);
   for (int idx = tid; idx < G * (D / 4); idx += 64 * WAVES) {
     const int h = idx / (D / 4), e4 = idx % (D / 4);
     float M = -INFINITY;
@@ -530,13 +547,12 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeArgs 
   if (h == 0 && tid == 0) a.kv_len[b] = N;
 }
 
-constexpr int kMfmaWaves = 4;
-
 template <typename T, int D, int G>
 hipError_t launch_both(const DecodeArgs& a, hipStream_t st) {
   const dim3 grid(a.n_chunks, a.Hkv, a.B);
   if constexpr (sizeof(T) == 2) {
-    decode_mfma_kernel<D, G, kMfmaWaves><<<grid, 64 * kMfmaWaves, 0, st>>>(a);
+    if (a.waves == 1) decode_mfma_kernel<D, G, 1><<<grid, 64, 0, st>>>(a);
+    else              decode_mfma_kernel<D, G, 4><<<grid, 256, 0, st>>>(a);
   } else {
     decode_valu_kernel<D, G><<<grid, kValuThreads, 0, st>>>(a);
   }
@@ -558,7 +574,7 @@ hipError_t launch_g(const DecodeArgs& a, int G, hipStream_t st) {
 
 }  // namespace
 
-int decode_chunk_unit(bool bf16) { return bf16 ? kMfmaWaves * kVT : kValuWaves * kRowsPerIter; }
+int decode_chunk_unit(int waves, bool bf16) { return bf16 ? waves * kVT : kValuWaves * kRowsPerIter; }
 int decode_max_chunks() { return 4096; }
 
 hipError_t launch_decode(const DecodeArgs& a, int G, int d, bool bf16, hipStream_t st) {

@@ -67,11 +67,17 @@ struct DecodeArgs {
   float* part;            // ws: [B][Hkv][n_chunks][G][d+4] chunk partials (o, m, l)
   int32_t* seq_len;       // ws: [B] attended length of this step
   int32_t B, Hkv, cap, chunk, n_chunks, append;
+  int32_t waves;          // waves per partial block (bf16: 1 or 4)
   float scale_log2;       // log2(e)/sqrt(d)
 };
-int decode_chunk_unit(bool bf16);
+// How a decode launch splits the cache: rows per block, blocks per KV head and
+// waves per block (every wave takes chunk / waves rows).
+struct DecodePlan {
+  int32_t chunk, n_chunks, waves;
+};
+DecodePlan decode_plan(int B, int Hkv, int cap, bool bf16);
+int decode_chunk_unit(int waves, bool bf16);
 int decode_max_chunks();
-int decode_chunk_rows(int B, int Hkv, int cap, bool bf16);
 size_t decode_ws_bytes(int B, int Hkv, int G, int d, int cap);
 hipError_t launch_decode(const DecodeArgs& a, int G, int d, bool bf16, hipStream_t st);
 
