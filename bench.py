@@ -73,17 +73,20 @@ def _evict_bytes(Hq, Hkv, d, L, w, n_keep, esz=2):
 
 def measured_traffic():
     """HBM bytes per decode launch from the committed counter runs, or None when
-    the decode kernel source has changed since the counters were taken."""
+    the decode kernels or their launch plan have changed since the counters were
+    taken (the record holds the sha256 of each source it depends on)."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "decode_traffic.json")
     try:
         with open(path) as f:
             rec = json.load(f)
-        with open(os.path.join(ROOT, rec["source"]), "rb") as f:
-            sha = hashlib.sha256(f.read()).hexdigest()
-    except (OSError, KeyError, ValueError):
+        for src, sha in rec["sources_sha256"].items():
+            with open(os.path.join(ROOT, src), "rb") as f:
+                if hashlib.sha256(f.read()).hexdigest() != sha:
+                    return None
+    except (OSError, KeyError, ValueError, AttributeError):
         return None
-    return rec["traffic_bytes_per_launch"] if sha == rec["source_sha256"] else None
+    return rec["traffic_bytes_per_launch"]
 
 
 def cpu_baseline(wl, pr, dc, min_seconds):
@@ -521,7 +524,7 @@ def main():
             "traffic": measured_traffic(),
             "traffic_note": "HBM bytes per decode launch (FETCH_SIZE x2 + WRITE_SIZE, scaled "
                             "by a 512 MiB copy; profiles/pmc_bf16_L8192_sweep.md); null if "
-                            "the decode kernel changed since",
+                            "the decode kernels or their launch plan changed since",
             "avg_launch_us": round(avg_launch_us, 3),
             "bytes_per_launch": round(dec_bytes_total / launches),
             "timing": "HIP events around each ratio's graph of decode launches, "
