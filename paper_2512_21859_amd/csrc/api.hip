@@ -78,6 +78,10 @@ namespace tb {
 // * Small caches (up to ~3k rows per head here) are fastest with one-wave
 //   blocks: each wave writes its own partial from registers, with no LDS
 //   combine or barrier (410 rows: 7.6 us per step vs 8.2 with 4-wave blocks).
+//   Up to 2048 rows per head, chunks of 32 or 64 rows leave at most 32
+//   partials per head, which one wave per query head merges in a single
+//   round of loads (410..1536 rows: 0.3..0.5 us less per step); beyond that,
+//   chunks are sized for at most 64 partials and the block merge.
 // * Larger caches use 4-wave blocks, with the fewest rows per block that keep
 //   the grid at one block per CU (256 CUs), since a CU holding two blocks sets
 //   the step time.
@@ -87,7 +91,8 @@ DecodePlan decode_plan(int B, int Hkv, int cap, bool bf16) {
   if (bf16 && units * cap <= 12288) {
     p.waves = 1;
     const long long unit = decode_chunk_unit(1, true);
-    p.chunk = static_cast<int32_t>((cap + unit * 64 - 1) / (unit * 64) * unit);
+    const long long parts = cap <= 2048 ? 32 : 64;
+    p.chunk = static_cast<int32_t>((cap + unit * parts - 1) / (unit * parts) * unit);
   } else {
     p.waves = bf16 ? 4 : 1;
     const long long unit = decode_chunk_unit(p.waves, bf16);

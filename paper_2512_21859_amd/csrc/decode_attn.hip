@@ -15,7 +15,8 @@
 //     (each takes a quarter of the rows; the block combines them through LDS).
 //   merge kernel, grid = (Hq, B): combines a query head's chunk partials by
 //     log-sum-exp in a fixed order, writes the output; the block of query
-//     head 0 advances kv_len[b].
+//     head 0 advances kv_len[b].  One wave per query head when one round of
+//     loads covers the chunks, else a 256-thread block with an LDS tree.
 // bf16 runs on the matrix cores (v_mfma_f32_16x16x32_bf16), one wave per
 // 32-key block at a time:
 //   S^T[32 keys x 16 heads] = K[32 x d] . Q^T[d x 16]   (heads padded to 16)
@@ -461,6 +462,97 @@ __global__ __launch_bounds__(kValuThreads) void decode_valu_kernel(DecodeArgs a)
 // merge runs over all of them and never waits for the length; the length is
 // only needed for the final kv_len store.
 // --------------------------------------------------------------------------
+// --------------------------------------------------------------------------
+// Merge by one wave per (query head, sequence), for up to 64 / (d/4) * 16
+// chunks (32 at d = 128): lane = (chunk split, float4 slice of o); every lane
+// issues its 16 partial loads at once, then the splits are combined by
+// cross-lane swaps in a fixed order (lower split first).  No LDS, no barrier;
+// measured faster than the block merge below whenever one round of loads
+// covers the chunks (21 chunks of the L = 8192 workload: 6.6 vs 7.1 us per
+// step), slower when it needs two.
+// --------------------------------------------------------------------------
+constexpr int kWaveMergePerLane = 16;
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(64) void decode_merge_wave_kernel(DecodeArgs a) {
+  constexpr int E4 = D / 4;                  // float4 slices of one head's o
+  constexpr int SPL = 64 / E4;               // chunk splits per wave
+  constexpr int KPT = kWaveMergePerLane;
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int Hkv = a.Hkv, Hq = Hkv * G;
+  const int g = h / G, hh = h % G;
+  const int lane = threadIdx.x, e4 = lane % E4, sp = lane / E4;
+  const int N = a.seq_len[b];
+  const int n_used = a.n_chunks;
+  const size_t bg = static_cast<size_t>(b) * Hkv + g;
+  const float* base = a.part + (bg * a.n_chunks * G + hh) * (D + 4);
+  constexpr size_t CSTRIDE = static_cast<size_t>(G) * (D + 4);
+
+  float M = -INFINITY, L = 0.f;
+  float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int c0 = sp; c0 < n_used; c0 += SPL * KPT) {
+    float mm[KPT], ll[KPT];
+    float4 oo[KPT];
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) {
+      const int cc = c0 + k * SPL;
+      const float* pc = base + min(cc, n_used - 1) * CSTRIDE;
+      const float2 ml = *reinterpret_cast<const float2*>(pc + D);
+      oo[k] = *reinterpret_cast<const float4*>(pc + 4 * e4);
+      mm[k] = cc < n_used ? ml.x : -INFINITY;
+      ll[k] = cc < n_used ? ml.y : 0.f;
+    }
+    // keep every load above this point: they must all be in flight together
+    __builtin_amdgcn_sched_barrier(0);
+    float mx = M;
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) mx = fmaxf(mx, mm[k]);
+    if (mx == -INFINITY) continue;
+    const float corr = exp2f(M - mx);
+    L *= corr; O.x *= corr; O.y *= corr; O.z *= corr; O.w *= corr;
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) {
+      const float wgt = exp2f(mm[k] - mx);
+      L += wgt * ll[k];
+      O.x += wgt * oo[k].x; O.y += wgt * oo[k].y; O.z += wgt * oo[k].z; O.w += wgt * oo[k].w;
+    }
+    M = mx;
+  }
+  // splits s and s ^ (off / E4) meet at lanes l and l ^ off; both lanes combine
+  // (lower split, upper split) in that order, so they hold identical results
+#pragma unroll
+  for (int off = 32; off >= E4; off >>= 1) {
+    const float Mo = __shfl_xor(M, off), Lo = __shfl_xor(L, off);
+    const float4 Oo = make_float4(__shfl_xor(O.x, off), __shfl_xor(O.y, off),
+                                  __shfl_xor(O.z, off), __shfl_xor(O.w, off));
+    const bool upper = (lane & off) != 0;
+    const float Ma = upper ? Mo : M, La = upper ? Lo : L;
+    const float Mb = upper ? M : Mo, Lb = upper ? L : Lo;
+    const float4 Oa = upper ? Oo : O, Ob = upper ? O : Oo;
+    const float Mn = fmaxf(Ma, Mb);
+    if (Mn != -INFINITY) {
+      const float w1 = exp2f(Ma - Mn), w2 = exp2f(Mb - Mn);
+      L = La * w1 + Lb * w2;
+      O = make_float4(Oa.x * w1 + Ob.x * w2, Oa.y * w1 + Ob.y * w2,
+                      Oa.z * w1 + Ob.z * w2, Oa.w * w1 + Ob.w * w2);
+    }
+    M = Mn;
+  }
+  if (sp == 0) {
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    T* out = static_cast<T*>(a.out) + (static_cast<size_t>(b) * Hq + h) * D + 4 * e4;
+    if constexpr (sizeof(T) == 2) {
+      typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+      *reinterpret_cast<bf16x4*>(out) =
+          bf16x4{static_cast<__bf16>(O.x * inv), static_cast<__bf16>(O.y * inv),
+                 static_cast<__bf16>(O.z * inv), static_cast<__bf16>(O.w * inv)};
+    } else {
+      *reinterpret_cast<float4*>(out) = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
+    }
+  }
+  if (h == 0 && lane == 0) a.kv_len[b] = N;
+}
+
 constexpr int kMergeThreads = 256;
 constexpr int kMergePerThread = 8;
 
@@ -558,7 +650,10 @@ hipError_t launch_both(const DecodeArgs& a, hipStream_t st) {
   }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  decode_merge_kernel<T, D, G><<<dim3(a.Hkv * G, a.B), kMergeThreads, 0, st>>>(a);
+  if (a.n_chunks <= (256 / D) * kWaveMergePerLane)
+    decode_merge_wave_kernel<T, D, G><<<dim3(a.Hkv * G, a.B), 64, 0, st>>>(a);
+  else
+    decode_merge_kernel<T, D, G><<<dim3(a.Hkv * G, a.B), kMergeThreads, 0, st>>>(a);
   return hipGetLastError();
 }
 
