@@ -50,7 +50,9 @@ def _parse():
                     help="skip the supplementary 28-layer L=32768 ratio sweep")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the 2 GiB read / copy bandwidth ceilings")
-    ap.add_argument("--only", choices=("cold", "long", "layers", "ceiling"),
+    ap.add_argument("--no-scorers", action="store_true",
+                    help="skip the scorer-variant timings")
+    ap.add_argument("--only", choices=("cold", "long", "layers", "ceiling", "scorers"),
                     help="run one supplementary measurement alone and print its JSON "
                          "(for profiling that workload by itself)")
     ap.add_argument("--pmc-calibration", action="store_true",
@@ -266,6 +268,43 @@ def cold_decode(torch, _lib, Evictor, dev, wl, q_win, k, v, qd, knd, vnd,
             "timing": "best of 3: HIP events around a graph of the decode steps"}
 
 
+def scorer_variants(torch, _lib, synth, Evictor, dev, reps=10):
+    """Supplementary: scoring time of each scorer (max-pool window scores, the
+    mean-pooled variant, KNorm) at the L = 8192 and L = 131072 shapes, from a
+    graph of `reps` scoring calls; KNorm's bandwidth counts one read of K plus
+    the fp32 scores written."""
+    out = {}
+    for wid in (2, 5):
+        wl = synth.WORKLOADS[wid]
+        B, Hq, Hkv, d, w, L = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L
+        pr = synth.make_prompt(wl)
+        q_win, k = pr["q_win"].to(dev), pr["k"].to(dev)
+        del pr
+        row = {}
+        for scorer in ("snapkv", "snapkv_avg", "knorm"):
+            ev = Evictor(B, L, Hq, Hkv, d, w, wl.pool, device=dev, scorer=scorer)
+            cs = torch.cuda.Stream()
+            ev.score(q_win, k, [L], cs)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=cs):
+                for _ in range(reps):
+                    ev.score(q_win, k, [L], cs)
+            torch.cuda.synchronize()
+            us = _best_ms(torch, g.replay) * 1e3 / reps
+            row[scorer] = {"us": round(us, 2)}
+            if scorer == "knorm":
+                nbytes = Hkv * L * d * 2 + Hkv * (L - w) * 4
+                row[scorer]["GBps"] = round(nbytes / (us * 1e-6) / 1e9, 1)
+                row[scorer]["frac_of_8TBps"] = round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+            del g, ev
+        out[f"L{L}_{Hq}q{Hkv}kv"] = row
+        del q_win, k
+        torch.cuda.empty_cache()
+    out["timing"] = f"best of 3 replays of a graph of {reps} scoring calls, divided by {reps}"
+    return out
+
+
 def layer_sweep(torch, _lib, synth, Evictor, dev, T=None):
     """Supplementary: the 28-layer model shape at L = 32768 (28 q / 4 kv heads,
     d = 128, w = 32, pool 7) over the ratios k/20, k = 0..19.  Per ratio: evict
@@ -384,10 +423,11 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    if args.only in ("long", "layers", "ceiling"):
+    if args.only in ("long", "layers", "ceiling", "scorers"):
         fn = {"long": lambda: long_context(torch, _lib, synth, Evictor, dev),
               "layers": lambda: layer_sweep(torch, _lib, synth, Evictor, dev),
-              "ceiling": lambda: hbm_ceiling(torch, dev)}[args.only]
+              "ceiling": lambda: hbm_ceiling(torch, dev),
+              "scorers": lambda: scorer_variants(torch, _lib, synth, Evictor, dev)}[args.only]
         print(json.dumps({"section": args.only, **fn()}), flush=True)
         return
     wl = synth.WORKLOADS[2]
@@ -545,6 +585,8 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_long_context:
         result["long_context"] = long_context(torch, _lib, synth, Evictor, dev)
+    if not args.no_scorers:
+        result["scorers"] = scorer_variants(torch, _lib, synth, Evictor, dev)
     if not args.no_layer_sweep:
         result["layer_sweep"] = layer_sweep(torch, _lib, synth, Evictor, dev)
     if not args.no_ceiling:

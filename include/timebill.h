@@ -11,6 +11,8 @@
  *
  *   tb_score_window  observation-window scores (softmax of the last w queries
  *                    against the prompt keys, summed per KV head, max-pooled);
+ *                    tb_score_window_avgpool and tb_score_knorm are the
+ *                    scorer variants (mean-pooled window scores; key norms);
  *   tb_select_topk   per-KV-head top-k of the scores keeping n_keep positions;
  *   tb_compact_kv    gather of the kept K/V rows into a compact cache;
  *   tb_decode_attn   single-token grouped-query decode attention over the
@@ -108,12 +110,34 @@ tb_status tb_score_window(const void* q_win, const void* k, int32_t B,
                           tb_dtype dt, float* scores, float* raw_scores,
                           void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* The same scores with the max-pool replaced by a mean (the average-pool
+ * variant of the observation-window scorer):
+ *   scores[j] = (1/pool) * sum of A[j'] over |j - j'| <= pool/2, with A taken
+ *               as 0 outside the prefix [0, L[b] - w)   (divisor always pool).
+ * The mean is summed in float64 from the fp32 raw scores.  Arguments,
+ * requirements and workspace as tb_score_window. */
+tb_status tb_score_window_avgpool(const void* q_win, const void* k, int32_t B,
+                                  const int32_t* L, int32_t Lmax, int32_t Hq,
+                                  int32_t Hkv, int32_t d, int32_t w, int32_t pool,
+                                  tb_dtype dt, float* scores, float* raw_scores,
+                                  void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* KNorm scores (the norm-based scorer cited for the fixed-ratio baselines,
+ * Sec. 6.1): for KV head g of sequence b and prefix position j < L[b] - w,
+ *   scores[j] = -||k[b][g][j]||_2,
+ * so tb_select_topk keeps the smallest key norms (plus the window, as for
+ * every scorer).  Sums of squares in float64, fp32 output; one read of K.
+ * L: [host][B].  Requires w >= 1, w < L[b] <= Lmax.  No workspace. */
+tb_status tb_score_knorm(const void* k, int32_t B, const int32_t* L, int32_t Lmax,
+                         int32_t Hkv, int32_t d, int32_t w, tb_dtype dt,
+                         float* scores, hipStream_t stream);
+
 /* Per-KV-head top-k keeping n_keep[b] = tb_keep_count(L[b], alpha[b], w)
  * positions (Eq. N_kv: a fraction alpha of the prompt's KV is evicted once,
  * after prefill, Sec. 4.2 and Sec. 5.2).  Selects the n_keep[b] - w prefix
  * positions with the largest scores (ties -> lower position), writes them
  * ascending to keep_idx followed by the window positions L[b]-w .. L[b]-1.
- * scores must be >= 0 (as tb_score_window produces).
+ * Scores may be any finite floats (-0 equals +0); NaN is not supported.
  * L, alpha: [host][B] inputs.  n_keep: [host][B] output, filled before return.
  * ws: tb_workspace_bytes(TB_OP_SELECT, ...) bytes (currently 0; may be NULL). */
 tb_status tb_select_topk(const float* scores, int32_t B, const int32_t* L,

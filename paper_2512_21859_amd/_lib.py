@@ -22,7 +22,7 @@ TB_OP_SCORE, TB_OP_SELECT, TB_OP_COMPACT, TB_OP_DECODE = range(4)
 V_TILE = 32          # the compact V cache is stored as transposed tiles of 32 rows
 
 EXPORTED = ("tb_keep_count", "tb_last_error", "tb_workspace_bytes", "tb_score_window",
-            "tb_select_topk", "tb_compact_kv", "tb_decode_attn", "tb_ete_fit", "tb_wcet",
+            "tb_score_window_avgpool", "tb_score_knorm", "tb_select_topk", "tb_compact_kv", "tb_decode_attn", "tb_ete_fit", "tb_wcet",
             "tb_alpha_star")
 
 _lib = None
@@ -54,6 +54,10 @@ def load() -> ctypes.CDLL:
     lib.tb_score_window.argtypes = [vp, vp, i32, p_i32, i32, i32, i32, i32, i32, i32, i32,
                                     vp, vp, vp, sz, vp]
     lib.tb_score_window.restype = i32
+    lib.tb_score_window_avgpool.argtypes = lib.tb_score_window.argtypes
+    lib.tb_score_window_avgpool.restype = i32
+    lib.tb_score_knorm.argtypes = [vp, i32, p_i32, i32, i32, i32, i32, i32, vp, vp]
+    lib.tb_score_knorm.restype = i32
     lib.tb_select_topk.argtypes = [vp, i32, p_i32, i32, i32, i32, p_dbl, vp, p_i32, vp, sz, vp]
     lib.tb_select_topk.restype = i32
     lib.tb_compact_kv.argtypes = [vp, vp, vp, i32, p_i32, i32, i32, i32, i32, i32, vp, vp, vp,
@@ -117,8 +121,9 @@ def tb_workspace_bytes(op: int, B: int, Lmax: int, Hq: int, Hkv: int, d: int, w:
 
 def tb_score_window(q_win: torch.Tensor, k: torch.Tensor, L: Sequence[int], w: int, pool: int,
                     scores: torch.Tensor, raw_scores: Optional[torch.Tensor] = None,
-                    ws: Optional[torch.Tensor] = None, stream=None) -> None:
-    """q_win [B,Hq,w,d], k [B,Hkv,Lmax,d] (bf16/fp32); scores [B,Hkv,Lmax] fp32."""
+                    ws: Optional[torch.Tensor] = None, stream=None, avgpool: bool = False) -> None:
+    """q_win [B,Hq,w,d], k [B,Hkv,Lmax,d] (bf16/fp32); scores [B,Hkv,Lmax] fp32.
+    avgpool=True calls tb_score_window_avgpool (mean instead of max)."""
     B, Hq, w_, d = q_win.shape
     _, Hkv, Lmax, d2 = k.shape
     if w_ != w or d2 != d or k.shape[0] != B or k.dtype != q_win.dtype:
@@ -128,11 +133,23 @@ def tb_score_window(q_win: torch.Tensor, k: torch.Tensor, L: Sequence[int], w: i
     if raw_scores is not None and tuple(raw_scores.shape) != (B, Hkv, Lmax):
         raise ValueError("raw_scores must be [B, Hkv, Lmax]")
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
-    _check(load().tb_score_window(
+    fn = load().tb_score_window_avgpool if avgpool else load().tb_score_window
+    _check(fn(
         _dev(q_win, "q_win"), _dev(k, "k"), B, _i32_array(L), Lmax, Hq, Hkv, d, w, pool,
         _dtype_code(k), _dev(scores, "scores", torch.float32),
         _dev(raw_scores, "raw_scores", torch.float32), _dev(ws, "ws"), ws_bytes,
         _stream(stream)))
+
+
+def tb_score_knorm(k: torch.Tensor, L: Sequence[int], w: int, scores: torch.Tensor,
+                   stream=None) -> None:
+    """k [B,Hkv,Lmax,d] (bf16/fp32) -> scores [B,Hkv,Lmax] fp32 = -||k_j|| (prefix)."""
+    B, Hkv, Lmax, d = k.shape
+    if tuple(scores.shape) != (B, Hkv, Lmax):
+        raise ValueError("scores must be [B, Hkv, Lmax]")
+    _check(load().tb_score_knorm(_dev(k, "k"), B, _i32_array(L), Lmax, Hkv, d, w,
+                                 _dtype_code(k), _dev(scores, "scores", torch.float32),
+                                 _stream(stream)))
 
 
 def tb_select_topk(scores: torch.Tensor, L: Sequence[int], w: int, alpha: Sequence[float],

@@ -146,12 +146,14 @@ size_t tb_workspace_bytes(int32_t op, int32_t B, int32_t Lmax, int32_t Hq, int32
   }
 }
 
-tb_status tb_score_window(const void* q_win, const void* k, int32_t B, const int32_t* L,
-                          int32_t Lmax, int32_t Hq, int32_t Hkv, int32_t d, int32_t w,
-                          int32_t pool, tb_dtype dt, float* scores, float* raw_scores,
-                          void* ws, size_t ws_bytes, hipStream_t stream) {
+namespace {
+
+tb_status score_window_impl(const char* name, bool avg, const void* q_win, const void* k,
+                            int32_t B, const int32_t* L, int32_t Lmax, int32_t Hq, int32_t Hkv,
+                            int32_t d, int32_t w, int32_t pool, tb_dtype dt, float* scores,
+                            float* raw_scores, void* ws, size_t ws_bytes, hipStream_t stream) {
   try {
-    if (!q_win || !k || !L || !scores) return fail(TB_EINVAL, "tb_score_window: null pointer");
+    if (!q_win || !k || !L || !scores) return fail(TB_EINVAL, "%s: null pointer", name);
     tb_status st = check_common(B, Hq, Hkv, d, dt);
     if (st != TB_OK) return st;
     if (w < 1) return fail(TB_EINVAL, "w must be >= 1 (got %d)", w);
@@ -164,11 +166,12 @@ tb_status tb_score_window(const void* q_win, const void* k, int32_t B, const int
         return fail(TB_EINVAL, "need w < L[%d] <= Lmax (w=%d, L=%d, Lmax=%d)", b, w, L[b], Lmax);
     const size_t need = tb::score_ws_bytes(B, Lmax, Hkv, R);
     if (ws_bytes < need || (need > 0 && !ws))
-      return fail(TB_EWORKSPACE, "tb_score_window: workspace %zu < %zu bytes", ws_bytes, need);
+      return fail(TB_EWORKSPACE, "%s: workspace %zu < %zu bytes", name, ws_bytes, need);
 
     tb::ScoreArgs a{};
     a.q_win = q_win; a.k = k; a.scores = scores; a.raw_scores = raw_scores;
     a.B = B; a.Lmax = Lmax; a.Hq = Hq; a.Hkv = Hkv; a.w = w; a.pool = pool; a.R = R;
+    a.pool_avg = avg ? 1 : 0;
     a.n_tiles = (Lmax + tb::kScoreTile - 1) / tb::kScoreTile;
     a.row_chunks = (R + tb::kScoreRows - 1) / tb::kScoreRows;
     a.scale = 1.0 / sqrt(static_cast<double>(d));
@@ -186,11 +189,49 @@ tb_status tb_score_window(const void* q_win, const void* k, int32_t B, const int
     a.row_Z = reinterpret_cast<double*>(p);
     p += align256(units * R * sizeof(double));
     a.raw = raw_scores ? raw_scores : reinterpret_cast<float*>(p);
-    return hip_status(tb::launch_score(a, d, dt == TB_BF16, stream), "tb_score_window launch");
+    return hip_status(tb::launch_score(a, d, dt == TB_BF16, stream), name);
   } catch (const std::exception& e) {
-    return fail(TB_EINTERNAL, "tb_score_window: %s", e.what());
+    return fail(TB_EINTERNAL, "%s: %s", name, e.what());
   } catch (...) {
-    return fail(TB_EINTERNAL, "tb_score_window: internal error");
+    return fail(TB_EINTERNAL, "%s: internal error", name);
+  }
+}
+
+}  // namespace
+
+tb_status tb_score_window(const void* q_win, const void* k, int32_t B, const int32_t* L,
+                          int32_t Lmax, int32_t Hq, int32_t Hkv, int32_t d, int32_t w,
+                          int32_t pool, tb_dtype dt, float* scores, float* raw_scores,
+                          void* ws, size_t ws_bytes, hipStream_t stream) {
+  return score_window_impl("tb_score_window", false, q_win, k, B, L, Lmax, Hq, Hkv, d, w, pool,
+                           dt, scores, raw_scores, ws, ws_bytes, stream);
+}
+
+tb_status tb_score_window_avgpool(const void* q_win, const void* k, int32_t B, const int32_t* L,
+                                  int32_t Lmax, int32_t Hq, int32_t Hkv, int32_t d, int32_t w,
+                                  int32_t pool, tb_dtype dt, float* scores, float* raw_scores,
+                                  void* ws, size_t ws_bytes, hipStream_t stream) {
+  return score_window_impl("tb_score_window_avgpool", true, q_win, k, B, L, Lmax, Hq, Hkv, d, w,
+                           pool, dt, scores, raw_scores, ws, ws_bytes, stream);
+}
+
+tb_status tb_score_knorm(const void* k, int32_t B, const int32_t* L, int32_t Lmax, int32_t Hkv,
+                         int32_t d, int32_t w, tb_dtype dt, float* scores, hipStream_t stream) {
+  try {
+    if (!k || !L || !scores) return fail(TB_EINVAL, "tb_score_knorm: null pointer");
+    tb_status st = check_common(B, Hkv, Hkv, d, dt);
+    if (st != TB_OK) return st;
+    if (w < 1) return fail(TB_EINVAL, "w must be >= 1 (got %d)", w);
+    tb::KnormArgs a{};
+    for (int b = 0; b < B; ++b) {
+      if (!(L[b] > w && L[b] <= Lmax))
+        return fail(TB_EINVAL, "need w < L[%d] <= Lmax (w=%d, L=%d, Lmax=%d)", b, w, L[b], Lmax);
+      a.L[b] = L[b];
+    }
+    a.k = k; a.scores = scores; a.B = B; a.Lmax = Lmax; a.Hkv = Hkv; a.w = w;
+    return hip_status(tb::launch_knorm(a, d, dt == TB_BF16, stream), "tb_score_knorm launch");
+  } catch (...) {
+    return fail(TB_EINTERNAL, "tb_score_knorm: internal error");
   }
 }
 

@@ -25,11 +25,21 @@ struct ScoreArgs {
   double* row_Z;          // ws: [B][Hkv][R]
   float* raw;             // raw scores: raw_scores if given, else ws [B][Hkv][Lmax]
   int32_t B, Lmax, Hq, Hkv, w, pool, R, n_tiles, row_chunks;
+  int32_t pool_avg;       // 0: max-pool, 1: mean over the window (zeros outside the prefix)
   double scale;           // 1/sqrt(d)
   int32_t L[kMaxB];
 };
 size_t score_ws_bytes(int B, int Lmax, int Hkv, int R);
 hipError_t launch_score(const ScoreArgs& a, int d, bool bf16, hipStream_t st);
+
+// ---------------------------------------------------------------- KNorm
+struct KnormArgs {
+  const void* k;          // [B][Hkv][Lmax][d]
+  float* scores;          // [B][Hkv][Lmax]: -||k_j|| for j < L[b] - w
+  int32_t B, Lmax, Hkv, w;
+  int32_t L[kMaxB];
+};
+hipError_t launch_knorm(const KnormArgs& a, int d, bool bf16, hipStream_t st);
 
 // ---------------------------------------------------------------- selection
 struct SelectArgs {

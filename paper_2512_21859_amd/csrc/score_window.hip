@@ -24,7 +24,9 @@
 //   K3 score_accum: block = 64 prefix columns; A[j] = sum_r e[r][j] *
 //      exp(m[r][tile] - M[r]) / Z[r] in float64 (four row groups, four
 //      independent accumulators each, combined in a fixed order); raw A as fp32.
-//   K4 pool: max of the raw scores over |j - j'| <= pool/2 within the prefix.
+//   K4 pool: max of the raw scores over |j - j'| <= pool/2 within the prefix
+//      (or their mean with zeros outside the prefix and divisor pool, summed in
+//      float64, for the average-pool variant).
 //
 // The per-logit exponential is the one place fp64 arithmetic is avoided: on
 // this part the fp64 vector instructions compete with the fp64 matrix
@@ -337,10 +339,17 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(ScoreArgs a) {
   const int hp = a.pool / 2;
   const size_t bg = static_cast<size_t>(b) * a.Hkv + g;
   const float* raw = a.raw + bg * a.Lmax;
-  float mx = raw[j];
   const int lo = max(j - hp, 0), hi = min(j + hp, pref - 1);
-  for (int jn = lo; jn <= hi; ++jn) mx = fmaxf(mx, raw[jn]);
-  a.scores[bg * a.Lmax + j] = mx;
+  if (a.pool_avg) {
+    // positions outside the prefix count as zeros; the divisor is always pool
+    double sum = 0.0;
+    for (int jn = lo; jn <= hi; ++jn) sum += raw[jn];
+    a.scores[bg * a.Lmax + j] = static_cast<float>(sum / a.pool);
+  } else {
+    float mx = raw[j];
+    for (int jn = lo; jn <= hi; ++jn) mx = fmaxf(mx, raw[jn]);
+    a.scores[bg * a.Lmax + j] = mx;
+  }
 }
 
 }  // namespace

@@ -1,9 +1,10 @@
 // Per-KV-head top-k of the pooled scores with lower-position tie-break,
 // emitted as ascending kept positions followed by the window.
 //
-// One block of 1024 threads per (sequence, KV head).  Scores are >= 0, so
-// their IEEE bit patterns order like the values; the selection is integer
-// work and bit-exact:
+// One block of 1024 threads per (sequence, KV head).  Each score is mapped to
+// an unsigned key that orders like the float (non-negative: sign bit set;
+// negative: all bits flipped; -0 as +0), so the selection is integer work and
+// bit-exact for any finite scores (KNorm's are negative):
 //   0. one pass over the prefix finds the largest and smallest key; the bits
 //      above their highest differing bit are common to every key, so the radix
 //      search starts just below them (digits spread over bins from the first
@@ -37,7 +38,9 @@ constexpr int kTileN = kThreads * kPer;       // 16384
 constexpr int kCacheN = 32768;                // prefix kept in LDS when it fits
 
 __device__ __forceinline__ uint32_t key_of(float f) {
-  return __float_as_uint(f) & 0x7fffffffu;    // scores are >= 0 (-0 -> 0)
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;               // -0 orders as +0
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
 // Block-wide exclusive scan of v (1024 threads); also returns the total.
@@ -143,10 +146,10 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
   });
   block_max_min(kmax, kmin, s_wave);          // ends with a barrier
   const uint32_t diff = kmax ^ kmin;
-  // bits [lo, 31) still to resolve; keys are < 2^31, so the common part of the
-  // keys above bit lo is kmax's
+  // bits [0, lo) still to resolve; the keys share every bit above them, so
+  // their common part is kmax's
   int lo = diff ? 32 - __clz(diff) : 1;
-  uint32_t mask = ~((1u << lo) - 1u) & 0x7fffffffu;
+  uint32_t mask = lo >= 32 ? 0u : ~((1u << lo) - 1u);
   uint32_t prefix = kmax & mask;
   uint32_t rank = static_cast<uint32_t>(n_sel);
 

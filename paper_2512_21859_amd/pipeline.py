@@ -15,22 +15,36 @@ import torch
 from . import _lib
 
 
+SCORERS = ("snapkv", "snapkv_avg", "knorm")
+
+
 class Evictor:
-    """Score / select buffers and workspace for one layer shape."""
+    """Score / select buffers and workspace for one layer shape.
+
+    scorer: "snapkv" (observation-window scores, max-pooled; the paper's
+    eviction), "snapkv_avg" (the same scores mean-pooled) or "knorm" (negated
+    key norms; the window queries are not used)."""
 
     def __init__(self, B: int, Lmax: int, Hq: int, Hkv: int, d: int, w: int, pool: int,
-                 device="cuda", keep_raw: bool = False):
+                 device="cuda", keep_raw: bool = False, scorer: str = "snapkv"):
+        if scorer not in SCORERS:
+            raise ValueError(f"scorer must be one of {SCORERS}")
+        self.scorer = scorer
         self.B, self.Lmax, self.Hq, self.Hkv, self.d, self.w, self.pool = B, Lmax, Hq, Hkv, d, w, pool
         self.scores = torch.empty((B, Hkv, Lmax), dtype=torch.float32, device=device)
         self.raw = (torch.empty((B, Hkv, Lmax), dtype=torch.float32, device=device)
                     if keep_raw else None)
         self.keep_idx = torch.empty((B, Hkv, Lmax), dtype=torch.int32, device=device)
-        nbytes = _lib.tb_workspace_bytes(_lib.TB_OP_SCORE, B, Lmax, Hq, Hkv, d, w, 0)
+        nbytes = (_lib.tb_workspace_bytes(_lib.TB_OP_SCORE, B, Lmax, Hq, Hkv, d, w, 0)
+                  if scorer != "knorm" else 0)
         self.ws = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=device)
 
     def score(self, q_win: torch.Tensor, k: torch.Tensor, L: Sequence[int], stream=None) -> None:
-        _lib.tb_score_window(q_win, k, L, self.w, self.pool, self.scores, self.raw, self.ws,
-                             stream)
+        if self.scorer == "knorm":
+            _lib.tb_score_knorm(k, L, self.w, self.scores, stream)
+        else:
+            _lib.tb_score_window(q_win, k, L, self.w, self.pool, self.scores, self.raw, self.ws,
+                                 stream, avgpool=self.scorer == "snapkv_avg")
 
     def select(self, L: Sequence[int], alphas: Sequence[float], stream=None):
         return _lib.tb_select_topk(self.scores, L, self.w, alphas, self.keep_idx, None, stream)

@@ -72,11 +72,12 @@ def _i32(*v):
     return (ctypes.c_int32 * len(v))(*v)
 
 
-def _score(lib, **kw):
+def _score(lib, fn=None, **kw):
     a = dict(q=FAKE, k=FAKE, B=1, L=_i32(100), Lmax=100, Hq=4, Hkv=2, d=128, w=8, pool=7,
              dt=_lib.TB_BF16, sc=FAKE, raw=None, ws=FAKE, wsb=1 << 40)
     a.update(kw)
-    return lib.tb_score_window(a["q"], a["k"], a["B"], a["L"], a["Lmax"], a["Hq"], a["Hkv"],
+    fn = lib.tb_score_window if fn is None else fn
+    return fn(a["q"], a["k"], a["B"], a["L"], a["Lmax"], a["Hq"], a["Hkv"],
                                a["d"], a["w"], a["pool"], a["dt"], a["sc"], a["raw"], a["ws"],
                                a["wsb"], None)
 
@@ -97,6 +98,33 @@ def test_score_validation(lib):
     assert _score(lib, Hq=40, Hkv=1, w=32) == E.TB_EUNSUPPORTED   # G*w > 1024
     assert _score(lib, wsb=16) == E.TB_EWORKSPACE
     assert b"workspace" in lib.tb_last_error()
+
+
+def test_score_avgpool_validation(lib):
+    """The average-pool entry validates exactly like tb_score_window."""
+    E = _lib
+    for kw, want in [(dict(q=None), E.TB_EINVAL), (dict(pool=4), E.TB_EINVAL),
+                     (dict(w=100), E.TB_EINVAL), (dict(Hq=40, Hkv=1, w=32), E.TB_EUNSUPPORTED),
+                     (dict(wsb=16), E.TB_EWORKSPACE)]:
+        assert _score(lib, fn=lib.tb_score_window_avgpool, **kw) == want, kw
+    assert b"tb_score_window_avgpool: workspace" in lib.tb_last_error()
+
+
+def test_score_knorm_validation(lib):
+    E = _lib
+
+    def call(k=FAKE, B=1, L=100, Lmax=100, Hkv=2, d=128, w=8, dt=_lib.TB_BF16, sc=FAKE):
+        return lib.tb_score_knorm(k, B, _i32(L), Lmax, Hkv, d, w, dt, sc, None)
+
+    assert call(k=None) == E.TB_EINVAL
+    assert call(sc=None) == E.TB_EINVAL
+    assert call(B=0) == E.TB_EINVAL
+    assert call(d=96) == E.TB_EUNSUPPORTED
+    assert call(dt=7) == E.TB_EUNSUPPORTED
+    assert call(w=0) == E.TB_EINVAL
+    assert call(w=100) == E.TB_EINVAL
+    assert call(L=101) == E.TB_EINVAL
+    assert b"L[0]" in lib.tb_last_error()
 
 
 def test_select_validation(lib):
