@@ -6,13 +6,20 @@ the HIP path).
 
 TimeBill evicts with SnapKV (Sec. 6.1) and compares against fixed-ratio
 eviction whose scorers it cites without defining them (Sec. 6.1, the
-fixed-alpha baselines, citing KNorm and H2O).  Two variants are built on the
+fixed-alpha baselines, citing KNorm and H2O).  Three variants are built on the
 same select / compact / decode path:
 
 * KNorm: a prefix key's score is the negated L2 norm of its (post-RoPE) key
   vector, so keeping the largest scores keeps the smallest norms (the cited
   norm-based strategy).  Reading: as for SnapKV, the last w positions are
   always kept and only the prefix j < N_x - w competes; ties go to the lower
+  position.
+* H2O: a key's score is the attention mass it receives from every prompt
+  query under the causal softmax of Sec. 4.2, summed over the G query heads of
+  its KV head (the accumulated-attention "heavy hitter" score).  Reading: the
+  queries are the prefill's (post-RoPE) queries at all N_x positions; there is
+  no pooling; the last w positions are kept as a recent window and count
+  toward n_keep, the prefix j < N_x - w competes; ties go to the lower
   position.
 * Average-pool SnapKV: the window scores of timebill_oracle.window_scores
   smoothed by a mean instead of a max.  Reading: odd kernel P, stride 1,
@@ -24,7 +31,7 @@ from __future__ import annotations
 
 import numpy as np
 
-__all__ = ["knorm_scores", "avg_pool"]
+__all__ = ["knorm_scores", "avg_pool", "h2o_scores"]
 
 
 def knorm_scores(k: np.ndarray, n_x: int, w: int) -> np.ndarray:
@@ -48,3 +55,24 @@ def avg_pool(a: np.ndarray, pool: int) -> np.ndarray:
     for off in range(pool):             # sum of the pool shifted copies
         out += padded[..., off:off + n]
     return out / pool
+
+
+def h2o_scores(q: np.ndarray, k: np.ndarray, n_x: int) -> np.ndarray:
+    """q [Hq, >= n_x, d], k [Hkv, >= n_x, d] -> [Hkv, n_x]: for key j, the sum over
+    the group's query heads h and query positions i >= j of
+    softmax_{j' <= i}(q[h, i] . k[j'] / sqrt(d)) at j'."""
+    hq, hkv = q.shape[0], k.shape[0]
+    G = hq // hkv
+    d = q.shape[-1]
+    scale = 1.0 / np.sqrt(d)
+    causal = np.tril(np.ones((n_x, n_x), dtype=bool))          # row i sees j <= i
+    out = np.zeros((hkv, n_x), dtype=np.float64)
+    for h in range(hq):
+        g = h // G
+        s = (np.asarray(q[h, :n_x], dtype=np.float64) @ np.asarray(k[g, :n_x], dtype=np.float64).T) * scale
+        s = np.where(causal, s, -np.inf)
+        s -= s.max(axis=1, keepdims=True)
+        p = np.exp(s)
+        p /= p.sum(axis=1, keepdims=True)
+        out[g] += p.sum(axis=0)
+    return out

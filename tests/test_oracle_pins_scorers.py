@@ -96,3 +96,50 @@ def test_select_keep_signed_scores_bruteforce():
                     best, best_sum = sub, s                   # so the first maximum is the smallest set
             want = list(best) + list(range(pref, n_x))
             assert O.select_keep(sc, n_x, w, n_keep).tolist() == want
+
+
+def test_h2o_hand_example():
+    ex = _ex()["h2o"]
+    c = np.array(ex["c"], dtype=np.float64)
+    k = np.log(c).reshape(1, ex["n_x"], 1)
+    q = np.array(ex["q"], dtype=np.float64).reshape(1, ex["n_x"], 1)
+    sc = S.h2o_scores(q, k, ex["n_x"])[0]
+    np.testing.assert_allclose(sc, _frac(ex["scores"]), rtol=1e-15)
+    for case in ex["keep"]:
+        n_keep = O.keep_count(ex["n_x"], case["alpha"], ex["w"])
+        assert n_keep == case["n_keep"]
+        keep = O.select_keep(sc[: ex["n_x"] - ex["w"]], ex["n_x"], ex["w"], n_keep)
+        assert keep.tolist() == case["keep"], case
+
+
+def test_h2o_total_mass_and_torch():
+    """Every causal row sums to 1, so the scores of a KV head total G * N_x; the
+    column sums equal those of torch's float64 softmax over a masked product."""
+    rng = np.random.default_rng(5)
+    hq, hkv, n, d = 6, 2, 97, 32
+    q = rng.standard_normal((hq, n, d))
+    k = rng.standard_normal((hkv, n, d)) * 1.5
+    sc = S.h2o_scores(q, k, n)
+    np.testing.assert_allclose(sc.sum(axis=1), np.full(hkv, (hq // hkv) * n), rtol=1e-13)
+    qt = torch.from_numpy(q)
+    kt = torch.from_numpy(k).repeat_interleave(hq // hkv, dim=0)
+    mask = torch.ones(n, n, dtype=torch.bool).tril()
+    logits = (qt @ kt.transpose(1, 2)) / math.sqrt(d)
+    p = torch.softmax(logits.masked_fill(~mask, float("-inf")), dim=-1)
+    ref = p.sum(dim=1).reshape(hkv, hq // hkv, n).sum(dim=1).numpy()
+    np.testing.assert_allclose(sc, ref, rtol=1e-12)
+
+
+def test_h2o_last_row_only_matches_window_mass():
+    """The last query row's contribution equals the window column mass of a
+    one-row window at the last position (both are one causal softmax row)."""
+    rng = np.random.default_rng(8)
+    hq, hkv, n, d = 2, 1, 40, 16
+    q = rng.standard_normal((hq, n, d))
+    k = rng.standard_normal((hkv, n, d))
+    full = S.h2o_scores(q, k, n)
+    head = S.h2o_scores(q[:, : n - 1], k, n - 1)                 # rows 0 .. n-2
+    last = full[0].copy()
+    last[: n - 1] -= head[0]
+    mass = O.window_column_mass(q[:, n - 1:], k, n, 0)
+    np.testing.assert_allclose(last, mass, rtol=1e-12, atol=1e-15)
