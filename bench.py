@@ -270,9 +270,9 @@ def cold_decode(torch, _lib, Evictor, dev, wl, q_win, k, v, qd, knd, vnd,
 
 def scorer_variants(torch, _lib, synth, Evictor, dev, reps=10):
     """Supplementary: scoring time of each scorer (max-pool window scores, the
-    mean-pooled variant, KNorm) at the L = 8192 and L = 131072 shapes, from a
-    graph of `reps` scoring calls; KNorm's bandwidth counts one read of K plus
-    the fp32 scores written."""
+    mean-pooled variant, KNorm, and at L = 8192 H2O) at the L = 8192 and
+    L = 131072 shapes, from a graph of `reps` scoring calls (2 for H2O); KNorm's
+    bandwidth counts one read of K plus the fp32 scores written."""
     out = {}
     for wid in (2, 5):
         wl = synth.WORKLOADS[wid]
@@ -280,24 +280,36 @@ def scorer_variants(torch, _lib, synth, Evictor, dev, reps=10):
         pr = synth.make_prompt(wl)
         q_win, k = pr["q_win"].to(dev), pr["k"].to(dev)
         del pr
+        # H2O needs the queries of every prompt position and ~2 Hq L^2 d float64
+        # flops per call: measured at L = 8192 only (L = 131072 would be 141 TFLOP)
+        scorers = ("snapkv", "snapkv_avg", "knorm") + (("h2o",) if L <= 8192 else ())
+        q_all = synth.make_queries(wl).to(dev) if "h2o" in scorers else None
         row = {}
-        for scorer in ("snapkv", "snapkv_avg", "knorm"):
+        for scorer in scorers:
             ev = Evictor(B, L, Hq, Hkv, d, w, wl.pool, device=dev, scorer=scorer)
+            qin = q_all if scorer == "h2o" else q_win
+            n = 2 if scorer == "h2o" else reps
             cs = torch.cuda.Stream()
-            ev.score(q_win, k, [L], cs)
+            ev.score(qin, k, [L], cs)
             torch.cuda.synchronize()
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=cs):
-                for _ in range(reps):
-                    ev.score(q_win, k, [L], cs)
+                for _ in range(n):
+                    ev.score(qin, k, [L], cs)
             torch.cuda.synchronize()
-            us = _best_ms(torch, g.replay) * 1e3 / reps
+            us = _best_ms(torch, g.replay) * 1e3 / n
             row[scorer] = {"us": round(us, 2)}
             if scorer == "knorm":
                 nbytes = Hkv * L * d * 2 + Hkv * (L - w) * 4
                 row[scorer]["GBps"] = round(nbytes / (us * 1e-6) / 1e9, 1)
                 row[scorer]["frac_of_8TBps"] = round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+            if scorer == "h2o":
+                # two passes over the causal pairs (i >= j), 2 d flops per pair and head
+                flops = 2 * 2 * Hq * d * (L * (L + 1) // 2)
+                row[scorer]["fp64_TFLOPs"] = round(flops / (us * 1e-6) / 1e12, 2)
+                row[scorer]["frac_of_78.6"] = round(flops / (us * 1e-6) / 1e12 / 78.6, 4)
             del g, ev
+        del q_all
         out[f"L{L}_{Hq}q{Hkv}kv"] = row
         del q_win, k
         torch.cuda.empty_cache()

@@ -11,8 +11,9 @@
  *
  *   tb_score_window  observation-window scores (softmax of the last w queries
  *                    against the prompt keys, summed per KV head, max-pooled);
- *                    tb_score_window_avgpool and tb_score_knorm are the
- *                    scorer variants (mean-pooled window scores; key norms);
+ *                    tb_score_window_avgpool, tb_score_knorm and
+ *                    tb_score_h2o are the scorer variants (mean-pooled window
+ *                    scores; key norms; accumulated attention of all queries);
  *   tb_select_topk   per-KV-head top-k of the scores keeping n_keep positions;
  *   tb_compact_kv    gather of the kept K/V rows into a compact cache;
  *   tb_decode_attn   single-token grouped-query decode attention over the
@@ -76,7 +77,8 @@ typedef enum {
   TB_OP_SCORE = 0,
   TB_OP_SELECT = 1,
   TB_OP_COMPACT = 2,
-  TB_OP_DECODE = 3
+  TB_OP_DECODE = 3,
+  TB_OP_H2O = 4
 } tb_op;
 
 /* [host] Retained positions after evicting a fraction alpha of L prompt
@@ -131,6 +133,23 @@ tb_status tb_score_window_avgpool(const void* q_win, const void* k, int32_t B,
 tb_status tb_score_knorm(const void* k, int32_t B, const int32_t* L, int32_t Lmax,
                          int32_t Hkv, int32_t d, int32_t w, tb_dtype dt,
                          float* scores, hipStream_t stream);
+
+/* H2O scores (the accumulated-attention scorer cited for the fixed-ratio
+ * baselines, Sec. 6.1): for KV head g of sequence b and every position j < L[b],
+ *   scores[j] = sum over the G query heads h of group g and query positions
+ *               i >= j of softmax_j'(q[h][i] . k[j'] / sqrt(d)),  j' <= i,
+ * i.e. the attention mass key j receives from all prompt queries under the
+ * causal softmax of Sec. 4.2.  tb_select_topk then keeps the largest prefix
+ * scores plus the last w positions (the recent window).
+ *   q: [B][Hq][Lmax][d], the prefill's queries at every prompt position.
+ * Arithmetic: float64 dot products and sums (two passes over the causal
+ * product: row statistics, then column mass), fp32 output.  Cost grows as
+ * L^2: about 2 Hq L^2 d flops per call.
+ * L: [host][B].  Requires 1 <= L[b] <= Lmax.
+ * ws: tb_workspace_bytes(TB_OP_H2O, B, Lmax, Hq, Hkv, d, 0, 0) bytes. */
+tb_status tb_score_h2o(const void* q, const void* k, int32_t B, const int32_t* L,
+                       int32_t Lmax, int32_t Hq, int32_t Hkv, int32_t d, tb_dtype dt,
+                       float* scores, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Per-KV-head top-k keeping n_keep[b] = tb_keep_count(L[b], alpha[b], w)
  * positions (Eq. N_kv: a fraction alpha of the prompt's KV is evicted once,

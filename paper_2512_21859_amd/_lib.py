@@ -18,11 +18,11 @@ LIB_PATH = os.path.join(_HERE, "libtimebill.so")
 
 TB_OK, TB_EINVAL, TB_EUNSUPPORTED, TB_EWORKSPACE, TB_EHIP, TB_EINTERNAL = range(6)
 TB_F32, TB_BF16 = 0, 1
-TB_OP_SCORE, TB_OP_SELECT, TB_OP_COMPACT, TB_OP_DECODE = range(4)
+TB_OP_SCORE, TB_OP_SELECT, TB_OP_COMPACT, TB_OP_DECODE, TB_OP_H2O = range(5)
 V_TILE = 32          # the compact V cache is stored as transposed tiles of 32 rows
 
 EXPORTED = ("tb_keep_count", "tb_last_error", "tb_workspace_bytes", "tb_score_window",
-            "tb_score_window_avgpool", "tb_score_knorm", "tb_select_topk", "tb_compact_kv", "tb_decode_attn", "tb_ete_fit", "tb_wcet",
+            "tb_score_window_avgpool", "tb_score_knorm", "tb_score_h2o", "tb_select_topk", "tb_compact_kv", "tb_decode_attn", "tb_ete_fit", "tb_wcet",
             "tb_alpha_star")
 
 _lib = None
@@ -58,6 +58,8 @@ def load() -> ctypes.CDLL:
     lib.tb_score_window_avgpool.restype = i32
     lib.tb_score_knorm.argtypes = [vp, i32, p_i32, i32, i32, i32, i32, i32, vp, vp]
     lib.tb_score_knorm.restype = i32
+    lib.tb_score_h2o.argtypes = [vp, vp, i32, p_i32, i32, i32, i32, i32, i32, vp, vp, sz, vp]
+    lib.tb_score_h2o.restype = i32
     lib.tb_select_topk.argtypes = [vp, i32, p_i32, i32, i32, i32, p_dbl, vp, p_i32, vp, sz, vp]
     lib.tb_select_topk.restype = i32
     lib.tb_compact_kv.argtypes = [vp, vp, vp, i32, p_i32, i32, i32, i32, i32, i32, vp, vp, vp,
@@ -150,6 +152,21 @@ def tb_score_knorm(k: torch.Tensor, L: Sequence[int], w: int, scores: torch.Tens
     _check(load().tb_score_knorm(_dev(k, "k"), B, _i32_array(L), Lmax, Hkv, d, w,
                                  _dtype_code(k), _dev(scores, "scores", torch.float32),
                                  _stream(stream)))
+
+
+def tb_score_h2o(q: torch.Tensor, k: torch.Tensor, L: Sequence[int], scores: torch.Tensor,
+                 ws: torch.Tensor, stream=None) -> None:
+    """q [B,Hq,Lmax,d] (all prompt queries), k [B,Hkv,Lmax,d] -> scores [B,Hkv,Lmax]
+    fp32: the attention mass each key receives from every prompt query."""
+    B, Hq, Lmax, d = q.shape
+    _, Hkv, Lmax2, d2 = k.shape
+    if Lmax2 != Lmax or d2 != d or k.shape[0] != B or k.dtype != q.dtype:
+        raise ValueError("q / k shapes or dtypes disagree")
+    if tuple(scores.shape) != (B, Hkv, Lmax):
+        raise ValueError("scores must be [B, Hkv, Lmax]")
+    _check(load().tb_score_h2o(_dev(q, "q"), _dev(k, "k"), B, _i32_array(L), Lmax, Hq, Hkv, d,
+                               _dtype_code(k), _dev(scores, "scores", torch.float32),
+                               _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def tb_select_topk(scores: torch.Tensor, L: Sequence[int], w: int, alpha: Sequence[float],

@@ -127,6 +127,13 @@ size_t tb_workspace_bytes(int32_t op, int32_t B, int32_t Lmax, int32_t Hq, int32
       case TB_OP_SELECT:
       case TB_OP_COMPACT:
         return 0;
+      case TB_OP_H2O: {
+        if (B < 1 || Lmax < 1 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0) {
+          fail(TB_EINVAL, "tb_workspace_bytes(H2O): bad sizes");
+          return 0;
+        }
+        return tb::h2o_ws_bytes(B, Lmax, Hq);
+      }
       case TB_OP_DECODE: {
         if (B < 1 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0 || cap < 1 || d < 1) {
           fail(TB_EINVAL, "tb_workspace_bytes(DECODE): bad sizes");
@@ -213,6 +220,36 @@ tb_status tb_score_window_avgpool(const void* q_win, const void* k, int32_t B, c
                                   void* ws, size_t ws_bytes, hipStream_t stream) {
   return score_window_impl("tb_score_window_avgpool", true, q_win, k, B, L, Lmax, Hq, Hkv, d, w,
                            pool, dt, scores, raw_scores, ws, ws_bytes, stream);
+}
+
+tb_status tb_score_h2o(const void* q, const void* k, int32_t B, const int32_t* L, int32_t Lmax,
+                       int32_t Hq, int32_t Hkv, int32_t d, tb_dtype dt, float* scores, void* ws,
+                       size_t ws_bytes, hipStream_t stream) {
+  try {
+    if (!q || !k || !L || !scores) return fail(TB_EINVAL, "tb_score_h2o: null pointer");
+    tb_status st = check_common(B, Hq, Hkv, d, dt);
+    if (st != TB_OK) return st;
+    tb::H2oArgs a{};
+    for (int b = 0; b < B; ++b) {
+      if (!(L[b] >= 1 && L[b] <= Lmax))
+        return fail(TB_EINVAL, "need 1 <= L[%d] <= Lmax (L=%d, Lmax=%d)", b, L[b], Lmax);
+      a.L[b] = L[b];
+    }
+    const size_t need = tb::h2o_ws_bytes(B, Lmax, Hq);
+    if (ws_bytes < need || !ws)
+      return fail(TB_EWORKSPACE, "tb_score_h2o: workspace %zu < %zu bytes", ws_bytes, need);
+    const size_t part = align256(static_cast<size_t>(B) * Hq * Lmax * sizeof(double));
+    char* p = static_cast<char*>(ws);
+    a.row_M = reinterpret_cast<double*>(p);
+    a.row_Z = reinterpret_cast<double*>(p + part);
+    a.col_part = reinterpret_cast<double*>(p + 2 * part);
+    a.q = q; a.k = k; a.scores = scores;
+    a.B = B; a.Lmax = Lmax; a.Hq = Hq; a.Hkv = Hkv;
+    a.scale = 1.0 / sqrt(static_cast<double>(d));
+    return hip_status(tb::launch_h2o(a, d, dt == TB_BF16, stream), "tb_score_h2o launch");
+  } catch (...) {
+    return fail(TB_EINTERNAL, "tb_score_h2o: internal error");
+  }
 }
 
 tb_status tb_score_knorm(const void* k, int32_t B, const int32_t* L, int32_t Lmax, int32_t Hkv,

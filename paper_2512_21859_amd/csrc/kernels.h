@@ -41,6 +41,21 @@ struct KnormArgs {
 };
 hipError_t launch_knorm(const KnormArgs& a, int d, bool bf16, hipStream_t st);
 
+// ---------------------------------------------------------------- H2O
+struct H2oArgs {
+  const void* q;          // [B][Hq][Lmax][d]  all prompt queries
+  const void* k;          // [B][Hkv][Lmax][d]
+  float* scores;          // [B][Hkv][Lmax]: accumulated attention for j < L[b]
+  double* row_M;          // ws: [B][Hq][Lmax] row max (logit units)
+  double* row_Z;          // ws: [B][Hq][Lmax] row normaliser
+  double* col_part;       // ws: [B][Hq][Lmax] per-head column mass
+  int32_t B, Lmax, Hq, Hkv;
+  double scale;           // 1/sqrt(d)
+  int32_t L[kMaxB];
+};
+size_t h2o_ws_bytes(int B, int Lmax, int Hq);
+hipError_t launch_h2o(const H2oArgs& a, int d, bool bf16, hipStream_t st);
+
 // ---------------------------------------------------------------- selection
 struct SelectArgs {
   const float* scores;    // [B][Hkv][Lmax]

@@ -15,15 +15,17 @@ import torch
 from . import _lib
 
 
-SCORERS = ("snapkv", "snapkv_avg", "knorm")
+SCORERS = ("snapkv", "snapkv_avg", "knorm", "h2o")
 
 
 class Evictor:
     """Score / select buffers and workspace for one layer shape.
 
     scorer: "snapkv" (observation-window scores, max-pooled; the paper's
-    eviction), "snapkv_avg" (the same scores mean-pooled) or "knorm" (negated
-    key norms; the window queries are not used)."""
+    eviction), "snapkv_avg" (the same scores mean-pooled), "knorm" (negated
+    key norms; the window queries are not used) or "h2o" (accumulated
+    attention of every prompt query: score() then takes all the prefill's
+    queries [B, Hq, Lmax, d] in place of the window queries)."""
 
     def __init__(self, B: int, Lmax: int, Hq: int, Hkv: int, d: int, w: int, pool: int,
                  device="cuda", keep_raw: bool = False, scorer: str = "snapkv"):
@@ -35,13 +37,19 @@ class Evictor:
         self.raw = (torch.empty((B, Hkv, Lmax), dtype=torch.float32, device=device)
                     if keep_raw else None)
         self.keep_idx = torch.empty((B, Hkv, Lmax), dtype=torch.int32, device=device)
-        nbytes = (_lib.tb_workspace_bytes(_lib.TB_OP_SCORE, B, Lmax, Hq, Hkv, d, w, 0)
-                  if scorer != "knorm" else 0)
+        if scorer == "knorm":
+            nbytes = 0
+        elif scorer == "h2o":
+            nbytes = _lib.tb_workspace_bytes(_lib.TB_OP_H2O, B, Lmax, Hq, Hkv, d, 0, 0)
+        else:
+            nbytes = _lib.tb_workspace_bytes(_lib.TB_OP_SCORE, B, Lmax, Hq, Hkv, d, w, 0)
         self.ws = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=device)
 
     def score(self, q_win: torch.Tensor, k: torch.Tensor, L: Sequence[int], stream=None) -> None:
         if self.scorer == "knorm":
             _lib.tb_score_knorm(k, L, self.w, self.scores, stream)
+        elif self.scorer == "h2o":
+            _lib.tb_score_h2o(q_win, k, L, self.scores, self.ws, stream)
         else:
             _lib.tb_score_window(q_win, k, L, self.w, self.pool, self.scores, self.raw, self.ws,
                                  stream, avgpool=self.scorer == "snapkv_avg")

@@ -8,7 +8,9 @@ values.
 
 Seeds: 1_000_000 * workload_id + 1000 * layer + stream, with stream 0 for
 K, V and window queries, 1 for heavy-hitter positions and directions, 2 for
-decode-step q / k / v and 3 for per-sequence lengths and eviction ratios.
+decode-step q / k / v, 3 for per-sequence lengths and eviction ratios and 4
+for the queries at every prompt position (used by the accumulated-attention
+scorer).
 
 The workloads stand in for the paper's LongBench prompts on Qwen2.5-7B-Instruct
 (context up to 32768 tokens, Sec. 6.1): head shapes 28 query / 4 KV heads of
@@ -132,6 +134,18 @@ def make_prompt(wl: Workload, layer: int = 0, L: Optional[List[int]] = None,
                 k[b, gk, pos] = (4.0 * math.sqrt(d)) * u
     return {"q_win": q_win.to(wl.dtype), "k": k.to(wl.dtype), "v": v.to(wl.dtype),
             "L": list(L)}
+
+
+def make_queries(wl: Workload, layer: int = 0, L: Optional[List[int]] = None):
+    """Queries at every prompt position: [B, Hq, Lmax, d] in the workload dtype,
+    N(0,1) (stream 4); rows j >= L[b] are zero."""
+    if L is None:
+        L, _ = lengths_and_alphas(wl)
+    g4 = _gen(seed_of(wl.wid, layer, 4))
+    q = torch.zeros((wl.B, wl.Hq, max(L), wl.d), dtype=torch.float32)
+    for b in range(wl.B):
+        q[b, :, : L[b]] = torch.randn((wl.Hq, L[b], wl.d), generator=g4)
+    return q.to(wl.dtype)
 
 
 def make_decode(wl: Workload, layer: int = 0, T: Optional[int] = None):

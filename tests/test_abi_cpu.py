@@ -23,7 +23,7 @@ def lib():
 
 def _declared():
     text = open(HEADER).read()
-    decl = r"^(?:int32_t|size_t|double|tb_status|const char\*)\s+(tb_[a-z_]+)\("
+    decl = r"^(?:int32_t|size_t|double|tb_status|const char\*)\s+(tb_[a-z0-9_]+)\("
     return sorted(set(re.findall(decl, text, re.M)))
 
 
@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(_lib.EXPORTED), names
     nm = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True,
                         text=True, check=True).stdout
-    exported = set(re.findall(r" T (tb_[a-z_]+)$", nm, re.M))
+    exported = set(re.findall(r" T (tb_[a-z0-9_]+)$", nm, re.M))
     for n in names:
         assert n in exported, f"{n} not exported"
         assert hasattr(lib, n)
@@ -125,6 +125,25 @@ def test_score_knorm_validation(lib):
     assert call(w=100) == E.TB_EINVAL
     assert call(L=101) == E.TB_EINVAL
     assert b"L[0]" in lib.tb_last_error()
+
+
+def test_score_h2o_validation(lib):
+    E = _lib
+
+    def call(q=FAKE, k=FAKE, B=1, L=100, Lmax=100, Hq=4, Hkv=2, d=128, dt=_lib.TB_BF16,
+             sc=FAKE, ws=FAKE, wsb=1 << 30):
+        return lib.tb_score_h2o(q, k, B, _i32(L), Lmax, Hq, Hkv, d, dt, sc, ws, wsb, None)
+
+    assert call(q=None) == E.TB_EINVAL
+    assert call(B=0) == E.TB_EINVAL
+    assert call(Hq=5) == E.TB_EINVAL
+    assert call(d=96) == E.TB_EUNSUPPORTED
+    assert call(L=0) == E.TB_EINVAL
+    assert call(L=101) == E.TB_EINVAL
+    need = _lib.tb_workspace_bytes(_lib.TB_OP_H2O, 1, 100, 4, 2, 128, 0, 0)
+    assert need >= 3 * 4 * 100 * 8
+    assert call(wsb=need - 1) == E.TB_EWORKSPACE
+    assert call(ws=None) == E.TB_EWORKSPACE
 
 
 def test_select_validation(lib):

@@ -164,3 +164,96 @@ def test_knorm_long_context(alpha):
     kk = keep.cpu().numpy()
     for g in range(wl.Hkv):
         check_keep(kk[0, g, :n_keep[0]], ref[g], wl.L, w, n_keep[0], f"knorm L=131072 g={g}")
+
+
+# ------------------------------------------------------------------ H2O
+def _h2o_gpu(q, k, L):
+    B, Hq, Lmax, d = q.shape
+    Hkv = k.shape[1]
+    ws = torch.empty((_lib.tb_workspace_bytes(_lib.TB_OP_H2O, B, Lmax, Hq, Hkv, d, 0, 0),),
+                     dtype=torch.uint8, device=DEV)
+    scores = torch.full((B, Hkv, Lmax), 123.0, dtype=torch.float32, device=DEV)
+    _lib.tb_score_h2o(q.to(DEV), k.to(DEV), L, scores, ws)
+    torch.cuda.synchronize()
+    return f64(scores)
+
+
+@pytest.mark.parametrize("dtype,d,Hq,Hkv,L", [
+    (torch.bfloat16, 128, 14, 2, [1000, 257]),
+    (torch.float32, 64, 4, 2, [300]),
+    (torch.bfloat16, 64, 3, 3, [37, 64, 65]),
+])
+def test_h2o_scores_and_selection(dtype, d, Hq, Hkv, L):
+    case(f"h2o dtype={dtype} d={d} Hq={Hq} Hkv={Hkv} L={L}")
+    wl = synth.custom(970 + d + Hq, dtype, len(L), L, Hq, Hkv, d, 16, 1, 1)
+    pr = synth.make_prompt(wl, L=L, pad_value=5.0)
+    q = synth.make_queries(wl, L=L)
+    sc = _h2o_gpu(q, pr["k"], L)
+    G, w = Hq // Hkv, min(16, min(L) - 1)
+    for b in range(len(L)):
+        ref = S.h2o_scores(f64(q[b]), f64(pr["k"][b]), L[b])
+        assert score_rel_err(sc[b, :, : L[b]], ref) <= AVG_REL_TOL
+        np.testing.assert_allclose(sc[b, :, : L[b]].sum(axis=1), G * L[b], rtol=1e-6)
+        assert np.all(sc[b, :, L[b]:] == 123.0)
+        keep = torch.full((1, Hkv, L[b]), -1, dtype=torch.int32, device=DEV)
+        for alpha in (0.3, 0.7):
+            n_keep = _lib.tb_select_topk(torch.from_numpy(sc[b:b + 1, :, : L[b]]).float().to(DEV),
+                                         [L[b]], w, [alpha], keep)
+            torch.cuda.synchronize()
+            kk = keep.cpu().numpy()
+            for g in range(Hkv):
+                check_keep(kk[0, g, :n_keep[0]], ref[g, : L[b] - w], L[b], w, n_keep[0],
+                           f"h2o b={b} g={g} alpha={alpha}")
+
+
+def test_h2o_full_size_sampled():
+    """L = 8192 workload shape: every KV head's scores total G * L, and the last
+    64 columns (which only need the statistics of the last 64 query rows) match
+    the oracle computed column by column."""
+    wl = synth.WORKLOADS[2]
+    case(f"h2o full size {wl.name}: total mass and the last 64 columns")
+    pr = synth.make_prompt(wl)
+    q = synth.make_queries(wl)
+    L = wl.L
+    sc = _h2o_gpu(q, pr["k"], [L])[0]
+    G = wl.Hq // wl.Hkv
+    np.testing.assert_allclose(sc[:, :L].sum(axis=1), G * L, rtol=1e-6)
+    q64, k64 = f64(q[0]), f64(pr["k"][0])
+    tail = 64
+    want = np.zeros((wl.Hkv, tail))
+    for h in range(wl.Hq):
+        g = h // G
+        s = (q64[h, L - tail:] @ k64[g, :L].T) / np.sqrt(wl.d)          # rows L-64 .. L-1
+        rows = np.arange(L - tail, L)[:, None]
+        s = np.where(np.arange(L)[None, :] <= rows, s, -np.inf)
+        p = np.exp(s - s.max(axis=1, keepdims=True))
+        p /= p.sum(axis=1, keepdims=True)
+        want[g] += p[:, L - tail:].sum(axis=0)                           # columns L-64 .. L-1
+    assert score_rel_err(sc[:, L - tail: L], want) <= AVG_REL_TOL
+
+
+def test_h2o_end_to_end_decode():
+    wl = synth.custom(990, torch.bfloat16, 1, [1500], 8, 2, 128, 32, 1, 6)
+    L, T, alpha = [1500], 6, 0.6
+    case(f"h2o end to end L={L} alpha={alpha}, {T} decode steps")
+    pr = synth.make_prompt(wl, L=L)
+    dc = synth.make_decode(wl, T=T)
+    q = synth.make_queries(wl, L=L)
+    ev = Evictor(1, L[0], wl.Hq, wl.Hkv, wl.d, wl.w, 1, scorer="h2o")
+    cache = _lib.KVCache(1, wl.Hq, wl.Hkv, _lib.tb_keep_count(L[0], alpha, wl.w) + T, wl.d,
+                         wl.dtype)
+    n_keep = ev.evict(q.to(DEV), pr["k"].to(DEV), pr["v"].to(DEV), L, [alpha], cache)
+    out = run_decode(cache, dc["q"].to(DEV), dc["k_new"].to(DEV), dc["v_new"].to(DEV))
+    torch.cuda.synchronize()
+    k64, v64 = f64(pr["k"][0]), f64(pr["v"][0])
+    ref = S.h2o_scores(f64(q[0]), k64, L[0])[:, : L[0] - wl.w]
+    kk = ev.keep_idx.cpu().numpy()
+    for g in range(wl.Hkv):
+        check_keep(kk[0, g, :n_keep[0]], ref[g], L[0], wl.w, n_keep[0], f"h2o g={g}")
+    kept = kk[0, :, :n_keep[0]]
+    kc = np.stack([k64[g, kept[g]] for g in range(wl.Hkv)])
+    vc = np.stack([v64[g, kept[g]] for g in range(wl.Hkv)])
+    res = O.decode_sequence(f64(dc["q"][:, 0]), f64(dc["k_new"][:, 0]), f64(dc["v_new"][:, 0]),
+                            kc, vc)
+    want = np.stack([res[t] for t in range(T)])
+    assert float(np.max(np.abs(f64(out[:, 0]) - want))) <= DECODE_TOL[wl.dtype]
