@@ -1,0 +1,135 @@
+"""GPU edge cases through the C ABI against the float64 oracle: the largest
+batch, the smallest prefixes, pools wider than the prefix, empty and one-row
+caches, and inputs whose results are fixed by the mathematics (q = 0 gives the
+mean of V; a single row gives that row; equal keys give uniform softmax
+rows, so ties are resolved by position)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import timebill_oracle as O
+from paper_2512_21859_amd import _lib, synth
+from paper_2512_21859_amd.pipeline import Evictor
+from tests.parity_util import DECODE_TOL, check_keep, f64, score_rel_err
+from tests.test_parity_gpu import SCORE_REL_TOL, _run_layer
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU in this container")
+    _lib.load()
+    torch.cuda.init()
+
+
+def case(msg):
+    print(f"\n[case] {msg}", flush=True)
+
+
+def test_max_batch_ragged_end_to_end():
+    """B = 64 (the largest batch): ragged short prompts and per-sequence ratios."""
+    rng = np.random.default_rng(64)
+    L = rng.integers(9, 300, 64).tolist()
+    alphas = rng.uniform(0.0, 0.95, 64).tolist()
+    case(f"B=64 ragged L in [{min(L)}, {max(L)}], per-sequence alpha")
+    wl = synth.custom(1064, torch.bfloat16, 64, L, 8, 2, 64, 8, 5, 4)
+    _run_layer(wl, 0, L, alphas, 4, [0, 3])
+
+
+@pytest.mark.parametrize("pool", [1, 3, 129])
+def test_smallest_prefix_and_wide_pool(pool):
+    """L = w + 1 (one prefix position) and L = w + 5 with a pool wider than
+    the prefix; ratios that keep everything, only the window, or in between."""
+    case(f"prefix of 1 and 5 positions, pool={pool}")
+    w = 8
+    L = [w + 1, w + 5]
+    wl = synth.custom(1100 + pool, torch.float32, 2, L, 4, 2, 64, w, pool, 3)
+    for alphas in ([0.0, 0.0], [0.5, 0.3], [0.99, 0.9]):
+        _run_layer(wl, 0, L, alphas, 3, [0, 2])
+
+
+def _cache_with(B, Hq, Hkv, d, cap, dtype, kc, vc, lens):
+    cache = _lib.KVCache(B, Hq, Hkv, cap, d, dtype)
+    cache.k.copy_(kc)
+    cache.v.copy_(_lib.v_rows_to_tiles(vc))
+    cache.kv_len.copy_(torch.tensor(lens, dtype=torch.int32))
+    cache.host_len = list(lens)
+    return cache
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_decode_empty_and_one_row_caches(dtype):
+    """kv_len = 0 with an append attends over the new row alone, so the output
+    is that row's value for every query head; without an append there is
+    nothing to attend and the output is zero.  The length advances only with
+    the append."""
+    case(f"decode over empty caches dtype={dtype}")
+    B, Hkv, G, d, cap = 2, 2, 4, 128, 64
+    Hq = G * Hkv
+    g = torch.Generator().manual_seed(5)
+    z = torch.zeros((B, Hkv, cap, d), dtype=dtype)
+    cache = _cache_with(B, Hq, Hkv, d, cap, dtype, z, z, [0, 0])
+    q = torch.randn((B, Hq, d), generator=g).to(dtype).to(DEV)
+    kn = torch.randn((B, Hkv, d), generator=g).to(dtype).to(DEV)
+    vn = torch.randn((B, Hkv, d), generator=g).to(dtype).to(DEV)
+    out = torch.empty((B, Hq, d), dtype=dtype, device=DEV)
+    cache.decode(q, None, None, out)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(out).item() == 0
+    assert cache.kv_len.cpu().tolist() == [0, 0]
+    cache.decode(q, kn, vn, out)
+    torch.cuda.synchronize()
+    want = vn.repeat_interleave(G, dim=1)
+    assert torch.equal(out, want)                       # one row: the weight is exactly 1
+    assert cache.kv_len.cpu().tolist() == [1, 1]
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_decode_zero_query_is_mean_of_values(dtype):
+    """q = 0 makes every logit 0, so the output is the mean of the cached and
+    appended values (checked against the float64 mean)."""
+    case(f"decode with q = 0 dtype={dtype}")
+    B, Hkv, G, d, cap = 1, 2, 7, 128, 2048
+    Hq = G * Hkv
+    lens = [1999]
+    g = torch.Generator().manual_seed(6)
+    kc = torch.randn((B, Hkv, cap, d), generator=g).to(dtype)
+    vc = torch.randn((B, Hkv, cap, d), generator=g).to(dtype)
+    cache = _cache_with(B, Hq, Hkv, d, cap, dtype, kc, vc, lens)
+    q = torch.zeros((B, Hq, d), dtype=dtype, device=DEV)
+    kn = torch.randn((B, Hkv, d), generator=g).to(dtype)
+    vn = torch.randn((B, Hkv, d), generator=g).to(dtype)
+    out = torch.empty((B, Hq, d), dtype=dtype, device=DEV)
+    cache.decode(q, kn.to(DEV), vn.to(DEV), out)
+    torch.cuda.synchronize()
+    rows = torch.cat([vc[0, :, : lens[0]], vn[0][:, None, :]], dim=1).to(torch.float64)
+    want = rows.mean(dim=1).repeat_interleave(G, dim=0).numpy()
+    err = float(np.abs(f64(out[0]) - want).max())
+    assert err <= DECODE_TOL[dtype], err
+
+
+def test_equal_keys_select_by_position():
+    """Identical keys give every window row a uniform softmax, so all prefix
+    scores tie and the selection keeps the lowest positions."""
+    case("equal keys: uniform scores, ties to the lowest positions")
+    L, w, Hq, Hkv, d = [300], 16, 4, 2, 64
+    wl = synth.custom(1200, torch.float32, 1, L, Hq, Hkv, d, w, 3, 1, heavy="none")
+    pr = synth.make_prompt(wl, L=L)
+    k = pr["k"].clone()
+    k[:] = k[:, :, :1, :]                                # every key equals key 0
+    ev = Evictor(1, L[0], Hq, Hkv, d, w, 3)
+    ev.score(pr["q_win"].to(DEV), k.to(DEV), L)
+    n_keep = ev.select(L, [0.5])
+    torch.cuda.synchronize()
+    kk = ev.keep_idx.cpu().numpy()
+    pooled = O.max_pool(O.window_scores(f64(pr["q_win"][0]), f64(k[0]), L[0], w), 3)
+    assert score_rel_err(ev.scores.cpu().numpy()[0, :, : L[0] - w], pooled) <= SCORE_REL_TOL
+    n_sel = n_keep[0] - w
+    for g in range(Hkv):
+        check_keep(kk[0, g, :n_keep[0]], pooled[g], L[0], w, n_keep[0], f"equal keys g={g}")
+        # every window row sees all prefix positions with the same weight, so the
+        # prefix scores all tie and the lowest n_sel positions are kept
+        assert kk[0, g, :n_sel].tolist() == list(range(n_sel))
