@@ -229,6 +229,17 @@ double tb_alpha_star(const double* prefill_abc, const double* step_pq, double n_
                      int32_t n_hat_w, double budget, double t_predict, double alpha_max,
                      int32_t* feasible);
 
+/* [host] Longest predictor input that runs within the prefill phase
+ * (Sec. 5.2, deployment: the response-length predictor runs beside the
+ * prefill, and its input prompt is compressed so that its own execution time
+ * a_p N_p^2 + b_p N_p + c_p does not exceed a N_x^2 + b N_x + c).  Returns the
+ * largest integer N_p in [0, max_len] satisfying that bound, -1 when not even
+ * N_p = 0 does, and -2 on bad arguments (null pointers, max_len < 0, n_x < 0,
+ * or a_p or b_p negative: the model must grow with length).
+ * prefill_abc = {a, b, c}, predict_abc = {a_p, b_p, c_p}. */
+int64_t tb_predictor_length(const double* prefill_abc, const double* predict_abc,
+                            double n_x, int64_t max_len);
+
 #ifdef __cplusplus
 }
 #endif

@@ -14,6 +14,9 @@ What it computes (TimeBill, arXiv 2512.21859):
 * Retained length at decode step i: (1 - alpha) N_x + i - 1 (Eq. N_kv); the
   decode phase sums the steps i = 1 .. N_hat - 1 (Eqs. decoding-step,
   decoding-phase); WCET = prefill + decode phase at N_hat_W (Eq. wcet).
+* The predictor runs beside the prefill (Sec. 5.2): its input is compressed
+  to the longest N_p whose own time a_p N_p^2 + b_p N_p + c_p stays within the
+  prefill time a N_x^2 + b N_x + c.
 * alpha* = the smallest alpha in [0, alpha_max] with
   t_predict + WCET(alpha) <= T (Sec. 5.1, Eq. problem_converted), in closed
   form (Eq. alpha_with_predictor).
@@ -88,3 +91,15 @@ def fit_poly(n, t, degree: int):
     V = np.vander(n, degree + 1)
     coef, *_ = np.linalg.lstsq(V, t, rcond=None)
     return coef
+
+
+def predictor_length(prefill_abc, predict_abc, n_x: float, max_len: int) -> int:
+    """Largest integer N_p in [0, max_len] with t_predict(N_p) <= t_prefill(N_x),
+    by direct search over the integers; -1 when none fits."""
+    budget = t_prefill(prefill_abc, n_x)
+    a, b, c = predict_abc
+    best = -1
+    for n in range(max_len + 1):
+        if a * n * n + b * n + c <= budget:
+            best = n
+    return best

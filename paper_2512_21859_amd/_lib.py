@@ -23,7 +23,7 @@ V_TILE = 32          # the compact V cache is stored as transposed tiles of 32 r
 
 EXPORTED = ("tb_keep_count", "tb_last_error", "tb_workspace_bytes", "tb_score_window",
             "tb_score_window_avgpool", "tb_score_knorm", "tb_score_h2o", "tb_select_topk", "tb_compact_kv", "tb_decode_attn", "tb_ete_fit", "tb_wcet",
-            "tb_alpha_star")
+            "tb_alpha_star", "tb_predictor_length")
 
 _lib = None
 
@@ -74,6 +74,8 @@ def load() -> ctypes.CDLL:
     lib.tb_wcet.restype = dbl
     lib.tb_alpha_star.argtypes = [p_dbl, p_dbl, dbl, i32, dbl, dbl, dbl, p_i32]
     lib.tb_alpha_star.restype = dbl
+    lib.tb_predictor_length.argtypes = [p_dbl, p_dbl, dbl, ctypes.c_int64]
+    lib.tb_predictor_length.restype = ctypes.c_int64
     _lib = lib
     return lib
 
@@ -305,3 +307,14 @@ class KVCache:
         tb_decode_attn(q, k_new, v_new, self.k, self.v, self.kv_len, out, self.ws, stream)
         if k_new is not None:
             self.host_len = [n + 1 for n in self.host_len]
+
+
+def tb_predictor_length(prefill_abc: Sequence[float], predict_abc: Sequence[float], n_x: float,
+                        max_len: int) -> int:
+    """Largest predictor input length N_p <= max_len whose predicted time fits
+    within the predicted prefill time (-1: none fits)."""
+    r = load().tb_predictor_length(_dbl_array(prefill_abc), _dbl_array(predict_abc), float(n_x),
+                                   int(max_len))
+    if r == -2:
+        raise ValueError("tb_predictor_length: bad arguments")
+    return int(r)

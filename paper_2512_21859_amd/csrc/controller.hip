@@ -1,5 +1,6 @@
 // Time-budget controller (host code): least-squares fit of the execution-time
-// model, WCET and the closed-form eviction ratio alpha*.
+// model, WCET, the closed-form eviction ratio alpha*, and the longest
+// predictor input that finishes within the prefill phase.
 //
 // Model (TimeBill Sec. 4.2): prefill a N_x^2 + b N_x + c, decode step
 // p N_kv + q with N_kv = (1 - alpha) N_x + i - 1 at step i (Eq. N_kv); the
@@ -101,6 +102,29 @@ double tb_alpha_star(const double* prefill_abc, const double* step_pq, double n_
                      (n_hat_w - 2) / (2.0 * n_x) + q / (p * n_x);
   if (feasible) *feasible = raw <= alpha_max ? 1 : 0;
   return std::min(alpha_max, std::max(0.0, raw));
+}
+
+int64_t tb_predictor_length(const double* prefill_abc, const double* predict_abc, double n_x,
+                            int64_t max_len) {
+  if (!prefill_abc || !predict_abc || max_len < 0 || !(n_x >= 0)) return -2;
+  const double ap = predict_abc[0], bp = predict_abc[1], cp = predict_abc[2];
+  if (!(ap >= 0) || !(bp >= 0)) return -2;           // the model must grow with length
+  const double T = prefill(prefill_abc, n_x);
+  auto f = [&](double x) { return (ap * x + bp) * x + cp; };
+  if (!(cp <= T)) return -1;                         // not even an empty input fits
+  if (f(static_cast<double>(max_len)) <= T) return max_len;
+  // f is increasing on [0, inf): the answer is the floor of the positive root
+  double r;
+  if (ap > 0) {
+    const double disc = bp * bp + 4.0 * ap * (T - cp);
+    r = (2.0 * (T - cp)) / (bp + sqrt(disc));         // the same root, without cancellation
+  } else {
+    r = (T - cp) / bp;                               // bp > 0 here since f(max_len) > T >= cp
+  }
+  int64_t n = static_cast<int64_t>(std::min<double>(std::max(0.0, floor(r)), static_cast<double>(max_len)));
+  while (n + 1 <= max_len && f(static_cast<double>(n + 1)) <= T) ++n;   // settle rounding
+  while (n > 0 && f(static_cast<double>(n)) > T) --n;
+  return n;
 }
 
 }  // extern "C"

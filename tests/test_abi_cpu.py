@@ -23,7 +23,7 @@ def lib():
 
 def _declared():
     text = open(HEADER).read()
-    decl = r"^(?:int32_t|size_t|double|tb_status|const char\*)\s+(tb_[a-z0-9_]+)\("
+    decl = r"^(?:int32_t|int64_t|size_t|double|tb_status|const char\*)\s+(tb_[a-z0-9_]+)\("
     return sorted(set(re.findall(decl, text, re.M)))
 
 

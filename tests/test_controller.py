@@ -154,3 +154,29 @@ def test_choose_alpha_matches_reference():
             ref = C.alpha_star(e["prefill_abc"], e["step_pq"], e["n_x"], nw, budget, 0.1, 0.95)
             assert got[2] == nw == c["N_hat_W"]
             assert got[1] == ref[1] and abs(got[0] - ref[0]) < 1e-12
+
+
+def test_predictor_length_golden_and_abi():
+    """Hand-derived cases (tests/golden/controller_example.json) for the oracle's
+    integer search and for tb_predictor_length."""
+    ex = _ex()["predictor_length"]
+    for cs in ex["cases"]:
+        got_o = C.predictor_length(ex["prefill_abc"], cs["predict_abc"], ex["n_x"], cs["max_len"])
+        got_c = _lib.tb_predictor_length(ex["prefill_abc"], cs["predict_abc"], ex["n_x"],
+                                         cs["max_len"])
+        assert got_o == cs["n_p"], cs
+        assert got_c == cs["n_p"], cs
+
+
+def test_predictor_length_random_against_search():
+    rng = np.random.default_rng(17)
+    for _ in range(300):
+        pre = [rng.uniform(0, 2e-6), rng.uniform(0, 1e-3), rng.uniform(0, 0.05)]
+        pred = [rng.choice([0.0, rng.uniform(0, 4e-6)]), rng.uniform(0, 2e-3),
+                rng.uniform(0, 0.2)]
+        n_x = float(rng.integers(1, 3000))
+        max_len = int(rng.integers(0, 3000))
+        assert (_lib.tb_predictor_length(pre, pred, n_x, max_len)
+                == C.predictor_length(pre, pred, n_x, max_len))
+    with pytest.raises(ValueError):
+        _lib.tb_predictor_length([1, 0, 0], [0, -1.0, 0], 10.0, 10)
