@@ -58,6 +58,8 @@ __all__ = [
     "select_keep",
     "compact",
     "decode_step",
+    "prefill_attention",
+    "prefill_window_stats",
     "decode_partial",
     "merge_partials",
     "evict_sequence",
@@ -251,4 +253,41 @@ def decode_sequence(q_steps, k_new, v_new, k_cache, v_cache, steps=None):
             vv = np.concatenate([vc[g], vn[: t + 1, g]], axis=0)
             o[g * G:(g + 1) * G] = decode_step(q_steps[t, g * G:(g + 1) * G], kk, vv)
         out[t] = o
+    return out
+
+
+def prefill_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, n_x: int,
+                      rows=None) -> np.ndarray:
+    """Causal attention of the prompt (Sec. 4.2's attention with a causal mask):
+    q [Hq, >= n_x, d], k/v [Hkv, >= n_x, d] -> [Hq, len(rows), d] for the query
+    rows `rows` (default: all n_x), row i attending over keys 0..i."""
+    hq, hkv = q.shape[0], k.shape[0]
+    G = hq // hkv
+    d = q.shape[-1]
+    rows = np.arange(n_x) if rows is None else np.asarray(rows)
+    out = np.empty((hq, len(rows), d), dtype=np.float64)
+    for h in range(hq):
+        g = h // G
+        kk = np.asarray(k[g, :n_x], dtype=np.float64)
+        vv = np.asarray(v[g, :n_x], dtype=np.float64)
+        for r, i in enumerate(rows):
+            out[h, r] = decode_step(np.asarray(q[h:h + 1, i], dtype=np.float64),
+                                    kk[: i + 1], vv[: i + 1])[0]
+    return out
+
+
+def prefill_window_stats(q: np.ndarray, k: np.ndarray, n_x: int, w: int) -> np.ndarray:
+    """For the last w query rows i = n_x - w + r: (M, Z) with M the row's largest
+    logit q.k/sqrt(d) over keys 0..i and Z = sum_j exp(s_j - M).  [Hq, w, 2]."""
+    hq, hkv = q.shape[0], k.shape[0]
+    G = hq // hkv
+    d = q.shape[-1]
+    out = np.empty((hq, w, 2), dtype=np.float64)
+    for h in range(hq):
+        kk = np.asarray(k[h // G, :n_x], dtype=np.float64)
+        for r in range(w):
+            i = n_x - w + r
+            s = kk[: i + 1] @ np.asarray(q[h, i], dtype=np.float64) / math.sqrt(d)
+            m = s.max()
+            out[h, r] = (m, np.exp(s - m).sum())
     return out

@@ -287,3 +287,30 @@ def test_fraction_sanity_of_hand_example():
     h = _hand()
     total = sum(Fraction(n, d) for n, d in h["column_mass"])
     assert total == 4
+
+
+def test_prefill_attention_matches_torch_sdpa():
+    """Causal prefill attention and the window statistics against torch's float64
+    scaled_dot_product_attention (KV heads repeated by G) and logsumexp."""
+    rng = np.random.default_rng(41)
+    hq, hkv, n, d, w = 6, 2, 77, 32, 5
+    q = rng.standard_normal((hq, n, d))
+    k = rng.standard_normal((hkv, n, d)) * 1.3
+    v = rng.standard_normal((hkv, n, d))
+    got = O.prefill_attention(q, k, v, n)
+    qt = torch.from_numpy(q)[None]
+    kt = torch.from_numpy(k).repeat_interleave(hq // hkv, dim=0)[None]
+    vt = torch.from_numpy(v).repeat_interleave(hq // hkv, dim=0)[None]
+    ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, is_causal=True)[0]
+    np.testing.assert_allclose(got, ref.numpy(), rtol=1e-12, atol=1e-12)
+    rows = [0, 1, 40, n - 1]
+    np.testing.assert_allclose(O.prefill_attention(q, k, v, n, rows), got[:, rows], rtol=0, atol=0)
+    st = O.prefill_window_stats(q, k, n, w)
+    logits = (qt[0] @ kt[0].transpose(1, 2)) / math.sqrt(d)
+    mask = torch.ones(n, n, dtype=torch.bool).tril()
+    logits = logits.masked_fill(~mask, float("-inf"))[:, n - w:]
+    lse = torch.logsumexp(logits, dim=-1).numpy()
+    np.testing.assert_allclose(st[..., 0], logits.max(dim=-1).values.numpy(), rtol=0, atol=1e-13)
+    np.testing.assert_allclose(st[..., 0] + np.log(st[..., 1]), lse, rtol=1e-13)
+    # row 0 attends to key 0 only: its output is v[0]
+    np.testing.assert_allclose(got[:, 0], np.repeat(v[:, 0], hq // hkv, axis=0), rtol=0, atol=0)
