@@ -50,9 +50,11 @@ def _parse():
                     help="skip the supplementary 28-layer L=32768 ratio sweep")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the 2 GiB read / copy bandwidth ceilings")
+    ap.add_argument("--no-prefill", action="store_true",
+                    help="skip the prefill-attention sweep")
     ap.add_argument("--no-scorers", action="store_true",
                     help="skip the scorer-variant timings")
-    ap.add_argument("--only", choices=("cold", "long", "layers", "ceiling", "scorers"),
+    ap.add_argument("--only", choices=("cold", "long", "layers", "ceiling", "scorers", "prefill"),
                     help="run one supplementary measurement alone and print its JSON "
                          "(for profiling that workload by itself)")
     ap.add_argument("--pmc-calibration", action="store_true",
@@ -317,6 +319,49 @@ def scorer_variants(torch, _lib, synth, Evictor, dev, reps=10):
     return out
 
 
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def prefill_sweep(torch, _lib, synth, dev, lengths=(1024, 2048, 4096, 8192, 16384, 32768)):
+    """Supplementary: causal prefill attention (28 q / 4 kv heads, d = 128, bf16)
+    at prompt lengths N, the time fitted with the paper's prefill-phase form
+    a N^2 + b N + c (tb_ete_fit, degree 2) and the bf16 matrix-core rate
+    (causal flops 4 Hq d N(N+1)/2)."""
+    Lmax = max(lengths)
+    wl = synth.custom(2000, torch.bfloat16, 1, [Lmax], 28, 4, 128, 32, 7, 1)
+    pr = synth.make_prompt(wl, L=[Lmax])
+    q = synth.make_queries(wl, L=[Lmax]).to(dev)
+    k, v = pr["k"].to(dev), pr["v"].to(dev)
+    del pr
+    out = torch.empty_like(q)
+    Hq, d = wl.Hq, wl.d
+    rows = []
+    for n in lengths:
+        reps = max(2, min(20, (1 << 25) // (n * n // 64)))
+        cs = torch.cuda.Stream()
+        _lib.tb_prefill_attn(q, k, v, [n], out, stream=cs)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cs):
+            for _ in range(reps):
+                _lib.tb_prefill_attn(q, k, v, [n], out, stream=cs)
+        torch.cuda.synchronize()
+        us = _best_ms(torch, g.replay) * 1e3 / reps
+        flops = 4 * Hq * d * (n * (n + 1) // 2)
+        rows.append({"n": n, "us": round(us, 2), "TFLOPs": round(flops / (us * 1e-6) / 1e12, 1),
+                     "frac_of_bf16_peak": round(flops / (us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4)})
+        del g
+    a, b_, c = _lib.tb_ete_fit([r["n"] for r in rows], [r["us"] for r in rows], 2)
+    pred = [a * r["n"] ** 2 + b_ * r["n"] + c for r in rows]
+    mape = 100.0 * sum(abs(f - r["us"]) / r["us"] for f, r in zip(pred, rows)) / len(rows)
+    del q, k, v, out
+    torch.cuda.empty_cache()
+    return {"workload": "causal prefill attention, bf16, B=1, 28 q / 4 kv heads, d=128",
+            "per_length": rows,
+            "prefill_time_fit": {"a_us_per_n2": a, "b_us_per_n": b_, "c_us": c, "mape_pct": mape},
+            "timing": "best of 3 replays of a graph of repeated calls (2..20 by length)"}
+
+
 def layer_sweep(torch, _lib, synth, Evictor, dev, T=None):
     """Supplementary: the 28-layer model shape at L = 32768 (28 q / 4 kv heads,
     d = 128, w = 32, pool 7) over the ratios k/20, k = 0..19.  Per ratio: evict
@@ -435,11 +480,12 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    if args.only in ("long", "layers", "ceiling", "scorers"):
+    if args.only in ("long", "layers", "ceiling", "scorers", "prefill"):
         fn = {"long": lambda: long_context(torch, _lib, synth, Evictor, dev),
               "layers": lambda: layer_sweep(torch, _lib, synth, Evictor, dev),
               "ceiling": lambda: hbm_ceiling(torch, dev),
-              "scorers": lambda: scorer_variants(torch, _lib, synth, Evictor, dev)}[args.only]
+              "scorers": lambda: scorer_variants(torch, _lib, synth, Evictor, dev),
+              "prefill": lambda: prefill_sweep(torch, _lib, synth, dev)}[args.only]
         print(json.dumps({"section": args.only, **fn()}), flush=True)
         return
     wl = synth.WORKLOADS[2]
@@ -597,6 +643,8 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_long_context:
         result["long_context"] = long_context(torch, _lib, synth, Evictor, dev)
+    if not args.no_prefill:
+        result["prefill"] = prefill_sweep(torch, _lib, synth, dev)
     if not args.no_scorers:
         result["scorers"] = scorer_variants(torch, _lib, synth, Evictor, dev)
     if not args.no_layer_sweep:

@@ -200,6 +200,25 @@ tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new,
                          int32_t cap, tb_dtype dt, void* out, void* ws,
                          size_t ws_bytes, hipStream_t stream);
 
+/* Causal grouped-query prefill attention, the step before eviction (the
+ * prefill phase of Sec. 4.2, whose time the paper models as
+ * a N_x^2 + b N_x + c, Eq. prefill_phase_time_raw):
+ *   out[b][h][i] = sum_{j <= i} softmax_j(q[b][h][i] . k[j] / sqrt(d)) v[j]
+ * over the rows of KV head h / (Hq/Hkv), for i < L[b].
+ *   q, out: [B][Hq][Lmax][d];  k, v: [B][Hkv][Lmax][d]  (rows >= L[b] unread
+ *   / unwritten).
+ * bf16 only, on the matrix cores; softmax statistics in fp32, P rounded to
+ * bf16 for the PV product.  window_stats (nullable, [B][Hq][w][2] fp32)
+ * receives, for the last w rows i = L[b]-w+r, the row's logit maximum M (in
+ * the units of q.k/sqrt(d)) and Z = sum_j exp(s_j - M): the observation
+ * window's softmax statistics as a by-product (the eviction scorer keeps its
+ * own float64 statistics; these are fp32).  Requires 1 <= L[b] <= Lmax and,
+ * with window_stats, 1 <= w <= L[b].  No workspace. */
+tb_status tb_prefill_attn(const void* q, const void* k, const void* v, int32_t B,
+                          const int32_t* L, int32_t Lmax, int32_t Hq, int32_t Hkv,
+                          int32_t d, tb_dtype dt, void* out, int32_t w,
+                          float* window_stats, hipStream_t stream);
+
 /* ---- time-budget controller (host) ------------------------------------ */
 
 /* [host] Least-squares fit of the execution-time model from profiled pairs

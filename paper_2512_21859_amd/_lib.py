@@ -22,7 +22,8 @@ TB_OP_SCORE, TB_OP_SELECT, TB_OP_COMPACT, TB_OP_DECODE, TB_OP_H2O = range(5)
 V_TILE = 32          # the compact V cache is stored as transposed tiles of 32 rows
 
 EXPORTED = ("tb_keep_count", "tb_last_error", "tb_workspace_bytes", "tb_score_window",
-            "tb_score_window_avgpool", "tb_score_knorm", "tb_score_h2o", "tb_select_topk", "tb_compact_kv", "tb_decode_attn", "tb_ete_fit", "tb_wcet",
+            "tb_score_window_avgpool", "tb_score_knorm", "tb_score_h2o", "tb_prefill_attn",
+            "tb_select_topk", "tb_compact_kv", "tb_decode_attn", "tb_ete_fit", "tb_wcet",
             "tb_alpha_star", "tb_predictor_length")
 
 _lib = None
@@ -60,6 +61,9 @@ def load() -> ctypes.CDLL:
     lib.tb_score_knorm.restype = i32
     lib.tb_score_h2o.argtypes = [vp, vp, i32, p_i32, i32, i32, i32, i32, i32, vp, vp, sz, vp]
     lib.tb_score_h2o.restype = i32
+    lib.tb_prefill_attn.argtypes = [vp, vp, vp, i32, p_i32, i32, i32, i32, i32, i32, vp, i32, vp,
+                                    vp]
+    lib.tb_prefill_attn.restype = i32
     lib.tb_select_topk.argtypes = [vp, i32, p_i32, i32, i32, i32, p_dbl, vp, p_i32, vp, sz, vp]
     lib.tb_select_topk.restype = i32
     lib.tb_compact_kv.argtypes = [vp, vp, vp, i32, p_i32, i32, i32, i32, i32, i32, vp, vp, vp,
@@ -169,6 +173,25 @@ def tb_score_h2o(q: torch.Tensor, k: torch.Tensor, L: Sequence[int], scores: tor
     _check(load().tb_score_h2o(_dev(q, "q"), _dev(k, "k"), B, _i32_array(L), Lmax, Hq, Hkv, d,
                                _dtype_code(k), _dev(scores, "scores", torch.float32),
                                _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def tb_prefill_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, L: Sequence[int],
+                    out: torch.Tensor, w: int = 0, window_stats: Optional[torch.Tensor] = None,
+                    stream=None) -> None:
+    """Causal GQA prefill attention: q [B,Hq,Lmax,d], k/v [B,Hkv,Lmax,d] (bf16) ->
+    out [B,Hq,Lmax,d]; window_stats [B,Hq,w,2] fp32 gets (M, Z) of the last w rows."""
+    B, Hq, Lmax, d = q.shape
+    _, Hkv, Lmax2, d2 = k.shape
+    if tuple(v.shape) != tuple(k.shape) or Lmax2 != Lmax or d2 != d or k.shape[0] != B:
+        raise ValueError("q / k / v shapes disagree")
+    if tuple(out.shape) != tuple(q.shape):
+        raise ValueError("out must match q")
+    if window_stats is not None and tuple(window_stats.shape) != (B, Hq, w, 2):
+        raise ValueError("window_stats must be [B, Hq, w, 2]")
+    _check(load().tb_prefill_attn(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), B, _i32_array(L),
+                                  Lmax, Hq, Hkv, d, _dtype_code(q), _dev(out, "out"), w,
+                                  _dev(window_stats, "window_stats", torch.float32),
+                                  _stream(stream)))
 
 
 def tb_select_topk(scores: torch.Tensor, L: Sequence[int], w: int, alpha: Sequence[float],

@@ -252,6 +252,33 @@ tb_status tb_score_h2o(const void* q, const void* k, int32_t B, const int32_t* L
   }
 }
 
+tb_status tb_prefill_attn(const void* q, const void* k, const void* v, int32_t B,
+                          const int32_t* L, int32_t Lmax, int32_t Hq, int32_t Hkv, int32_t d,
+                          tb_dtype dt, void* out, int32_t w, float* window_stats,
+                          hipStream_t stream) {
+  try {
+    if (!q || !k || !v || !L || !out) return fail(TB_EINVAL, "tb_prefill_attn: null pointer");
+    tb_status st = check_common(B, Hq, Hkv, d, dt);
+    if (st != TB_OK) return st;
+    if (dt != TB_BF16) return fail(TB_EUNSUPPORTED, "tb_prefill_attn: bf16 only");
+    if (window_stats && w < 1) return fail(TB_EINVAL, "w must be >= 1 when window_stats is given");
+    tb::PrefillArgs a{};
+    for (int b = 0; b < B; ++b) {
+      if (!(L[b] >= 1 && L[b] <= Lmax))
+        return fail(TB_EINVAL, "need 1 <= L[%d] <= Lmax (L=%d, Lmax=%d)", b, L[b], Lmax);
+      if (window_stats && w > L[b])
+        return fail(TB_EINVAL, "need w <= L[%d] (w=%d, L=%d)", b, w, L[b]);
+      a.L[b] = L[b];
+    }
+    a.q = q; a.k = k; a.v = v; a.out = out; a.window_stats = window_stats;
+    a.B = B; a.Lmax = Lmax; a.Hq = Hq; a.Hkv = Hkv; a.w = window_stats ? w : 0;
+    a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(d)));
+    return hip_status(tb::launch_prefill(a, d, stream), "tb_prefill_attn launch");
+  } catch (...) {
+    return fail(TB_EINTERNAL, "tb_prefill_attn: internal error");
+  }
+}
+
 tb_status tb_score_knorm(const void* k, int32_t B, const int32_t* L, int32_t Lmax, int32_t Hkv,
                          int32_t d, int32_t w, tb_dtype dt, float* scores, hipStream_t stream) {
   try {

@@ -56,6 +56,19 @@ struct H2oArgs {
 size_t h2o_ws_bytes(int B, int Lmax, int Hq);
 hipError_t launch_h2o(const H2oArgs& a, int d, bool bf16, hipStream_t st);
 
+// ---------------------------------------------------------------- prefill
+struct PrefillArgs {
+  const void* q;          // [B][Hq][Lmax][d] bf16
+  const void* k;          // [B][Hkv][Lmax][d]
+  const void* v;          // [B][Hkv][Lmax][d]
+  void* out;              // [B][Hq][Lmax][d]
+  float* window_stats;    // nullable [B][Hq][w][2]: (row max, normaliser) of the last w rows
+  int32_t B, Lmax, Hq, Hkv, w;
+  float scale_log2;       // log2(e)/sqrt(d)
+  int32_t L[kMaxB];
+};
+hipError_t launch_prefill(const PrefillArgs& a, int d, hipStream_t st);
+
 // ---------------------------------------------------------------- selection
 struct SelectArgs {
   const float* scores;    // [B][Hkv][Lmax]
