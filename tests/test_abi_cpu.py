@@ -146,6 +146,27 @@ def test_score_h2o_validation(lib):
     assert call(ws=None) == E.TB_EWORKSPACE
 
 
+def test_prefill_validation(lib):
+    E = _lib
+
+    def call(q=FAKE, B=1, L=100, Lmax=100, Hq=4, Hkv=2, d=128, dt=_lib.TB_BF16, out=FAKE,
+             w=8, ws=FAKE):
+        return lib.tb_prefill_attn(q, FAKE, FAKE, B, _i32(L), Lmax, Hq, Hkv, d, dt, out, w, ws,
+                                   None)
+
+    assert call(q=None) == E.TB_EINVAL
+    assert call(out=None) == E.TB_EINVAL
+    assert call(dt=_lib.TB_F32) == E.TB_EUNSUPPORTED
+    assert b"bf16 only" in lib.tb_last_error()
+    assert call(Hq=5) == E.TB_EINVAL
+    assert call(d=96) == E.TB_EUNSUPPORTED
+    assert call(L=0) == E.TB_EINVAL
+    assert call(L=101) == E.TB_EINVAL
+    assert call(w=0) == E.TB_EINVAL                     # window statistics need w >= 1
+    assert call(w=101, L=100) == E.TB_EINVAL            # and w <= L
+    assert call(w=0, ws=None, B=0) == E.TB_EINVAL
+
+
 def test_select_validation(lib):
     E = _lib
     n_keep = (ctypes.c_int32 * 1)()
