@@ -33,17 +33,17 @@ typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 constexpr int kWaves = 4;
-constexpr int kRowsPerWave = 32;              // two 16-query column tiles
-constexpr int kBlockRows = kWaves * kRowsPerWave;   // 128
 constexpr int kStage = 64;                    // keys per LDS stage
 constexpr int kKPad = 8;                      // bf16 padding of a K row in LDS
 constexpr int kVPad = 8;                      // bf16 padding of a V^T row in LDS
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-template <int D>
-__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2)))
+template <int D, int CQ>
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(CQ == 2 ? 2 : 1)))
 void prefill_attn_kernel(PrefillArgs a) {
+  constexpr int kRowsPerWave = 16 * CQ;       // CQ 16-query column tiles per wave
+  constexpr int kBlockRows = kWaves * kRowsPerWave;
   constexpr int KC = D / 32;                  // k-chunks of the QK^T product
   constexpr int NC = D / 16;                  // d-blocks of the PV product
   const int h = blockIdx.y, b = blockIdx.z;
@@ -66,22 +66,24 @@ void prefill_attn_kernel(PrefillArgs a) {
 
   const int row0 = qt * kBlockRows + wave * kRowsPerWave;     // this wave's first query
   // Q^T operands: column tile cq, lane holds query row0 + 16 cq + r16, d = 32 kc + 8 q4 .. +8
-  u32x4 qB[2][KC];
+  u32x4 qB[CQ][KC];
 #pragma unroll
-  for (int cq = 0; cq < 2; ++cq) {
+  for (int cq = 0; cq < CQ; ++cq) {
     const int qi = min(row0 + 16 * cq + r16, L - 1);            // rows past L: any valid row
     const uint16_t* src = qh + static_cast<size_t>(qi) * D;
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) qB[cq][kc] = *reinterpret_cast<const u32x4*>(src + 32 * kc + 8 * q4);
   }
 
-  f32x4 accO[2][NC];
+  f32x4 accO[CQ][NC];
+  float m_run[CQ], l_part[CQ];                // running max (base-2 domain) / lane's share of the sum
 #pragma unroll
-  for (int cq = 0; cq < 2; ++cq)
+  for (int cq = 0; cq < CQ; ++cq) {
 #pragma unroll
     for (int n = 0; n < NC; ++n) accO[cq][n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[2] = {-INFINITY, -INFINITY};    // running max of query r16 (base-2 domain)
-  float l_part[2] = {0.f, 0.f};               // this lane's share of the running sum
+    m_run[cq] = -INFINITY;
+    l_part[cq] = 0.f;
+  }
   const int krow0 = 8 * (r16 >> 2) + (r16 & 3);                // permuted K row of MFMA row r16
 
   const int key_end = min(L, (qt + 1) * kBlockRows);            // causal limit of the block
@@ -159,7 +161,7 @@ void prefill_attn_kernel(PrefillArgs a) {
         vA[n] = *reinterpret_cast<const u32x4*>(&s_vt[16 * n + r16][32 * sub + 8 * q4]);
       const bool need_mask = base + 32 > row0;                  // step reaches this wave's diagonal
 #pragma unroll
-      for (int cq = 0; cq < 2; ++cq) {
+      for (int cq = 0; cq < CQ; ++cq) {
         f32x4 S[2];
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
@@ -211,7 +213,7 @@ void prefill_attn_kernel(PrefillArgs a) {
   // finalize: lane holds d = 16 n + 4 q4 .. +3 of query row0 + 16 cq + r16
   uint16_t* outh = static_cast<uint16_t*>(a.out) + (static_cast<size_t>(b) * a.Hq + h) * a.Lmax * D;
 #pragma unroll
-  for (int cq = 0; cq < 2; ++cq) {
+  for (int cq = 0; cq < CQ; ++cq) {
     float l_tot = l_part[cq] + __shfl_xor(l_part[cq], 16);
     l_tot += __shfl_xor(l_tot, 32);
     const int qi = row0 + 16 * cq + r16;
@@ -237,11 +239,16 @@ void prefill_attn_kernel(PrefillArgs a) {
 }  // namespace
 
 hipError_t launch_prefill(const PrefillArgs& a, int d, hipStream_t st) {
+  // two column tiles per wave (244 VGPRs, two waves per SIMD); four tiles
+  // halve the LDS operand reads per product but need one wave per SIMD, and
+  // measured slower (310 vs 584 TFLOP/s at N = 32768)
+  constexpr int CQ = 2;
+  constexpr int rows = kWaves * 16 * CQ;
   int lmax = 0;
   for (int b = 0; b < a.B; ++b) lmax = max(lmax, a.L[b]);
-  const dim3 grid((lmax + kBlockRows - 1) / kBlockRows, a.Hq, a.B);
-  if (d == 128) prefill_attn_kernel<128><<<grid, 64 * kWaves, 0, st>>>(a);
-  else          prefill_attn_kernel<64><<<grid, 64 * kWaves, 0, st>>>(a);
+  const dim3 grid((lmax + rows - 1) / rows, a.Hq, a.B);
+  if (d == 128) prefill_attn_kernel<128, CQ><<<grid, 64 * kWaves, 0, st>>>(a);
+  else          prefill_attn_kernel<64, CQ><<<grid, 64 * kWaves, 0, st>>>(a);
   return hipGetLastError();
 }
 
