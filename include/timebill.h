@@ -92,7 +92,9 @@ const char* tb_last_error(void);
 
 /* [host] Workspace bytes the operation `op` needs for these sizes (0 if none).
  * `cap` is used by TB_OP_DECODE only; arguments an op does not use are
- * ignored.  Returns 0 and sets the error for invalid sizes. */
+ * ignored.  Returns 0 and sets the error for invalid sizes.  The decode need
+ * is not monotone in B (a small batch is split into more chunks): a caller
+ * whose batch size varies sizes for the largest need over those sizes. */
 size_t tb_workspace_bytes(int32_t op, int32_t B, int32_t Lmax, int32_t Hq,
                           int32_t Hkv, int32_t d, int32_t w, int32_t cap);
 
@@ -199,6 +201,31 @@ tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new,
                          int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
                          int32_t cap, tb_dtype dt, void* out, void* ws,
                          size_t ws_bytes, hipStream_t stream);
+
+/* ---- paged caches (serving) --------------------------------------------
+ * The same compaction and decode over caches kept in pages of 32 rows, one
+ * page holding a sequence's 32-row tile for every KV head:
+ *   k_pool [n_pages][Hkv][32][d]   K rows, row-major
+ *   v_pool [n_pages][Hkv][d][32]   the tile's V^T
+ *   block_table [B][max_pages]     int32 (device): row t/32 of sequence b is
+ *                                  in page block_table[b][t / 32]
+ * A sequence holds up to max_pages * 32 rows.  The pages a sequence writes
+ * (compaction: tiles below n_keep[b]; decode: the tile of row kv_len[b]) must
+ * be its own; entries past its length may hold any value (out-of-range
+ * entries are clamped into the pool before any read, so they never fault).
+ * Results equal the contiguous calls with cap = max_pages * 32. */
+tb_status tb_compact_kv_paged(const void* k, const void* v, const int32_t* keep_idx,
+                              int32_t B, const int32_t* n_keep, int32_t Lmax, int32_t Hkv,
+                              int32_t d, tb_dtype dt, void* k_pool, void* v_pool,
+                              int32_t n_pages, const int32_t* block_table, int32_t max_pages,
+                              int32_t* kv_len, hipStream_t stream);
+/* ws: tb_workspace_bytes(TB_OP_DECODE, B, 0, Hq, Hkv, d, 0, max_pages * 32). */
+tb_status tb_decode_attn_paged(const void* q, const void* k_new, const void* v_new,
+                               void* k_pool, void* v_pool, int32_t n_pages,
+                               const int32_t* block_table, int32_t max_pages,
+                               int32_t* kv_len, int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
+                               tb_dtype dt, void* out, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
 
 /* Causal grouped-query prefill attention, the step before eviction (the
  * prefill phase of Sec. 4.2, whose time the paper models as

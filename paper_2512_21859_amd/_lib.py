@@ -23,7 +23,7 @@ V_TILE = 32          # the compact V cache is stored as transposed tiles of 32 r
 
 EXPORTED = ("tb_keep_count", "tb_last_error", "tb_workspace_bytes", "tb_score_window",
             "tb_score_window_avgpool", "tb_score_knorm", "tb_score_h2o", "tb_prefill_attn",
-            "tb_select_topk", "tb_compact_kv", "tb_decode_attn", "tb_ete_fit", "tb_wcet",
+            "tb_select_topk", "tb_compact_kv_paged", "tb_decode_attn_paged", "tb_compact_kv", "tb_decode_attn", "tb_ete_fit", "tb_wcet",
             "tb_alpha_star", "tb_predictor_length")
 
 _lib = None
@@ -64,6 +64,12 @@ def load() -> ctypes.CDLL:
     lib.tb_prefill_attn.argtypes = [vp, vp, vp, i32, p_i32, i32, i32, i32, i32, i32, vp, i32, vp,
                                     vp]
     lib.tb_prefill_attn.restype = i32
+    lib.tb_compact_kv_paged.argtypes = [vp, vp, vp, i32, p_i32, i32, i32, i32, i32, vp, vp, i32,
+                                        vp, i32, vp, vp]
+    lib.tb_compact_kv_paged.restype = i32
+    lib.tb_decode_attn_paged.argtypes = [vp, vp, vp, vp, vp, i32, vp, i32, vp, i32, i32, i32, i32,
+                                         i32, vp, vp, sz, vp]
+    lib.tb_decode_attn_paged.restype = i32
     lib.tb_select_topk.argtypes = [vp, i32, p_i32, i32, i32, i32, p_dbl, vp, p_i32, vp, sz, vp]
     lib.tb_select_topk.restype = i32
     lib.tb_compact_kv.argtypes = [vp, vp, vp, i32, p_i32, i32, i32, i32, i32, i32, vp, vp, vp,
@@ -341,3 +347,55 @@ def tb_predictor_length(prefill_abc: Sequence[float], predict_abc: Sequence[floa
     if r == -2:
         raise ValueError("tb_predictor_length: bad arguments")
     return int(r)
+
+
+
+def _check_pools(k_pool, v_pool, block_table, dtype):
+    n_pages, Hkv, t, d = k_pool.shape
+    if t != V_TILE or tuple(v_pool.shape) != (n_pages, Hkv, d, V_TILE):
+        raise ValueError("pools must be k_pool [P, Hkv, 32, d] and v_pool [P, Hkv, d, 32]")
+    if k_pool.dtype != dtype or v_pool.dtype != dtype:
+        raise TypeError("pools must share the inputs' dtype")
+    if block_table.dim() != 2:
+        raise ValueError("block_table must be [B, max_pages]")
+    return n_pages, Hkv, d, block_table.shape[1]
+
+
+def tb_compact_kv_paged(k: torch.Tensor, v: torch.Tensor, keep_idx: torch.Tensor,
+                        n_keep: Sequence[int], k_pool: torch.Tensor, v_pool: torch.Tensor,
+                        block_table: torch.Tensor, kv_len: torch.Tensor, stream=None) -> None:
+    """k, v [B,Hkv,Lmax,d] -> the pages block_table [B, max_pages] names in
+    k_pool [P,Hkv,32,d] / v_pool [P,Hkv,d,32]; kv_len [B] int32 set to n_keep."""
+    B, Hkv, Lmax, d = k.shape
+    if v.shape != k.shape or v.dtype != k.dtype:
+        raise ValueError("k and v disagree")
+    n_pages, ph, pd, max_pages = _check_pools(k_pool, v_pool, block_table, k.dtype)
+    if (ph, pd) != (Hkv, d) or block_table.shape[0] != B:
+        raise ValueError("pool or block table shape does not match k")
+    _check(load().tb_compact_kv_paged(
+        _dev(k, "k"), _dev(v, "v"), _dev(keep_idx, "keep_idx", torch.int32), B,
+        _i32_array(n_keep), Lmax, Hkv, d, _dtype_code(k), _dev(k_pool, "k_pool"),
+        _dev(v_pool, "v_pool"), n_pages, _dev(block_table, "block_table", torch.int32),
+        max_pages, _dev(kv_len, "kv_len", torch.int32), _stream(stream)))
+
+
+def tb_decode_attn_paged(q: torch.Tensor, k_new: Optional[torch.Tensor],
+                         v_new: Optional[torch.Tensor], k_pool: torch.Tensor,
+                         v_pool: torch.Tensor, block_table: torch.Tensor, kv_len: torch.Tensor,
+                         out: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
+    """q, out [B,Hq,d]; k_new, v_new [B,Hkv,d] or None; pools and table as in
+    tb_compact_kv_paged (only the first B table rows and lengths are used)."""
+    B, Hq, d = q.shape
+    n_pages, Hkv, pd, max_pages = _check_pools(k_pool, v_pool, block_table, q.dtype)
+    if pd != d or block_table.shape[0] < B or kv_len.numel() < B:
+        raise ValueError("pool, block table or kv_len does not match q")
+    if out.shape != q.shape or out.dtype != q.dtype:
+        raise ValueError("out must match q")
+    for t, name in ((k_new, "k_new"), (v_new, "v_new")):
+        if t is not None and (tuple(t.shape) != (B, Hkv, d) or t.dtype != q.dtype):
+            raise ValueError(f"{name} must be [B, Hkv, d] of q's dtype")
+    _check(load().tb_decode_attn_paged(
+        _dev(q, "q"), _dev(k_new, "k_new"), _dev(v_new, "v_new"), _dev(k_pool, "k_pool"),
+        _dev(v_pool, "v_pool"), n_pages, _dev(block_table, "block_table", torch.int32),
+        max_pages, _dev(kv_len, "kv_len", torch.int32), B, Hq, Hkv, d, _dtype_code(q),
+        _dev(out, "out"), _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))

@@ -328,14 +328,22 @@ tb_status tb_select_topk(const float* scores, int32_t B, const int32_t* L, int32
   }
 }
 
-tb_status tb_compact_kv(const void* k, const void* v, const int32_t* keep_idx, int32_t B,
-                        const int32_t* n_keep, int32_t Lmax, int32_t Hkv, int32_t d,
-                        tb_dtype dt, int32_t cap, void* k_cache, void* v_cache,
-                        int32_t* kv_len, void* ws, size_t ws_bytes, hipStream_t stream) {
-  (void)ws; (void)ws_bytes;
+namespace {
+
+// Paged caches: table [B][max_pages] of page indices into pools of n_pages
+// pages; a sequence holds up to max_pages * 32 rows.
+struct Paging {
+  const int32_t* table;
+  int32_t max_pages, n_pages;
+};
+
+tb_status compact_impl(const char* name, const void* k, const void* v, const int32_t* keep_idx,
+                       int32_t B, const int32_t* n_keep, int32_t Lmax, int32_t Hkv, int32_t d,
+                       tb_dtype dt, int32_t cap, const Paging* pg, void* k_cache, void* v_cache,
+                       int32_t* kv_len, hipStream_t stream) {
   try {
     if (!k || !v || !keep_idx || !n_keep || !k_cache || !v_cache || !kv_len)
-      return fail(TB_EINVAL, "tb_compact_kv: null pointer");
+      return fail(TB_EINVAL, "%s: null pointer", name);
     tb_status st = check_common(B, Hkv, Hkv, d, dt);
     if (st != TB_OK) return st;
     if (Lmax < 1 || cap < 1) return fail(TB_EINVAL, "Lmax and cap must be >= 1");
@@ -352,22 +360,22 @@ tb_status tb_compact_kv(const void* k, const void* v, const int32_t* keep_idx, i
     }
     a.k = k; a.v = v; a.keep_idx = keep_idx; a.k_cache = k_cache; a.v_cache = v_cache;
     a.kv_len = kv_len; a.B = B; a.Lmax = Lmax; a.Hkv = Hkv; a.cap = cap;
-    return hip_status(tb::launch_compact(a, d, elem_bytes(dt), max_keep, stream),
-                      "tb_compact_kv launch");
+    if (pg) { a.table = pg->table; a.max_pages = pg->max_pages; a.n_pages = pg->n_pages; }
+    return hip_status(tb::launch_compact(a, d, elem_bytes(dt), max_keep, stream), name);
   } catch (...) {
-    return fail(TB_EINTERNAL, "tb_compact_kv: internal error");
+    return fail(TB_EINTERNAL, "%s: internal error", name);
   }
 }
 
-tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new, void* k_cache,
-                         void* v_cache, int32_t* kv_len, int32_t B, int32_t Hq, int32_t Hkv,
-                         int32_t d, int32_t cap, tb_dtype dt, void* out, void* ws,
-                         size_t ws_bytes, hipStream_t stream) {
+tb_status decode_impl(const char* name, const void* q, const void* k_new, const void* v_new,
+                      void* k_cache, void* v_cache, int32_t* kv_len, int32_t B, int32_t Hq,
+                      int32_t Hkv, int32_t d, int32_t cap, const Paging* pg, tb_dtype dt,
+                      void* out, void* ws, size_t ws_bytes, hipStream_t stream) {
   try {
     if (!q || !k_cache || !v_cache || !kv_len || !out || !ws)
-      return fail(TB_EINVAL, "tb_decode_attn: null pointer");
+      return fail(TB_EINVAL, "%s: null pointer", name);
     if ((k_new == nullptr) != (v_new == nullptr))
-      return fail(TB_EINVAL, "tb_decode_attn: k_new and v_new must both be given or both NULL");
+      return fail(TB_EINVAL, "%s: k_new and v_new must both be given or both NULL", name);
     tb_status st = check_common(B, Hq, Hkv, d, dt);
     if (st != TB_OK) return st;
     const int G = Hq / Hkv;
@@ -378,11 +386,12 @@ tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new, vo
     const bool bf16 = dt == TB_BF16;
     const size_t need = decode_ws(B, Hkv, G, d, cap, bf16);
     if (ws_bytes < need)
-      return fail(TB_EWORKSPACE, "tb_decode_attn: workspace %zu < %zu bytes", ws_bytes, need);
+      return fail(TB_EWORKSPACE, "%s: workspace %zu < %zu bytes", name, ws_bytes, need);
     tb::DecodeArgs a{};
     a.q = q; a.k_new = k_new; a.v_new = v_new; a.k_cache = k_cache; a.v_cache = v_cache;
     a.kv_len = kv_len; a.out = out;
     a.B = B; a.Hkv = Hkv; a.cap = cap;
+    if (pg) { a.table = pg->table; a.max_pages = pg->max_pages; a.n_pages = pg->n_pages; }
     const tb::DecodePlan plan = tb::decode_plan(B, Hkv, cap, bf16);
     a.chunk = plan.chunk;
     a.n_chunks = plan.n_chunks;
@@ -393,10 +402,65 @@ tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new, vo
     a.part = reinterpret_cast<float*>(p);
     p += align256(static_cast<size_t>(B) * Hkv * a.n_chunks * G * (d + 4) * sizeof(float));
     a.seq_len = reinterpret_cast<int32_t*>(p);
-    return hip_status(tb::launch_decode(a, G, d, bf16, stream), "tb_decode_attn launch");
+    return hip_status(tb::launch_decode(a, G, d, bf16, stream), name);
   } catch (...) {
-    return fail(TB_EINTERNAL, "tb_decode_attn: internal error");
+    return fail(TB_EINTERNAL, "%s: internal error", name);
   }
 }
+
+tb_status check_paging(const char* name, const int32_t* table, int32_t max_pages,
+                       int32_t n_pages) {
+  if (!table) return fail(TB_EINVAL, "%s: null block table", name);
+  if (max_pages < 1 || n_pages < 1)
+    return fail(TB_EINVAL, "%s: max_pages and n_pages must be >= 1 (got %d, %d)", name,
+                max_pages, n_pages);
+  if (max_pages > (1 << 26))
+    return fail(TB_EUNSUPPORTED, "%s: max_pages must be <= 2^26 (got %d)", name, max_pages);
+  return TB_OK;
+}
+
+}  // namespace
+
+tb_status tb_compact_kv(const void* k, const void* v, const int32_t* keep_idx, int32_t B,
+                        const int32_t* n_keep, int32_t Lmax, int32_t Hkv, int32_t d,
+                        tb_dtype dt, int32_t cap, void* k_cache, void* v_cache,
+                        int32_t* kv_len, void* ws, size_t ws_bytes, hipStream_t stream) {
+  (void)ws; (void)ws_bytes;
+  return compact_impl("tb_compact_kv", k, v, keep_idx, B, n_keep, Lmax, Hkv, d, dt, cap, nullptr,
+                      k_cache, v_cache, kv_len, stream);
+}
+
+tb_status tb_compact_kv_paged(const void* k, const void* v, const int32_t* keep_idx, int32_t B,
+                              const int32_t* n_keep, int32_t Lmax, int32_t Hkv, int32_t d,
+                              tb_dtype dt, void* k_pool, void* v_pool, int32_t n_pages,
+                              const int32_t* block_table, int32_t max_pages, int32_t* kv_len,
+                              hipStream_t stream) {
+  tb_status st = check_paging("tb_compact_kv_paged", block_table, max_pages, n_pages);
+  if (st != TB_OK) return st;
+  const Paging pg{block_table, max_pages, n_pages};
+  return compact_impl("tb_compact_kv_paged", k, v, keep_idx, B, n_keep, Lmax, Hkv, d, dt,
+                      max_pages * tb::kVTile, &pg, k_pool, v_pool, kv_len, stream);
+}
+
+tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new, void* k_cache,
+                         void* v_cache, int32_t* kv_len, int32_t B, int32_t Hq, int32_t Hkv,
+                         int32_t d, int32_t cap, tb_dtype dt, void* out, void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  return decode_impl("tb_decode_attn", q, k_new, v_new, k_cache, v_cache, kv_len, B, Hq, Hkv, d,
+                     cap, nullptr, dt, out, ws, ws_bytes, stream);
+}
+
+tb_status tb_decode_attn_paged(const void* q, const void* k_new, const void* v_new,
+                               void* k_pool, void* v_pool, int32_t n_pages,
+                               const int32_t* block_table, int32_t max_pages, int32_t* kv_len,
+                               int32_t B, int32_t Hq, int32_t Hkv, int32_t d, tb_dtype dt,
+                               void* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  tb_status st = check_paging("tb_decode_attn_paged", block_table, max_pages, n_pages);
+  if (st != TB_OK) return st;
+  const Paging pg{block_table, max_pages, n_pages};
+  return decode_impl("tb_decode_attn_paged", q, k_new, v_new, k_pool, v_pool, kv_len, B, Hq, Hkv,
+                     d, max_pages * tb::kVTile, &pg, dt, out, ws, ws_bytes, stream);
+}
+
 
 }  // extern "C"

@@ -1,7 +1,8 @@
 // Gather of the kept K/V rows into the compact caches.
 //
 // grid = (ceil(max n_keep / 32), Hkv, B), block = 256 threads; block t fills
-// destination rows [32t, 32t + 32) of one (sequence, KV head):
+// destination rows [32t, 32t + 32) of one (sequence, KV head), i.e. one
+// 32-row tile of the contiguous cache or one page of a paged cache:
 //   K rows are copied row-major: each row is split into 16-byte pieces, one
 //     per lane, so a wave instruction moves whole contiguous rows;
 //   V rows are gathered into LDS, then written as one transposed 32-row tile
@@ -19,7 +20,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kVT = kVTile;
 
-template <typename T, int D>
+template <typename T, int D, bool PAGED>
 __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   constexpr int ROW_BYTES = D * sizeof(T);
   constexpr int LPR = ROW_BYTES / 16;                 // lanes per row
@@ -38,8 +39,9 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   const int32_t* keep = a.keep_idx + bg * a.Lmax;
   const char* ks = static_cast<const char*>(a.k) + bg * a.Lmax * ROW_BYTES + part * 16;
   const char* vs = static_cast<const char*>(a.v) + bg * a.Lmax * ROW_BYTES + part * 16;
-  char* kd = static_cast<char*>(a.k_cache) + bg * a.cap * ROW_BYTES + part * 16;
-  T* vtile = static_cast<T*>(a.v_cache) + bg * a.cap * D + static_cast<size_t>(tile) * D * kVT;
+  const size_t off = cache_tile_off<PAGED>(a, b, g, tile, D);   // element offset of the tile
+  char* kd = static_cast<char*>(a.k_cache) + off * sizeof(T) + part * 16;   // tile row 0
+  T* vtile = static_cast<T*>(a.v_cache) + off;
 
   __shared__ T s_v[kVT][D + EPV];                     // padded rows
 
@@ -60,7 +62,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
 #pragma unroll
   for (int p = 0; p < PASSES; ++p) {
     const int rr = r0 + p * ROWS_PER_PASS;
-    if (i0 + rr < n) stg16(kd + static_cast<size_t>(i0 + rr) * ROW_BYTES, kr[p]);
+    if (i0 + rr < n) stg16(kd + static_cast<size_t>(rr) * ROW_BYTES, kr[p]);
     *reinterpret_cast<uint4*>(&s_v[rr][part * EPV]) = vr[p];   // zero past n_keep
   }
   __syncthreads();
@@ -79,7 +81,8 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
 template <typename T, int D>
 hipError_t launch_t(const CompactArgs& a, int max_keep, hipStream_t st) {
   const dim3 grid((max_keep + kVT - 1) / kVT, a.Hkv, a.B);
-  compact_kernel<T, D><<<grid, kThreads, 0, st>>>(a);
+  if (a.table) compact_kernel<T, D, true><<<grid, kThreads, 0, st>>>(a);
+  else         compact_kernel<T, D, false><<<grid, kThreads, 0, st>>>(a);
   return hipGetLastError();
 }
 

@@ -4,7 +4,9 @@
 // Cache layout: K rows are row-major [B][Hkv][cap][d]; V is stored
 // transposed in tiles of 32 rows, [B][Hkv][cap/32][d][32], so that the
 // matrix-core operand "8 consecutive keys of one V column" is one contiguous
-// 16-byte load.
+// 16-byte load.  Paged caches (a block table per sequence) keep the same
+// 32-row tiles in pools [pages][Hkv][32][d] / [pages][Hkv][d][32]; a wave's
+// 32-row step then starts with one table lookup.
 //
 // Two launches per decode step and layer (both capturable in a HIP graph):
 //   partial kernel, grid = (n_chunks, Hkv, B): block (c, g, b) covers key
@@ -52,7 +54,7 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 // bf16: matrix-core partial kernel.
 // --------------------------------------------------------------------------
 // At least two waves per SIMD (<= 256 VGPRs), whatever the block size.
-template <int D, int G, int WAVES>
+template <int D, int G, int WAVES, bool PAGED>
 __global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(2)))
 void decode_mfma_kernel(DecodeArgs a) {
   static_assert(G >= 1 && G <= 16, "query heads per KV head must fit 16 columns");
@@ -68,8 +70,8 @@ void decode_mfma_kernel(DecodeArgs a) {
   __shared__ float s_ml[WAVES][16][2];
 
   const size_t bg = static_cast<size_t>(b) * Hkv + g;
-  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache) + bg * a.cap * D;
-  const uint16_t* vt = static_cast<const uint16_t*>(a.v_cache) + bg * a.cap * D;
+  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
+  const uint16_t* vt = static_cast<const uint16_t*>(a.v_cache);
   const uint16_t* kn = static_cast<const uint16_t*>(a.k_new) + bg * D;
   const uint16_t* vn = static_cast<const uint16_t*>(a.v_new) + bg * D;
   const int cap = a.cap;
@@ -84,15 +86,15 @@ void decode_mfma_kernel(DecodeArgs a) {
   // kv_len: the first block's K/V loads only need rows < cap, so the length
   // load and the data loads are in flight together.
   u32x4 kr[2][KC], vr[NC];
-  auto load_block = [&](int base) {
+  auto load_block = [&](int base) {            // base: a multiple of 32 below cap
+    const size_t off = cache_tile_off<PAGED>(a, b, g, base / kVT, D);
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      const int key = base + krow0 + 4 * t;
-      const uint16_t* src = kc + static_cast<size_t>(min(key, cap - 1)) * D;
+      const uint16_t* src = kc + off + static_cast<size_t>(krow0 + 4 * t) * D;
 #pragma unroll
       for (int k = 0; k < KC; ++k) kr[t][k] = ld16(src + 32 * k + 8 * q4);
     }
-    const uint16_t* vtile = vt + static_cast<size_t>(base / kVT) * D * kVT;
+    const uint16_t* vtile = vt + off;
 #pragma unroll
     for (int n = 0; n < NC; ++n) vr[n] = ld16(vtile + (16 * n + r16) * kVT + 8 * q4);
   };
@@ -130,14 +132,14 @@ void decode_mfma_kernel(DecodeArgs a) {
   // The block owning row n0 stores the appended row (K row, V^T column) from
   // the registers that already hold it: no reload, nothing waits on it.
   if (app && n0 >= lo && n0 < hi && wave == 0) {
+    const size_t off = cache_tile_off<PAGED>(a, b, g, n0 / kVT, D);
     if (r16 == 0) {
-      uint16_t* kd = static_cast<uint16_t*>(a.k_cache) + (bg * cap + n0) * D;
+      uint16_t* kd = static_cast<uint16_t*>(a.k_cache) + off + static_cast<size_t>(n0 % kVT) * D;
 #pragma unroll
       for (int k = 0; k < KC; ++k) *reinterpret_cast<u32x4*>(kd + 32 * k + 8 * q4) = knew[k];
     }
     if (q4 == 0) {
-      uint16_t* vd = static_cast<uint16_t*>(a.v_cache) + bg * cap * D +
-                     static_cast<size_t>(n0 / kVT) * D * kVT + (n0 % kVT);
+      uint16_t* vd = static_cast<uint16_t*>(a.v_cache) + off + (n0 % kVT);
 #pragma unroll
       for (int n = 0; n < NC; ++n) vd[(16 * n + r16) * kVT] = vnew[n];
     }
@@ -290,7 +292,7 @@ constexpr int kValuWaves = kValuThreads / 64;
 constexpr int kUnroll = 4;                  // rows per 16-lane row group per iteration
 constexpr int kRowsPerIter = 4 * kUnroll;   // rows per wave per iteration
 
-template <int D, int G>
+template <int D, int G, bool PAGED>
 __global__ __launch_bounds__(kValuThreads) void decode_valu_kernel(DecodeArgs a) {
   constexpr int DPL = D / 16;                     // elements per lane
   const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
@@ -309,15 +311,15 @@ __global__ __launch_bounds__(kValuThreads) void decode_valu_kernel(DecodeArgs a)
   const int hi = min(lo + a.chunk, N);
 
   const size_t bg = static_cast<size_t>(b) * Hkv + g;
-  const float* kc = static_cast<const float*>(a.k_cache) + bg * a.cap * D;
-  const float* vt = static_cast<const float*>(a.v_cache) + bg * a.cap * D;
+  const float* kc = static_cast<const float*>(a.k_cache);
+  const float* vt = static_cast<const float*>(a.v_cache);
   const float* kn = static_cast<const float*>(a.k_new) + bg * D;
   const float* vn = static_cast<const float*>(a.v_new) + bg * D;
 
   if (app && n0 >= lo && n0 < hi && wave == 0) {
-    float* kd = static_cast<float*>(a.k_cache) + (bg * a.cap + n0) * D;
-    float* vd = static_cast<float*>(a.v_cache) + bg * a.cap * D +
-                static_cast<size_t>(n0 / kVT) * D * kVT + (n0 % kVT);
+    const size_t off = cache_tile_off<PAGED>(a, b, g, n0 / kVT, D);
+    float* kd = static_cast<float*>(a.k_cache) + off + static_cast<size_t>(n0 % kVT) * D;
+    float* vd = static_cast<float*>(a.v_cache) + off + (n0 % kVT);
     constexpr int PER = (D + 63) / 64;
     float kx[PER], vx[PER];
 #pragma unroll
@@ -360,11 +362,14 @@ __global__ __launch_bounds__(kValuThreads) void decode_valu_kernel(DecodeArgs a)
       const int row = base + u * 4 + grp;
       valid[u] = row < whi;
       const bool is_new = app && row == n0;
-      const float* vcol = vt + static_cast<size_t>(row / kVT) * D * kVT + (row % kVT);
+      const int rr = valid[u] ? row : wlo;                      // a row inside the cache
+      const size_t off = cache_tile_off<PAGED>(a, b, g, rr / kVT, D);
+      const float* krow = kc + off + static_cast<size_t>(rr % kVT) * D;
+      const float* vcol = vt + off + (rr % kVT);
 #pragma unroll
       for (int e = 0; e < DPL; ++e) {
         const int d = sub * DPL + e;
-        kf[u][e] = valid[u] ? (is_new ? kn[d] : kc[static_cast<size_t>(row) * D + d]) : 0.f;
+        kf[u][e] = valid[u] ? (is_new ? kn[d] : krow[d]) : 0.f;
         vf[u][e] = valid[u] ? (is_new ? vn[d] : vcol[d * kVT]) : 0.f;
       }
     }
@@ -639,14 +644,14 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeArgs 
   if (h == 0 && tid == 0) a.kv_len[b] = N;
 }
 
-template <typename T, int D, int G>
+template <typename T, int D, int G, bool PAGED>
 hipError_t launch_both(const DecodeArgs& a, hipStream_t st) {
   const dim3 grid(a.n_chunks, a.Hkv, a.B);
   if constexpr (sizeof(T) == 2) {
-    if (a.waves == 1) decode_mfma_kernel<D, G, 1><<<grid, 64, 0, st>>>(a);
-    else              decode_mfma_kernel<D, G, 4><<<grid, 256, 0, st>>>(a);
+    if (a.waves == 1) decode_mfma_kernel<D, G, 1, PAGED><<<grid, 64, 0, st>>>(a);
+    else              decode_mfma_kernel<D, G, 4, PAGED><<<grid, 256, 0, st>>>(a);
   } else {
-    decode_valu_kernel<D, G><<<grid, kValuThreads, 0, st>>>(a);
+    decode_valu_kernel<D, G, PAGED><<<grid, kValuThreads, 0, st>>>(a);
   }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -660,7 +665,8 @@ hipError_t launch_both(const DecodeArgs& a, hipStream_t st) {
 template <typename T, int D>
 hipError_t launch_g(const DecodeArgs& a, int G, hipStream_t st) {
   switch (G) {
-#define TB_CASE(GG) case GG: return launch_both<T, D, GG>(a, st);
+#define TB_CASE(GG) case GG: return a.table ? launch_both<T, D, GG, true>(a, st) \
+                                             : launch_both<T, D, GG, false>(a, st);
     TB_CASE(1) TB_CASE(2) TB_CASE(3) TB_CASE(4) TB_CASE(5) TB_CASE(6) TB_CASE(7) TB_CASE(8)
 #undef TB_CASE
     default: return hipErrorInvalidValue;

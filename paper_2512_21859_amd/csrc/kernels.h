@@ -88,12 +88,31 @@ struct CompactArgs {
   void* v_cache;          // [B][Hkv][cap/32][d][32]
   int32_t* kv_len;        // [B]
   int32_t B, Lmax, Hkv, cap;
+  // paged caches (table != nullptr): tile t of sequence b lives in page
+  // table[b * max_pages + t] of pools [n_pages][Hkv][32][d] (K) / [d][32] (V^T)
+  const int32_t* table;
+  int32_t max_pages, n_pages;
   int32_t n_keep[kMaxB];
 };
 hipError_t launch_compact(const CompactArgs& a, int d, int elem_bytes, int max_keep,
                           hipStream_t st);
 
 // ---------------------------------------------------------------- decode
+// Element offset of the 32-row tile t of (sequence b, KV head g) in the K
+// cache and in the V^T cache (the same offset for both: a tile holds 32 K rows
+// or one 32-key V^T tile).  Contiguous caches: [B][Hkv][cap][d]; paged: pools
+// [n_pages][Hkv][32][d], page from the block table, clamped into the pool.
+template <bool PAGED, typename Args>
+__device__ __forceinline__ size_t cache_tile_off(const Args& a, int b, int g, int t, int d) {
+  if constexpr (PAGED) {
+    int page = a.table[static_cast<size_t>(b) * a.max_pages + t];
+    page = page < 0 ? 0 : (page >= a.n_pages ? a.n_pages - 1 : page);
+    return (static_cast<size_t>(page) * a.Hkv + g) * kVTile * d;
+  } else {
+    return ((static_cast<size_t>(b) * a.Hkv + g) * a.cap + static_cast<size_t>(t) * kVTile) * d;
+  }
+}
+
 struct DecodeArgs {
   const void* q;          // [B][Hq][d]
   const void* k_new;      // [B][Hkv][d] (unused when append == 0)
@@ -106,6 +125,8 @@ struct DecodeArgs {
   int32_t* seq_len;       // ws: [B] attended length of this step
   int32_t B, Hkv, cap, chunk, n_chunks, append;
   int32_t waves;          // waves per partial block (bf16: 1 or 4)
+  const int32_t* table;   // paged caches (nullptr: contiguous); see CompactArgs
+  int32_t max_pages, n_pages;
   float scale_log2;       // log2(e)/sqrt(d)
 };
 // How a decode launch splits the cache: rows per block, blocks per KV head and

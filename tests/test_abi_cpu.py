@@ -216,6 +216,41 @@ def test_decode_validation(lib):
     assert call(ws=None) == E.TB_EINVAL
 
 
+def test_compact_paged_validation(lib):
+    E = _lib
+
+    def call(n=50, max_pages=2, n_pages=8, table=FAKE, kp=FAKE, d=128):
+        return lib.tb_compact_kv_paged(FAKE, FAKE, FAKE, 1, _i32(n), 100, 2, d, _lib.TB_BF16,
+                                       kp, FAKE, n_pages, table, max_pages, FAKE, None)
+
+    assert call(table=None) == E.TB_EINVAL
+    assert b"block table" in lib.tb_last_error()
+    assert call(max_pages=0) == E.TB_EINVAL
+    assert call(n_pages=0) == E.TB_EINVAL
+    assert call(max_pages=1 << 27) == E.TB_EUNSUPPORTED
+    assert call(n=65) == E.TB_EINVAL          # beyond max_pages * 32 rows
+    assert call(kp=None) == E.TB_EINVAL
+    assert call(d=32) == E.TB_EUNSUPPORTED
+
+
+def test_decode_paged_validation(lib):
+    E = _lib
+
+    def call(Hq=28, Hkv=4, d=128, max_pages=4, n_pages=8, table=FAKE, wsb=1 << 30, kn=FAKE,
+             vn=FAKE):
+        return lib.tb_decode_attn_paged(FAKE, kn, vn, FAKE, FAKE, n_pages, table, max_pages, FAKE,
+                                        1, Hq, Hkv, d, _lib.TB_BF16, FAKE, FAKE, wsb, None)
+
+    assert call(table=None) == E.TB_EINVAL
+    assert call(n_pages=0) == E.TB_EINVAL
+    assert call(kn=None) == E.TB_EINVAL
+    assert call(Hq=36) == E.TB_EUNSUPPORTED
+    assert call(d=256) == E.TB_EUNSUPPORTED
+    need = _lib.tb_workspace_bytes(_lib.TB_OP_DECODE, 1, 0, 28, 4, 128, 0, 4 * 32)
+    assert call(wsb=need - 1) == E.TB_EWORKSPACE
+    assert b"tb_decode_attn_paged: workspace" in lib.tb_last_error()
+
+
 def test_binding_refuses_cpu_tensors():
     import torch
     with pytest.raises(ValueError):

@@ -1,0 +1,209 @@
+"""GPU parity of the paged caches and of the multi-request server.
+
+Paged compaction and decode must give bit-for-bit what the contiguous entry
+points give on the same rows (the tile arithmetic is shared; only where a
+tile lives differs), with sequences' pages scattered through the pool, pages
+owned by nobody left untouched, and table entries past a sequence's length
+holding junk.  The server test runs a stream of requests with per-request
+ratios through admission, decode and retirement (slots move, pages are
+reused) and checks every output against the float64 oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import timebill_oracle as O
+from paper_2512_21859_amd import _lib, synth
+from paper_2512_21859_amd.serving import PAGE, Server
+from tests.parity_util import DECODE_TOL, check_keep, f64
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+FILL = 0.5
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU in this container")
+    _lib.load()
+    torch.cuda.init()
+
+
+def case(msg):
+    print(f"\n[case] {msg}", flush=True)
+
+
+def _gather_k(k_pool, pages, g, n):
+    return torch.cat([k_pool[p, g] for p in pages], dim=0)[:n]
+
+
+@pytest.mark.parametrize("dtype,d,G", [(torch.bfloat16, 128, 7), (torch.bfloat16, 128, 8),
+                                       (torch.bfloat16, 64, 1), (torch.float32, 128, 4),
+                                       (torch.float32, 64, 3)])
+def test_paged_equals_contiguous(dtype, d, G):
+    case(f"paged_vs_contiguous dtype={dtype} d={d} G={G}")
+    B, Hkv, Lmax, T = 3, 2, 1000, 40
+    Hq = G * Hkv
+    n_keep = [1, 517, 1000]                        # 517 + 40 crosses a page boundary
+    max_pages = 36                                 # 1152 rows >= 1000 + 40
+    gen = torch.Generator().manual_seed(77 + d + G)
+    k = torch.randn((B, Hkv, Lmax, d), generator=gen).to(dtype)
+    v = torch.randn((B, Hkv, Lmax, d), generator=gen).to(dtype)
+    keep = torch.zeros((B, Hkv, Lmax), dtype=torch.int32)
+    for b in range(B):
+        for g in range(Hkv):
+            keep[b, g, : n_keep[b]] = torch.sort(
+                torch.randperm(Lmax, generator=gen)[: n_keep[b]]).values.to(torch.int32)
+    q = torch.randn((T + 1, B, Hq, d), generator=gen).to(dtype)
+    kn = torch.randn((T, B, Hkv, d), generator=gen).to(dtype)
+    vn = torch.randn((T, B, Hkv, d), generator=gen).to(dtype)
+
+    # pages scattered through a pool larger than needed; each row ends in junk entries
+    need = [-(-(n + T) // PAGE) for n in n_keep]
+    n_pages = sum(need) + 13
+    perm = torch.randperm(n_pages, generator=gen).tolist()
+    pages, at = [], 0
+    for n in need:
+        pages.append(perm[at:at + n])
+        at += n
+    unused = perm[at:]
+    table = torch.empty((B, max_pages), dtype=torch.int32)
+    for b in range(B):
+        junk = [-7, 10 ** 6, n_pages][b]
+        table[b] = torch.tensor(pages[b] + [junk] * (max_pages - need[b]), dtype=torch.int32)
+    k_pool = torch.full((n_pages, Hkv, PAGE, d), FILL, dtype=dtype, device=DEV)
+    v_pool = torch.full((n_pages, Hkv, d, PAGE), FILL, dtype=dtype, device=DEV)
+    cap = max_pages * PAGE
+    kc = torch.full((B, Hkv, cap, d), FILL, dtype=dtype, device=DEV)
+    vc = torch.full((B, Hkv, cap // PAGE, d, PAGE), FILL, dtype=dtype, device=DEV)
+    len_p = torch.zeros((B,), dtype=torch.int32, device=DEV)
+    len_c = torch.zeros((B,), dtype=torch.int32, device=DEV)
+    kd, vd, keepd, tabd = k.to(DEV), v.to(DEV), keep.to(DEV), table.to(DEV)
+
+    _lib.tb_compact_kv(kd, vd, keepd, n_keep, kc, vc, len_c)
+    _lib.tb_compact_kv_paged(kd, vd, keepd, n_keep, k_pool, v_pool, tabd, len_p)
+    ws = torch.zeros((_lib.tb_workspace_bytes(_lib.TB_OP_DECODE, B, 0, Hq, Hkv, d, 0, cap),),
+                     dtype=torch.uint8, device=DEV)
+    ws_p = torch.zeros_like(ws)
+    qd, knd, vnd = q.to(DEV), kn.to(DEV), vn.to(DEV)
+    out_c = torch.empty((T + 1, B, Hq, d), dtype=dtype, device=DEV)
+    out_p = torch.empty_like(out_c)
+    for t in range(T + 1):
+        a, b_ = (knd[t], vnd[t]) if t < T else (None, None)
+        _lib.tb_decode_attn(qd[t], a, b_, kc, vc, len_c, out_c[t], ws)
+        _lib.tb_decode_attn_paged(qd[t], a, b_, k_pool, v_pool, tabd, len_p, out_p[t], ws_p)
+    torch.cuda.synchronize()
+
+    assert len_p.tolist() == len_c.tolist() == [n + T for n in n_keep]
+    assert torch.equal(out_p, out_c), "paged decode differs from the contiguous decode"
+    for b in range(B):
+        n = n_keep[b] + T
+        for g in range(Hkv):
+            assert torch.equal(_gather_k(k_pool, pages[b], g, n), kc[b, g, :n])
+            for t, p in enumerate(pages[b]):
+                assert torch.equal(v_pool[p, g], vc[b, g, t]), f"b={b} g={g} tile {t}"
+    for p in unused:
+        assert bool((k_pool[p] == FILL).all()) and bool((v_pool[p] == FILL).all()), \
+            f"page {p} owned by nobody was written"
+
+    # the oracle on sampled steps: kept prompt rows then the appended ones
+    got, k64, v64, q64 = f64(out_p), f64(k), f64(v), f64(q)
+    kn64, vn64 = f64(kn), f64(vn)
+    for b in range(B):
+        for g in range(Hkv):
+            idx = keep[b, g, : n_keep[b]].long().numpy()
+            for t in (0, T // 2, T - 1, T):
+                s = min(t + 1, T)
+                rk = np.concatenate([k64[b, g, idx], kn64[:s, b, g]])
+                rv = np.concatenate([v64[b, g, idx], vn64[:s, b, g]])
+                ref = O.decode_step(q64[t, b, g * G:(g + 1) * G], rk, rv)
+                err = np.abs(got[t, b, g * G:(g + 1) * G] - ref).max()
+                assert err <= DECODE_TOL[dtype], f"b={b} g={g} t={t}: max abs err {err}"
+
+
+def test_server_stream_matches_oracle():
+    """Ten requests with their own ratios and response lengths arrive over
+    time; admission waits for slots and pages; finished requests retire and
+    their pages are reused."""
+    n_req, layers, Hq, Hkv, d, w, pool = 10, 2, 28, 4, 128, 32, 7
+    G = Hq // Hkv
+    gen = torch.Generator().manual_seed(2512)
+    L = torch.randint(200, 2500, (n_req,), generator=gen).tolist()
+    alphas = (0.9 * torch.rand(n_req, generator=gen, dtype=torch.float64)).tolist()
+    max_new = torch.randint(3, 41, (n_req,), generator=gen).tolist()
+    arrive = sorted(torch.randint(0, 30, (n_req,), generator=gen).tolist())
+    case(f"server stream L={L} max_new={max_new} arrive={arrive}")
+    wl = synth.custom(61, torch.bfloat16, n_req, L, Hq, Hkv, d, w, pool, max(max_new))
+    prompts = [synth.make_prompt(wl, layer, L) for layer in range(layers)]
+    dec = [synth.make_decode(wl, layer) for layer in range(layers)]
+
+    srv = Server(layers, n_pages=260, max_seqs=5, max_pages=80, Hq=Hq, Hkv=Hkv, d=d,
+                 dtype=torch.bfloat16, w=w, pool=pool, max_admit=3, max_prompt=max(L))
+    queue = list(range(n_req))
+    done_steps = {r: 0 for r in range(n_req)}
+    n_keep_of, keep_of = {}, {}
+    outs = {r: [] for r in range(n_req)}
+    step, moved = 0, 0
+    while queue or srv.n_active:
+        for r in srv.slots.finished():
+            if srv.rids().index(r) != srv.n_active - 1:
+                moved += 1
+            keep_of[r] = [t.cpu() for t in srv.keep[r]]
+            srv.retire([r])
+        batch = []
+        while (queue and arrive[queue[0]] <= step and len(batch) < srv.max_admit and
+               srv.slots.fits([_lib.tb_keep_count(L[r], alphas[r], w) + max_new[r]
+                               for r in batch + [queue[0]]])):
+            batch.append(queue.pop(0))
+        if batch:
+            bl = [L[r] for r in batch]
+            lm = max(bl)
+            pr = [{key: prompts[layer][key][batch][:, :, :lm].contiguous().to(DEV)
+                   for key in ("q_win", "k", "v")} for layer in range(layers)]
+            for layer in range(layers):
+                pr[layer]["q_win"] = prompts[layer]["q_win"][batch].contiguous().to(DEV)
+            nk = srv.admit(batch, bl, [alphas[r] for r in batch],
+                           [max_new[r] for r in batch], pr, keep_sets=True)
+            n_keep_of.update(zip(batch, nk))
+        if srv.n_active:
+            rid = srv.rids()
+            qs = torch.stack([torch.stack([dec[layer]["q"][done_steps[r], r] for r in rid])
+                              for layer in range(layers)]).to(DEV)
+            ks = torch.stack([torch.stack([dec[layer]["k_new"][done_steps[r], r] for r in rid])
+                              for layer in range(layers)]).to(DEV)
+            vs = torch.stack([torch.stack([dec[layer]["v_new"][done_steps[r], r] for r in rid])
+                              for layer in range(layers)]).to(DEV)
+            out = torch.empty_like(qs)
+            srv.step(qs, ks, vs, out)
+            o = out.cpu()
+            for i, r in enumerate(rid):
+                outs[r].append(o[:, i])
+                done_steps[r] += 1
+        step += 1
+        assert step < 500, "stream did not drain"
+    torch.cuda.synchronize()
+    assert moved > 0, "no slot move was exercised"
+    assert len(srv.slots.free) == srv.slots.n_pages
+
+    tol = DECODE_TOL[torch.bfloat16]
+    for r in range(n_req):
+        assert len(outs[r]) == max_new[r]
+        for layer in range(layers):
+            k64 = f64(prompts[layer]["k"][r])
+            v64 = f64(prompts[layer]["v"][r])
+            q64 = f64(prompts[layer]["q_win"][r])
+            pooled = O.max_pool(O.window_scores(q64, k64, L[r], w), pool)
+            keep = keep_of[r][layer].numpy()
+            assert keep.shape == (Hkv, n_keep_of[r])
+            for g in range(Hkv):
+                check_keep(keep[g], pooled[g], L[r], w, n_keep_of[r], f"r={r} l={layer} g={g}")
+            dq, dk, dv = (f64(dec[layer][x][:, r]) for x in ("q", "k_new", "v_new"))
+            for s in range(max_new[r]):
+                got = f64(outs[r][s][layer])
+                for g in range(Hkv):
+                    rk = np.concatenate([k64[g, keep[g]], dk[: s + 1, g]])
+                    rv = np.concatenate([v64[g, keep[g]], dv[: s + 1, g]])
+                    ref = O.decode_step(dq[s, g * G:(g + 1) * G], rk, rv)
+                    err = np.abs(got[g * G:(g + 1) * G] - ref).max()
+                    assert err <= tol, f"r={r} layer={layer} g={g} step={s}: err {err}"

@@ -1,0 +1,99 @@
+"""Host bookkeeping of the paged server (no device): page reservation, dense
+slots, retirement by moving the last request, and the block-table rows."""
+import random
+
+import numpy as np
+import pytest
+
+from paper_2512_21859_amd.serving import PAGE, SlotTable
+
+
+def _invariants(st: SlotTable):
+    owned = [p for e in st.slots for p in e.pages]
+    assert len(owned) == len(set(owned)), "a page is owned twice"
+    assert not set(owned) & set(st.free), "a page is both owned and free"
+    assert sorted(owned + st.free) == list(range(st.n_pages)), "pages lost or invented"
+    assert len(st.slots) <= st.max_seqs
+    rows = st.table_rows()
+    assert rows.shape == (len(st.slots), st.max_pages)
+    for i, e in enumerate(st.slots):
+        assert e.length + e.left <= len(e.pages) * PAGE, "reservation too small"
+        assert rows[i, : len(e.pages)].tolist() == e.pages
+        # every row decode can touch (tiles below the final length) is the request's own page
+        last_tile = (e.length + e.left - 1) // PAGE
+        assert set(rows[i, : last_tile + 1].tolist()) <= set(e.pages)
+    assert st.lengths().tolist() == [e.length for e in st.slots]
+
+
+def test_reserve_and_release():
+    st = SlotTable(n_pages=9, max_seqs=3, max_pages=4)
+    assert st.admit(7, n_keep=33, max_new=0) == 0          # 2 pages
+    assert st.slots[0].pages == [0, 1]
+    assert st.admit(8, n_keep=100, max_new=28) == 1        # 128 rows: 4 pages
+    with pytest.raises(ValueError):
+        st.admit(9, n_keep=100, max_new=29)                # 5 pages > max_pages
+    with pytest.raises(ValueError):
+        st.admit(7, n_keep=1, max_new=1)                   # already running
+    with pytest.raises(MemoryError):
+        st.admit(9, n_keep=120, max_new=8)                 # 4 pages needed, 3 free
+    st.admit(9, n_keep=90, max_new=6)                      # takes the last 3 pages
+    with pytest.raises(MemoryError):
+        st.admit(10, n_keep=1, max_new=0)                  # no slot left
+    _invariants(st)
+    assert st.retire(7) == 2                               # the last slot moved into 0
+    assert [e.rid for e in st.slots] == [9, 8]
+    assert st.retire(8) is None                            # last slot: nothing moves
+    _invariants(st)
+
+
+def test_fits_counts_pages_and_slots():
+    st = SlotTable(n_pages=8, max_seqs=4, max_pages=8)
+    assert st.fits([32 * 4, 32 * 4])
+    assert not st.fits([32 * 4, 32 * 4 + 1])
+    assert not st.fits([1] * 5)
+    assert not st.fits([32 * 9])
+
+
+def test_advance_and_finish():
+    st = SlotTable(n_pages=16, max_seqs=4, max_pages=4)
+    st.admit(1, 31, 2)
+    st.admit(2, 10, 1)
+    st.advance()
+    assert st.lengths().tolist() == [32, 11]
+    assert st.finished() == [2]
+    with pytest.raises(RuntimeError):
+        st.advance()                                       # request 2 has no steps left
+    st.retire(2)
+    st.advance()
+    assert st.lengths().tolist() == [33] and st.finished() == [1]
+    _invariants(st)
+
+
+def test_table_rows_pad_with_own_last_page():
+    st = SlotTable(n_pages=6, max_seqs=2, max_pages=5)
+    st.admit(0, 40, 0)                                     # pages 0, 1
+    st.admit(1, 1, 0)                                      # page 2
+    assert st.table_rows().tolist() == [[0, 1, 1, 1, 1], [2, 2, 2, 2, 2]]
+    assert st.table_rows(1, 2).tolist() == [[2, 2, 2, 2, 2]]
+
+
+def test_random_stream_keeps_invariants():
+    rng = random.Random(5)
+    st = SlotTable(n_pages=64, max_seqs=8, max_pages=12)
+    rid = 0
+    for _ in range(2000):
+        op = rng.random()
+        if op < 0.3:
+            n_keep, max_new = rng.randint(1, 300), rng.randint(0, 80)
+            if st.fits([n_keep + max_new]):
+                st.admit(rid, n_keep, max_new)
+                rid += 1
+        elif op < 0.8 and st.slots:
+            for r in st.finished():
+                st.retire(r)
+            if st.slots:
+                st.advance()
+        elif st.slots:
+            st.retire(rng.choice(st.slots).rid)
+        _invariants(st)
+    assert rid > 100
