@@ -54,7 +54,10 @@ def _parse():
                     help="skip the prefill-attention sweep")
     ap.add_argument("--no-scorers", action="store_true",
                     help="skip the scorer-variant timings")
-    ap.add_argument("--only", choices=("cold", "long", "layers", "ceiling", "scorers", "prefill"),
+    ap.add_argument("--no-paged", action="store_true",
+                    help="skip the paged-cache batch and serving-stream measurements")
+    ap.add_argument("--only", choices=("cold", "long", "layers", "ceiling", "scorers", "prefill",
+                                       "paged"),
                     help="run one supplementary measurement alone and print its JSON "
                          "(for profiling that workload by itself)")
     ap.add_argument("--pmc-calibration", action="store_true",
@@ -458,6 +461,169 @@ def layer_sweep(torch, _lib, synth, Evictor, dev, T=None):
                       f"{T} x {nl} decode launches"}
 
 
+def paged_serving(torch, _lib, synth, Evictor, dev, T=64, n_req=64, max_seqs=16,
+                  max_admit=8):
+    """Supplementary: paged caches.
+
+    (1) The ragged 16-sequence batch (prompts of 1024..16384 tokens, a ratio
+    in [0, 0.9] per sequence, 28 q / 4 kv heads, d = 128) decoded for T steps
+    from contiguous caches and from pages scattered through a pool, with the
+    same launch plan; both replayed from graphs.
+    (2) A stream of n_req requests through the server (one layer): prompts of
+    1024..16384 tokens, ratios in [0, 0.9], 64..256 new tokens each, all
+    waiting at the start; up to max_admit are evicted per admission batch and
+    up to max_seqs decode together; a finished request frees its pages at
+    once.  Timed by the wall clock (host bookkeeping included) and by HIP
+    events around each admission and decode step."""
+    from paper_2512_21859_amd.serving import PAGE, Server
+    wl = synth.WORKLOADS[4]
+    B, Hq, Hkv, d, w, pool = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.pool
+    L, alphas = synth.lengths_and_alphas(wl)
+    Lmax = max(L)
+    pr = synth.make_prompt(wl)
+    dc = synth.make_decode(wl, T=T)
+    q_win, k, v = (pr[x].to(dev) for x in ("q_win", "k", "v"))
+    qd, knd, vnd = (dc[x].to(dev) for x in ("q", "k_new", "v_new"))
+    del pr, dc
+    stream = torch.cuda.current_stream()
+    ev = Evictor(B, Lmax, Hq, Hkv, d, w, pool, device=dev)
+    ev.score(q_win, k, L, stream)
+    n_keep = ev.select(L, alphas, stream)
+    cap = -(-(max(n_keep) + T) // PAGE) * PAGE
+    cache = _lib.KVCache(B, Hq, Hkv, cap, d, wl.dtype, device=dev)
+    max_pages = cap // PAGE
+    need = [-(-(n + T) // PAGE) for n in n_keep]
+    gen = torch.Generator().manual_seed(4242)
+    perm = torch.randperm(sum(need), generator=gen).tolist()
+    table = torch.empty((B, max_pages), dtype=torch.int32)
+    at = 0
+    for b in range(B):
+        pg = perm[at:at + need[b]]
+        at += need[b]
+        table[b] = torch.tensor(pg + [pg[-1]] * (max_pages - need[b]), dtype=torch.int32)
+    table = table.to(dev)
+    k_pool = torch.zeros((sum(need), Hkv, PAGE, d), dtype=wl.dtype, device=dev)
+    v_pool = torch.zeros((sum(need), Hkv, d, PAGE), dtype=wl.dtype, device=dev)
+    len_p = torch.zeros((B,), dtype=torch.int32, device=dev)
+    ws_p = torch.zeros_like(cache.ws)
+    out_c = torch.empty((T, B, Hq, d), dtype=wl.dtype, device=dev)
+    out_p = torch.empty_like(out_c)
+
+    def reset():
+        cache.compact_from(k, v, ev.keep_idx, n_keep, stream)
+        _lib.tb_compact_kv_paged(k, v, ev.keep_idx, n_keep, k_pool, v_pool, table, len_p, stream)
+
+    reset()
+    torch.cuda.synchronize()
+    cs = torch.cuda.Stream()
+    g_c, g_p = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_c, stream=cs):
+        for t in range(T):
+            _lib.tb_decode_attn(qd[t], knd[t], vnd[t], cache.k, cache.v, cache.kv_len, out_c[t],
+                                cache.ws, stream=cs)
+    with torch.cuda.graph(g_p, stream=cs):
+        for t in range(T):
+            _lib.tb_decode_attn_paged(qd[t], knd[t], vnd[t], k_pool, v_pool, table, len_p,
+                                      out_p[t], ws_p, stream=cs)
+    torch.cuda.synchronize()
+    best = {"contiguous": float("inf"), "paged": float("inf")}
+    for _ in range(3):
+        for name, g in (("contiguous", g_c), ("paged", g_p)):
+            reset()
+            best[name] = min(best[name], _best_ms(torch, g.replay, reps=1))
+    same = bool(torch.equal(out_c, out_p))
+    dbytes = sum(_decode_bytes(Hq, Hkv, d, n + t + 1) for n in n_keep for t in range(T)) / T
+    batch = {"workload": f"bf16, B={B} ragged prompts {min(L)}..{max(L)}, ratios "
+                         f"{min(alphas):.2f}..{max(alphas):.2f}, 28 q / 4 kv heads, d=128, "
+                         f"{T} decode steps",
+             "n_keep_total": sum(n_keep), "pages": sum(need), "bit_identical": same}
+    for name in ("contiguous", "paged"):
+        us = best[name] * 1e3 / T
+        batch[name] = {"us_per_step": round(us, 2),
+                       "GBps": round(dbytes / (us * 1e-6) / 1e9, 1)}
+    batch["paged_over_contiguous"] = round(best["paged"] / best["contiguous"], 4)
+    del cache, k_pool, v_pool, g_c, g_p, q_win, k, v, qd, knd, vnd, ev, out_c, out_p
+    torch.cuda.empty_cache()
+
+    # (2) the stream
+    gen = torch.Generator().manual_seed(6464)
+    rL = torch.randint(1024, 16385, (n_req,), generator=gen).tolist()
+    ra = (0.9 * torch.rand(n_req, generator=gen, dtype=torch.float64)).tolist()
+    rn = torch.randint(64, 257, (n_req,), generator=gen).tolist()
+    Pmax = 16384
+    max_pages = -(-(Pmax + 256) // PAGE)
+    srv = Server(1, n_pages=max_seqs * max_pages, max_seqs=max_seqs, max_pages=max_pages,
+                 Hq=Hq, Hkv=Hkv, d=d, dtype=wl.dtype, w=w, pool=pool, max_admit=max_admit,
+                 max_prompt=Pmax, device=dev)
+    dg = torch.Generator(device=dev).manual_seed(77)
+    kb = torch.randn((max_admit, Hkv, Pmax, d), generator=dg, device=dev).to(wl.dtype)
+    vb = torch.randn((max_admit, Hkv, Pmax, d), generator=dg, device=dev).to(wl.dtype)
+    qb = torch.randn((max_admit, Hq, w, d), generator=dg, device=dev).to(wl.dtype)
+    qs = torch.randn((1, max_seqs, Hq, d), generator=dg, device=dev).to(wl.dtype)
+    ks = torch.randn((1, max_seqs, Hkv, d), generator=dg, device=dev).to(wl.dtype)
+    vs = torch.randn((1, max_seqs, Hkv, d), generator=dg, device=dev).to(wl.dtype)
+    out = torch.empty_like(qs)
+
+    def run(timed):
+        queue = list(range(n_req))
+        ev_pairs, de_pairs = [], []
+        steps = tokens = batch_sum = 0
+        dec_bytes = 0.0
+        while queue or srv.n_active:
+            fin = srv.slots.finished()
+            if fin:
+                srv.retire(fin)
+            adm = []
+            while (queue and len(adm) < max_admit and srv.slots.fits(
+                    [_lib.tb_keep_count(rL[r], ra[r], w) + rn[r] for r in adm + [queue[0]]])):
+                adm.append(queue.pop(0))
+            if adm:
+                b = len(adm)
+                e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                e[0].record(stream)
+                srv.admit(adm, [rL[r] for r in adm], [ra[r] for r in adm],
+                          [rn[r] for r in adm],
+                          [{"q_win": qb[:b], "k": kb[:b], "v": vb[:b]}], stream=stream)
+                e[1].record(stream)
+                ev_pairs.append(e)
+            n = srv.n_active
+            if n == 0:
+                continue                         # the last requests just retired
+            lens = srv.slots.lengths()
+            e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            e[0].record(stream)
+            srv.step(qs[:, :n], ks[:, :n], vs[:, :n], out[:, :n], stream=stream)
+            e[1].record(stream)
+            de_pairs.append(e)
+            steps += 1
+            tokens += n
+            batch_sum += n
+            dec_bytes += sum(_decode_bytes(Hq, Hkv, d, int(x) + 1) for x in lens)
+        torch.cuda.synchronize()
+        return ev_pairs, de_pairs, steps, tokens, batch_sum, dec_bytes
+
+    run(False)                                   # warm-up pass over the whole stream
+    t0 = time.perf_counter()
+    ev_pairs, de_pairs, steps, tokens, batch_sum, dec_bytes = run(True)
+    wall = time.perf_counter() - t0
+    ev_ms = sum(a.elapsed_time(b) for a, b in ev_pairs)
+    de_ms = sum(a.elapsed_time(b) for a, b in de_pairs)
+    stream_res = {
+        "workload": f"{n_req} requests, 1 layer bf16, prompts 1024..16384, ratios 0..0.9, "
+                    f"64..256 new tokens, <= {max_seqs} decoding, <= {max_admit} per admission",
+        "tokens": tokens, "decode_steps": steps, "admissions": len(ev_pairs),
+        "mean_batch": round(batch_sum / steps, 2),
+        "wall_s": round(wall, 4), "tokens_per_s_wall": round(tokens / wall, 1),
+        "gpu_decode_ms": round(de_ms, 3), "gpu_evict_ms": round(ev_ms, 3),
+        "tokens_per_s_gpu": round(tokens / ((de_ms + ev_ms) * 1e-3), 1),
+        "decode_GBps": round(dec_bytes / (de_ms * 1e-3) / 1e9, 1),
+        "timing": "second pass over the stream (the first warms up); GPU figures sum HIP "
+                  "events around each admission and each decode step"}
+    del srv, kb, vb, qb
+    torch.cuda.empty_cache()
+    return {"batch": batch, "stream": stream_res}
+
+
 def main():
     args = _parse()
     if args.gpus != 1:
@@ -480,12 +646,13 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    if args.only in ("long", "layers", "ceiling", "scorers", "prefill"):
+    if args.only in ("long", "layers", "ceiling", "scorers", "prefill", "paged"):
         fn = {"long": lambda: long_context(torch, _lib, synth, Evictor, dev),
               "layers": lambda: layer_sweep(torch, _lib, synth, Evictor, dev),
               "ceiling": lambda: hbm_ceiling(torch, dev),
               "scorers": lambda: scorer_variants(torch, _lib, synth, Evictor, dev),
-              "prefill": lambda: prefill_sweep(torch, _lib, synth, dev)}[args.only]
+              "prefill": lambda: prefill_sweep(torch, _lib, synth, dev),
+              "paged": lambda: paged_serving(torch, _lib, synth, Evictor, dev)}[args.only]
         print(json.dumps({"section": args.only, **fn()}), flush=True)
         return
     wl = synth.WORKLOADS[2]
@@ -645,6 +812,8 @@ def main():
         result["long_context"] = long_context(torch, _lib, synth, Evictor, dev)
     if not args.no_prefill:
         result["prefill"] = prefill_sweep(torch, _lib, synth, dev)
+    if not args.no_paged:
+        result["paged"] = paged_serving(torch, _lib, synth, Evictor, dev)
     if not args.no_scorers:
         result["scorers"] = scorer_variants(torch, _lib, synth, Evictor, dev)
     if not args.no_layer_sweep:
