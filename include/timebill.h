@@ -92,9 +92,9 @@ const char* tb_last_error(void);
 
 /* [host] Workspace bytes the operation `op` needs for these sizes (0 if none).
  * `cap` is used by TB_OP_DECODE only; arguments an op does not use are
- * ignored.  Returns 0 and sets the error for invalid sizes.  The decode need
- * is not monotone in B (a small batch is split into more chunks): a caller
- * whose batch size varies sizes for the largest need over those sizes. */
+ * ignored.  Returns 0 and sets the error for invalid sizes.  For
+ * TB_OP_DECODE the size covers every batch of at most B sequences with this
+ * cap (the split depends on the batch size). */
 size_t tb_workspace_bytes(int32_t op, int32_t B, int32_t Lmax, int32_t Hq,
                           int32_t Hkv, int32_t d, int32_t w, int32_t cap);
 

@@ -71,35 +71,59 @@ size_t decode_ws(int32_t B, int32_t Hkv, int32_t G, int32_t d, int32_t cap, bool
 
 namespace tb {
 
-// How a decode step splits the cache (measured on the single-layer L = 8192
-// workload, 4 KV heads):
-// * The merge reads a KV head's partials in one round of loads when there are
-//   at most 64 of them; a second round costs more than larger chunks do.
-// * Small caches (up to ~3k rows per head here) are fastest with one-wave
-//   blocks: each wave writes its own partial from registers, with no LDS
-//   combine or barrier (410 rows: 7.6 us per step vs 8.2 with 4-wave blocks).
-//   Up to 2048 rows per head, chunks of 32 or 64 rows leave at most 32
-//   partials per head, which one wave per query head merges in a single
-//   round of loads (410..1536 rows: 0.3..0.5 us less per step); beyond that,
-//   chunks are sized for at most 64 partials and the block merge.
-// * Larger caches use 4-wave blocks, with the fewest rows per block that keep
-//   the grid at one block per CU (256 CUs), since a CU holding two blocks sets
-//   the step time.
+// How a decode step splits the cache (bf16; measured over 410..32768 rows
+// per KV head at 1, 4 and 16 sequences of 4 KV heads, graph-replayed steps):
+// * A CU that holds two partial blocks sets the step time, so a KV head gets
+//   floor(256 / units) blocks (one per CU over the whole grid) and a block
+//   takes as many rows as that needs, however many.  (Capping a block at 1024
+//   rows, as before, put 272 blocks on 256 CUs at 4 x 16k rows: 33 us per
+//   step instead of 24.)
+// * The block's rows are split over 1, 2, 4 or 8 waves: rounding a chunk up to
+//   a multiple of 32 rows per wave can cost blocks, so among the shapes that
+//   keep at least 80% of the best block count, the one with the most waves
+//   that still gives each wave >= 64 rows (more loads in flight per CU,
+//   shorter per-wave chains).
+// * Small caches (<= 2560 rows) keep at most 32 partials per KV head, which
+//   one wave per query head merges in a single round of loads.
+// * Batches (B > 1) are usually ragged, and the plan sees only the capacity:
+//   blocks past a sequence's length exit at once, so small blocks (one wave,
+//   at most 384 rows) balance the real work across CUs.  On ragged batches and
+//   a 64-request serving stream this was 11-28% faster than one block per CU
+//   per KV head; on uniform batches it costs 2-6%.
+// fp32 runs the vector-ALU kernel at a fixed block shape, sized the old way.
 DecodePlan decode_plan(int B, int Hkv, int cap, bool bf16) {
   const long long units = static_cast<long long>(B) * Hkv;
   DecodePlan p{};
-  if (bf16 && units * cap <= 12288) {
+  if (!bf16) {
     p.waves = 1;
-    const long long unit = decode_chunk_unit(1, true);
-    const long long parts = cap <= 2048 ? 32 : 64;
-    p.chunk = static_cast<int32_t>((cap + unit * parts - 1) / (unit * parts) * unit);
-  } else {
-    p.waves = bf16 ? 4 : 1;
-    const long long unit = decode_chunk_unit(p.waves, bf16);
+    const long long unit = decode_chunk_unit(1, false);
     long long want = (static_cast<long long>(cap) * units + 255) / 256;
     want = std::min<long long>(std::max<long long>(want, unit), 1024);
     want = std::max<long long>(want, (cap + decode_max_chunks() - 1) / decode_max_chunks());
     p.chunk = static_cast<int32_t>((want + unit - 1) / unit * unit);
+    p.n_chunks = (cap + p.chunk - 1) / p.chunk;
+    return p;
+  }
+  const long long per_unit = std::max<long long>(1, 256 / units);
+  long long rows = (cap + per_unit - 1) / per_unit;
+  if (cap <= 2560) rows = std::max<long long>(rows, (cap + 31) / 32);
+  long long chunk[4], blocks[4], best_blocks = 0;
+  for (int i = 0; i < 4; ++i) {
+    const long long unit = static_cast<long long>(kVTile) << i;      // 32 rows per wave
+    chunk[i] = (rows + unit - 1) / unit * unit;
+    blocks[i] = units * ((cap + chunk[i] - 1) / chunk[i]);
+    best_blocks = std::max(best_blocks, blocks[i]);
+  }
+  int pick = 0;
+  for (int i = 1; i < 4; ++i)
+    if (blocks[i] * 5 >= best_blocks * 4 && (chunk[i] >> i) >= 64) pick = i;
+  p.waves = 1 << pick;
+  p.chunk = static_cast<int32_t>(chunk[pick]);
+  constexpr int kBatchChunk = 384;
+  if (B > 1 && p.chunk > kBatchChunk) {
+    const long long floor_rows = (static_cast<long long>(cap) + decode_max_chunks() - 1) / decode_max_chunks();
+    p.waves = 1;
+    p.chunk = static_cast<int32_t>(std::max<long long>(kBatchChunk, (floor_rows + 31) / 32 * 32));
   }
   p.n_chunks = (cap + p.chunk - 1) / p.chunk;
   return p;
@@ -139,9 +163,14 @@ size_t tb_workspace_bytes(int32_t op, int32_t B, int32_t Lmax, int32_t Hq, int32
           fail(TB_EINVAL, "tb_workspace_bytes(DECODE): bad sizes");
           return 0;
         }
-        // sized for the larger of the two dtype decompositions
-        return std::max(decode_ws(B, Hkv, Hq / Hkv, d, cap, true),
-                        decode_ws(B, Hkv, Hq / Hkv, d, cap, false));
+        // sized for the larger of the two dtype decompositions, and for every
+        // batch size up to B (the split depends on the batch size, so a caller
+        // that sizes for its largest batch can run any smaller one)
+        size_t need = 0;
+        for (int32_t b = 1; b <= B; ++b)
+          need = std::max({need, decode_ws(b, Hkv, Hq / Hkv, d, cap, true),
+                           decode_ws(b, Hkv, Hq / Hkv, d, cap, false)});
+        return need;
       }
       default:
         fail(TB_EINVAL, "tb_workspace_bytes: unknown op %d", op);

@@ -13,8 +13,8 @@
 //     rows [c*chunk, (c+1)*chunk) of KV head g of sequence b for all
 //     G = Hq/Hkv query heads of the group, so every K/V byte is read from HBM
 //     once per step, and writes one partial (m, l, o[G][d]).  A block has one
-//     wave (small caches: the wave stores its partial from registers) or four
-//     (each takes a quarter of the rows; the block combines them through LDS).
+//     wave (the wave stores its partial from registers) or 2, 4 or 8 (each
+//     takes an equal share of the rows; the block combines them through LDS).
 //   merge kernel, grid = (Hq, B): combines a query head's chunk partials by
 //     log-sum-exp in a fixed order, writes the output; the block of query
 //     head 0 advances kv_len[b].  One wave per query head when one round of
@@ -648,8 +648,13 @@ template <typename T, int D, int G, bool PAGED>
 hipError_t launch_both(const DecodeArgs& a, hipStream_t st) {
   const dim3 grid(a.n_chunks, a.Hkv, a.B);
   if constexpr (sizeof(T) == 2) {
-    if (a.waves == 1) decode_mfma_kernel<D, G, 1, PAGED><<<grid, 64, 0, st>>>(a);
-    else              decode_mfma_kernel<D, G, 4, PAGED><<<grid, 256, 0, st>>>(a);
+    switch (a.waves) {
+      case 1: decode_mfma_kernel<D, G, 1, PAGED><<<grid, 64, 0, st>>>(a); break;
+      case 2: decode_mfma_kernel<D, G, 2, PAGED><<<grid, 128, 0, st>>>(a); break;
+      case 4: decode_mfma_kernel<D, G, 4, PAGED><<<grid, 256, 0, st>>>(a); break;
+      case 8: decode_mfma_kernel<D, G, 8, PAGED><<<grid, 512, 0, st>>>(a); break;
+      default: return hipErrorInvalidValue;
+    }
   } else {
     decode_valu_kernel<D, G, PAGED><<<grid, kValuThreads, 0, st>>>(a);
   }

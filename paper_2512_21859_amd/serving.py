@@ -23,7 +23,7 @@ library calls; every computation runs in the kernels.
 """
 from __future__ import annotations
 
-from dataclasses import dataclass, field
+from dataclasses import dataclass
 from typing import Dict, List, Optional, Sequence
 
 import numpy as np
@@ -145,10 +145,9 @@ class Server:
         self.v_pool = torch.zeros((n_layers, n_pages, Hkv, d, PAGE), dtype=dtype, device=device)
         self.table = torch.zeros((max_seqs, max_pages), dtype=torch.int32, device=device)
         self.kv_len = torch.zeros((n_layers, max_seqs), dtype=torch.int32, device=device)
-        # the decode plan splits a small batch into more chunks, so the largest
-        # workspace need can come from any batch size up to max_seqs
-        dec = max(_lib.tb_workspace_bytes(_lib.TB_OP_DECODE, b, 0, Hq, Hkv, d, 0,
-                                          max_pages * PAGE) for b in range(1, max_seqs + 1))
+        # covers every batch size up to max_seqs
+        dec = _lib.tb_workspace_bytes(_lib.TB_OP_DECODE, max_seqs, 0, Hq, Hkv, d, 0,
+                                      max_pages * PAGE)
         self.dec_ws = torch.zeros((max(dec, 1),), dtype=torch.uint8, device=device)
         n = max_admit * Hkv * max_prompt
         self.scores_buf = torch.empty((n,), dtype=torch.float32, device=device)

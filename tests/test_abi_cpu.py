@@ -65,6 +65,17 @@ def test_workspace_sizes(lib):
     assert _lib.tb_workspace_bytes(9, 1, 1, 1, 1, 64, 1, 1) == 0
 
 
+def test_decode_workspace_covers_smaller_batches(lib):
+    """The decode split depends on the batch size; the reported workspace for B
+    covers every batch of at most B sequences, so it never shrinks as B grows."""
+    for Hq, Hkv, d in ((28, 4, 128), (32, 8, 128), (2, 1, 64)):
+        for cap in (32, 672, 2112, 8448, 16640, 32896, 131136):
+            sizes = [_lib.tb_workspace_bytes(_lib.TB_OP_DECODE, B, 0, Hq, Hkv, d, 0, cap)
+                     for B in range(1, 40)]
+            assert all(s > 0 for s in sizes)
+            assert sizes == sorted(sizes), (Hq, Hkv, d, cap)
+
+
 FAKE = ctypes.c_void_p(0x1000)     # never dereferenced: every call below fails validation
 
 
