@@ -62,6 +62,10 @@
 extern "C" {
 #endif
 
+/* Only the functions declared here are exported; the library is built with
+ * hidden visibility for everything else. */
+#pragma GCC visibility push(default)
+
 typedef enum {
   TB_OK = 0,
   TB_EINVAL = 1,        /* bad argument (null pointer, size, ratio, length) */
@@ -285,6 +289,8 @@ double tb_alpha_star(const double* prefill_abc, const double* step_pq, double n_
  * prefill_abc = {a, b, c}, predict_abc = {a_p, b_p, c_p}. */
 int64_t tb_predictor_length(const double* prefill_abc, const double* predict_abc,
                             double n_x, int64_t max_len);
+
+#pragma GCC visibility pop
 
 #ifdef __cplusplus
 }

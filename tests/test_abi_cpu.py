@@ -32,10 +32,12 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(_lib.EXPORTED), names
     nm = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True,
                         text=True, check=True).stdout
-    exported = set(re.findall(r" T (tb_[a-z0-9_]+)$", nm, re.M))
+    exported = set(re.findall(r" T (\S+)$", nm, re.M))
     for n in names:
         assert n in exported, f"{n} not exported"
         assert hasattr(lib, n)
+    # nothing else: internal code is built with hidden visibility
+    assert exported == set(names), sorted(exported - set(names))
 
 
 def test_keep_count_matches_oracle_and_table(lib):
