@@ -19,8 +19,10 @@
 // key 8(r/4) + 4t + r%4) so that lane group q of the S^T result holds keys
 // 8q .. 8q+7 of the step, exactly the P^T operand: the online softmax, the
 // bf16 packing of P and the rescale of O^T stay in the lane.  Softmax runs in
-// the base-2 domain with fp32 statistics; P is rounded to bf16 for the PV
-// product.
+// the base-2 domain with fp32 statistics (the running max on the raw dot
+// products, the scale folded into each exponent's FMA); P is rounded to bf16
+// for the PV product.  O^T is rescaled only in steps where some row's max
+// moved.
 
 #include "common.h"
 #include "kernels.h"
@@ -38,6 +40,25 @@ constexpr int kKPad = 8;                      // bf16 padding of a K row in LDS
 constexpr int kVPad = 8;                      // bf16 padding of a V^T row in LDS
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// max over the four 16-lane groups (lanes l, l^16, l^32, l^48) with the
+// row-swap permutes: a self-swap leaves each lane's value in one result and
+// its partner's in the other
+// (NaN-propagating maximum: one three-input instruction, no quieting of
+// the matrix-core results first)
+__device__ __forceinline__ float fmax2(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
+__device__ __forceinline__ float group_max(float x) {
+  const auto h = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmax2(__uint_as_float(h[0]), __uint_as_float(h[1]));
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmax2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// broadcast lane r16's value (lane group 0) to the lanes r16 + 16 q4
+__device__ __forceinline__ float from_group0(float x, int lane) {
+  return __shfl(x, lane & 15);
+}
 
 template <int D, int CQ>
 __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(CQ == 2 ? 2 : 1)))
@@ -76,18 +97,29 @@ void prefill_attn_kernel(PrefillArgs a) {
   }
 
   f32x4 accO[CQ][NC];
-  float m_run[CQ], l_part[CQ];                // running max (base-2 domain) / lane's share of the sum
+  // row sums of P on the matrix cores: a V^T tile whose row 0 is all ones, so
+  // the sum (of the same bf16-rounded P the numerator uses) lands in row 0 of
+  // accL: item 0 of the lanes of group 0
+  f32x4 accL[CQ];
+  float m_run[CQ];                            // running max of the raw dot products
+  // the window rows' normaliser is reported exact to fp32 (unrounded P), so
+  // the waves holding window rows also keep a vector-ALU sum
+  float l_part[CQ];
 #pragma unroll
   for (int cq = 0; cq < CQ; ++cq) {
 #pragma unroll
     for (int n = 0; n < NC; ++n) accO[cq][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    accL[cq] = f32x4{0.f, 0.f, 0.f, 0.f};
     m_run[cq] = -INFINITY;
     l_part[cq] = 0.f;
   }
+  const uint32_t one2 = r16 == 0 ? 0x3F803F80u : 0u;          // two bf16 ones
+  const u32x4 onesA = {one2, one2, one2, one2};
   const int krow0 = 8 * (r16 >> 2) + (r16 & 3);                // permuted K row of MFMA row r16
 
   const int key_end = min(L, (qt + 1) * kBlockRows);            // causal limit of the block
   const int wave_key_end = min(L, row0 + kRowsPerWave);         // causal limit of this wave
+  const bool stats_wave = a.window_stats != nullptr && row0 + kRowsPerWave > L - a.w;
 
   // Staging of 64 keys, fetched into registers one stage ahead.  K: thread =
   // (key tid/4, quarter tid%4 of d), rows copied as they are.  V: thread
@@ -171,41 +203,54 @@ void prefill_attn_kernel(PrefillArgs a) {
             acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kA[t][kc]), as_bf16x8(qB[cq][kc]), acc, 0, 0, 0);
           S[t] = acc;
         }
-        // lane holds keys base + 8 q4 + j (j = 4t + i) of query row0 + 16 cq + r16
+        // lane holds keys base + 8 q4 + j (j = 4t + i) of query row0 + 16 cq + r16;
+        // the running max is kept on the raw dot products (the scale is
+        // positive) and the scale enters each exponent through one FMA
         const int qi = row0 + 16 * cq + r16;
         float s[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) s[j] = S[j >> 2][j & 3] * a.scale_log2;
+        for (int j = 0; j < 8; ++j) s[j] = S[j >> 2][j & 3];
         if (need_mask) {
 #pragma unroll
           for (int j = 0; j < 8; ++j)
             if (base + 8 * q4 + j > qi) s[j] = -INFINITY;
         }
-        float mt = s[0];
-#pragma unroll
-        for (int j = 1; j < 8; ++j) mt = fmaxf(mt, s[j]);
-        mt = fmaxf(mt, __shfl_xor(mt, 16));
-        mt = fmaxf(mt, __shfl_xor(mt, 32));
-        const float m_new = fmaxf(m_run[cq], mt);
-        // every query sees key 0, so m_new is finite once its first step is done;
-        // a step entirely past a query's diagonal leaves it -inf only before that
-        const float corr = m_new == -INFINITY ? 1.f : exp2f(m_run[cq] - m_new);
+        float mt = fmax2(fmax2(fmax2(s[0], s[1]), fmax2(s[2], s[3])),
+                         fmax2(fmax2(s[4], s[5]), fmax2(s[6], s[7])));
+        mt = group_max(mt);
+        // finite: every wave's first step holds key 0, which no query masks
+        const float m_new = fmax2(m_run[cq], mt);
+        const float mc = m_new * a.scale_log2;
+        // 1 when the max did not move; 0 on the first step (m_run = -inf)
+        const float corr = __builtin_amdgcn_exp2f((m_run[cq] - m_new) * a.scale_log2);
         m_run[cq] = m_new;
         bf16x8 pB;
-        float psum = 0.f;
+        float p[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const float p = m_new == -INFINITY ? 0.f : exp2f(s[j] - m_new);
-          psum += p;
-          pB[j] = static_cast<__bf16>(p);
+          // hardware exp2: results below 2^-126 flush to zero, far below a
+          // softmax term that can matter next to the row max's term of 1
+          p[j] = __builtin_amdgcn_exp2f(fmaf(s[j], a.scale_log2, -mc));
+          pB[j] = static_cast<__bf16>(p[j]);
         }
-        l_part[cq] = l_part[cq] * corr + psum;
+        if (stats_wave) {                                     // wave-uniform
+          float psum = 0.f;
 #pragma unroll
-        for (int n = 0; n < NC; ++n) {
+          for (int j = 0; j < 8; ++j) psum += p[j];
+          l_part[cq] = l_part[cq] * corr + psum;
+        }
+        // rescaling by exactly 1 changes nothing: skip it unless some lane's max moved
+        if (__builtin_amdgcn_ballot_w64(corr != 1.f)) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) accO[cq][n][i] *= corr;
+          for (int n = 0; n < NC; ++n)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) accO[cq][n][i] *= corr;
+          accL[cq][0] *= corr;
+        }
+        accL[cq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(onesA), pB, accL[cq], 0, 0, 0);
+#pragma unroll
+        for (int n = 0; n < NC; ++n)
           accO[cq][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vA[n]), pB, accO[cq][n], 0, 0, 0);
-        }
       }
     }
   }
@@ -214,8 +259,12 @@ void prefill_attn_kernel(PrefillArgs a) {
   uint16_t* outh = static_cast<uint16_t*>(a.out) + (static_cast<size_t>(b) * a.Hq + h) * a.Lmax * D;
 #pragma unroll
   for (int cq = 0; cq < CQ; ++cq) {
-    float l_tot = l_part[cq] + __shfl_xor(l_part[cq], 16);
-    l_tot += __shfl_xor(l_tot, 32);
+    const float l_tot = from_group0(accL[cq][0], lane);      // sum of the P the numerator used
+    float z = 0.f;                                            // unrounded sum (window waves)
+    if (stats_wave) {
+      z = l_part[cq] + __shfl_xor(l_part[cq], 16);
+      z += __shfl_xor(z, 32);
+    }
     const int qi = row0 + 16 * cq + r16;
     if (qi < L) {
       const float inv = 1.f / l_tot;
@@ -227,10 +276,10 @@ void prefill_attn_kernel(PrefillArgs a) {
             bf16x4{static_cast<__bf16>(accO[cq][n][0] * inv), static_cast<__bf16>(accO[cq][n][1] * inv),
                    static_cast<__bf16>(accO[cq][n][2] * inv), static_cast<__bf16>(accO[cq][n][3] * inv)};
       // window rows: row max (natural-log units) and normaliser of the softmax
-      if (a.window_stats && q4 == 0 && qi >= L - a.w) {
+      if (stats_wave && q4 == 0 && qi >= L - a.w) {
         float* ws = a.window_stats + ((static_cast<size_t>(b) * a.Hq + h) * a.w + (qi - (L - a.w))) * 2;
-        ws[0] = m_run[cq] * 0.69314718055994531f;          // base-2 max -> natural units
-        ws[1] = l_tot;
+        ws[0] = m_run[cq] * a.scale_log2 * 0.69314718055994531f;   // raw max -> natural units
+        ws[1] = z;
       }
     }
   }
