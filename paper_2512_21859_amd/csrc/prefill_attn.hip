@@ -36,7 +36,6 @@ typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 constexpr int kWaves = 4;
 constexpr int kStage = 64;                    // keys per LDS stage
-constexpr int kKPad = 8;                      // bf16 padding of a K row in LDS
 constexpr int kVPad = 8;                      // bf16 padding of a V^T row in LDS
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -53,6 +52,17 @@ __device__ __forceinline__ float group_max(float x) {
   x = fmax2(__uint_as_float(h[0]), __uint_as_float(h[1]));
   const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return fmax2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// K rows sit in LDS unpadded, their 16-byte chunks permuted by row: chunk c
+// of row R is stored at c ^ kswz(R).  A K-operand read has 16 lanes take one
+// chunk index from the rows {0-3, 8-11, 16-19, 24-27} (+4 t) of the permuted
+// tile; the swizzle sends those 16 rows to 16 different bank groups (with a
+// padded stride rows R and R+16 shared banks: a 2-way conflict on every read).
+template <int D>
+__device__ __forceinline__ int kswz(int R) {
+  if constexpr (D == 128) return (R & 3) | ((R >> 1) & 12);          // 16 chunks per row
+  else return ((R >> 1) & 1) | ((R >> 2) & 6);                       // 8 chunks; rows pair up in 256 B
 }
 
 // broadcast lane r16's value (lane group 0) to the lanes r16 + 16 q4
@@ -77,7 +87,7 @@ void prefill_attn_kernel(PrefillArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q4 = lane >> 4, r16 = lane & 15;
 
-  __shared__ uint16_t s_k[kStage][D + kKPad];
+  __shared__ uint16_t s_k[kStage][D];
   __shared__ uint16_t s_vt[D][kStage + kVPad];
 
   const uint16_t* qh = static_cast<const uint16_t*>(a.q) + (static_cast<size_t>(b) * a.Hq + h) * a.Lmax * D;
@@ -150,7 +160,7 @@ void prefill_attn_kernel(PrefillArgs a) {
   auto stage = [&]() {
 #pragma unroll
     for (int e = 0; e < KQ / 8; ++e)
-      *reinterpret_cast<u32x4*>(&s_k[kr][kpart * KQ + 8 * e]) = kreg[e];
+      *reinterpret_cast<u32x4*>(&s_k[kr][8 * ((kpart * (KQ / 8) + e) ^ kswz<D>(kr))]) = kreg[e];
     if (tid < VTASKS) {
       const int k4 = tid % (kStage / 4), d8 = tid / (kStage / 4);
       // vreg[j] holds d = 8 d8 .. +7 of key 4 k4 + j (two bf16 per dword);
@@ -184,8 +194,10 @@ void prefill_attn_kernel(PrefillArgs a) {
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int kc = 0; kc < KC; ++kc)
-          kA[t][kc] = *reinterpret_cast<const u32x4*>(&s_k[32 * sub + krow0 + 4 * t][32 * kc + 8 * q4]);
+        for (int kc = 0; kc < KC; ++kc) {
+          const int R = 32 * sub + krow0 + 4 * t;
+          kA[t][kc] = *reinterpret_cast<const u32x4*>(&s_k[R][8 * ((4 * kc + q4) ^ kswz<D>(R))]);
+        }
       // V^T operands: d = 16 n + r16, keys 8 q4 .. +8 of the step
       u32x4 vA[NC];
 #pragma unroll
