@@ -98,7 +98,9 @@ def measured_traffic():
 
 def cpu_baseline(wl, pr, dc, min_seconds):
     """The float64 oracle on this host: whole passes of the step (eviction and
-    every decode step at each ratio), repeated until min_seconds have passed."""
+    every decode step at each ratio), repeated until min_seconds have passed,
+    with the time of each stage (scores, selection, compaction, decode)."""
+    import numpy as np
     from oracle import timebill_oracle as O
     try:
         from threadpoolctl import threadpool_info
@@ -111,22 +113,43 @@ def cpu_baseline(wl, pr, dc, min_seconds):
     qs = dc["q"][:, 0].double().numpy()
     kn = dc["k_new"][:, 0].double().numpy()
     vn = dc["v_new"][:, 0].double().numpy()
+    L, w, pool = wl.L, wl.w, wl.pool
+    stage = {"score": 0.0, "select": 0.0, "compact": 0.0, "decode": 0.0}
     tokens, passes = 0, 0
     t0 = time.perf_counter()
     while True:
         for a in wl.alphas:
-            r = O.evict_sequence(q64, k64, v64, wl.L, wl.w, wl.pool, a)
-            O.decode_sequence(qs, kn, vn, r["k_cache"], r["v_cache"])
+            c0 = time.perf_counter()
+            pooled = O.max_pool(O.window_scores(q64, k64, L, w), pool)
+            c1 = time.perf_counter()
+            nk = O.keep_count(L, a, w)
+            keep = [O.select_keep(pooled[g], L, w, nk) for g in range(k64.shape[0])]
+            c2 = time.perf_counter()
+            kc = np.stack([O.compact(k64[g], v64[g], keep[g])[0] for g in range(len(keep))])
+            vc = np.stack([O.compact(k64[g], v64[g], keep[g])[1] for g in range(len(keep))])
+            c3 = time.perf_counter()
+            O.decode_sequence(qs, kn, vn, kc, vc)
+            c4 = time.perf_counter()
+            stage["score"] += c1 - c0
+            stage["select"] += c2 - c1
+            stage["compact"] += c3 - c2
+            stage["decode"] += c4 - c3
             tokens += wl.T
         passes += 1
         wall = time.perf_counter() - t0
         if wall >= min_seconds:
             break
+    n = passes * len(wl.alphas)
     return {"value": tokens / wall, "unit": "tokens/s", "cores": int(threads),
             "kind": "oracle",
+            "stage_ms": {"score_per_eviction": round(stage["score"] / n * 1e3, 2),
+                         "select_per_eviction": round(stage["select"] / n * 1e3, 2),
+                         "compact_per_eviction": round(stage["compact"] / n * 1e3, 2),
+                         "decode_per_step": round(stage["decode"] / (n * wl.T) * 1e3, 3)},
             "sample": (f"float64 numpy oracle on the host: {passes} whole pass(es) of the step "
                        f"(eviction plus all {wl.T} decode steps at each of the "
-                       f"{len(wl.alphas)} ratios), {wall:.1f} s of CPU work")}
+                       f"{len(wl.alphas)} ratios), {wall:.1f} s of CPU work; stage times "
+                       f"averaged over the {n} evictions")}
 
 
 def long_context(torch, _lib, synth, Evictor, dev, steps=64, alpha=0.5):
@@ -206,22 +229,41 @@ def _best_ms(torch, fn, reps=3, stream=None):
 
 
 def hbm_ceiling(torch, dev, nbytes=2 << 30):
-    """Practical bandwidth ceilings over 2 GiB buffers: a streaming read (a
-    library sum) and a device-to-device copy, best of 5."""
+    """Practical bandwidth ceilings over 2 GiB buffers, best of 5: a streaming
+    read (the benchmark's own probe kernel, libtbbench.so: 16-byte
+    nontemporal loads, grid sizes 1-16 blocks per CU tried) and a
+    device-to-device copy (torch copy_)."""
+    import ctypes
     x = torch.ones((nbytes // 4,), dtype=torch.float32, device=dev)
     y = torch.empty_like(x)
-    x.sum()
     y.copy_(x)
     torch.cuda.synchronize()
-    rd = _best_ms(torch, lambda: x.sum(), reps=5)
     cp = _best_ms(torch, lambda: y.copy_(x), reps=5)
-    del x, y
+    del y
+    probe = ctypes.CDLL(os.path.join(ROOT, "paper_2512_21859_amd", "libtbbench.so"))
+    probe.tbb_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                      ctypes.c_int, ctypes.c_void_p]
+    probe.tbb_stream_read.restype = ctypes.c_int
+    sink = torch.zeros((16 * 256,), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    rd_best, rd_blocks = float("inf"), 0
+    for blocks in (256, 512, 1024, 2048, 4096):
+        def run():
+            if probe.tbb_stream_read(x.data_ptr(), nbytes, sink.data_ptr(), blocks,
+                                     stream.cuda_stream) != 0:
+                raise RuntimeError("stream-read probe failed")
+        run()
+        t = _best_ms(torch, run, reps=5)
+        if t < rd_best:
+            rd_best, rd_blocks = t, blocks
+    del x, sink
     torch.cuda.empty_cache()
-    return {"read_GBps": round(nbytes / (rd * 1e-3) / 1e9, 1),
+    return {"read_GBps": round(nbytes / (rd_best * 1e-3) / 1e9, 1),
+            "read_blocks": rd_blocks,
             "copy_GBps": round(2 * nbytes / (cp * 1e-3) / 1e9, 1),
             "bytes": nbytes,
-            "how": "torch sum (read) and copy_ (read + write) over 2 GiB fp32 buffers, "
-                   "HIP events, best of 5"}
+            "how": "streaming-read probe kernel (16-byte nontemporal loads, best grid) and "
+                   "torch copy_ (read + write) over 2 GiB buffers, HIP events, best of 5"}
 
 
 def cold_decode(torch, _lib, Evictor, dev, wl, q_win, k, v, qd, knd, vnd,
@@ -730,6 +772,9 @@ def main():
         ev_ms.sort()
         de_ms.sort()
         e_med, d_med = ev_ms[len(ev_ms) // 2], de_ms[len(de_ms) // 2]
+
+        def pct(xs, q):
+            return xs[min(len(xs) - 1, int(q * (len(xs) - 1) + 0.5))]
         nk = n_keep[a]
         dbytes = sum(_decode_bytes(Hq, Hkv, d, nk + t + 1) for t in range(T))
         ebytes = _evict_bytes(Hq, Hkv, d, L, w, nk)
@@ -739,7 +784,10 @@ def main():
         per_alpha.append({
             "alpha": a, "n_keep": nk,
             "evict_us": round(e_med * 1e3, 2),
+            "evict_us_p10_p90": [round(pct(ev_ms, 0.1) * 1e3, 2), round(pct(ev_ms, 0.9) * 1e3, 2)],
             "decode_us_per_token": round(d_med * 1e3 / T, 3),
+            "decode_us_per_token_p10_p90": [round(pct(de_ms, 0.1) * 1e3 / T, 3),
+                                            round(pct(de_ms, 0.9) * 1e3 / T, 3)],
             "decode_GBps": round(dbytes / (d_med * 1e-3) / 1e9, 1),
             "evict_plus_decode_GBps": round((dbytes + ebytes) / ((d_med + e_med) * 1e-3) / 1e9, 1),
             "tokens_per_s": round(T / ((d_med + e_med) * 1e-3), 1),
@@ -796,6 +844,8 @@ def main():
                       "divided by the launch count (inter-kernel gaps included)",
         },
         "per_alpha": per_alpha,
+        "per_alpha_timing": "median over the timed steps (p10, p90 beside it) of HIP events "
+                            "around each ratio's eviction and its graph of decode launches",
         "decode_time_fit": {"p_us_per_kv_row": slope, "q_us": icpt,
                             "r2": 1 - ss_res / ss_tot if ss_tot > 0 else 1.0,
                             "mape_pct": mape,

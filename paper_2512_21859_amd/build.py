@@ -16,6 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libtimebill.so")
+BENCH_LIB = os.path.join(HERE, "libtbbench.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -52,6 +53,15 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}")
+    # the benchmark's bandwidth probe: a separate library, not part of the ABI
+    bsrc = os.path.join(HERE, "bench_csrc", "stream_read.hip")
+    bobj = os.path.join(BUILD, "stream_read.o")
+    _run([HIPCC, *COMMON_FLAGS, "-c", bsrc, "-o", bobj])
+    tmp = BENCH_LIB + ".tmp"
+    _run([HIPCC, "-shared", f"--offload-arch={ARCH}", "-o", tmp, bobj])
+    os.replace(tmp, BENCH_LIB)
+    if verbose:
+        print(f"built {BENCH_LIB}")
     return LIB
 
 
