@@ -292,10 +292,10 @@ __global__ __launch_bounds__(kThreads) void score_accum_kernel(ScoreArgs a) {
   if (j0 >= pref) return;
   const int R = a.R;
   const size_t bg = static_cast<size_t>(b) * a.Hkv + g;
-  const int tid = threadIdx.x, col = tid & 63, rg = tid >> 6;
+  const int tid = threadIdx.x;
 
   __shared__ double coef[1024];
-  __shared__ double part[4][kT];
+  __shared__ double part[16][kT];
 
   for (int r = tid; r < R; r += kThreads) {
     const double m = a.tile_m[(bg * R + r) * a.n_tiles + ct];
@@ -303,29 +303,44 @@ __global__ __launch_bounds__(kThreads) void score_accum_kernel(ScoreArgs a) {
     coef[r] = (m != -INFINITY && Z > 0.0) ? exp(m - M) / Z : 0.0;
   }
   __syncthreads();
-
-  // key col of a tile row is stored at 4 (col % 16) + col / 16
-  const float* et = a.e + (bg * a.n_tiles + ct) * static_cast<size_t>(R) * kT +
-                    4 * (col & 15) + (col >> 4);
+  // Key col of a tile row is stored at 4 (col % 16) + col / 16, so the 16-byte
+  // vector at 4 q holds cols q, q + 16, q + 32, q + 48.  Thread (q, rs) reads
+  // those vectors from rows rs, rs + 16, ..., eight loads in flight, and keeps
+  // four float64 column sums; the 16 row phases are then added in order.
+  // (Sixteen loads in flight, issued before the coefficients, measured slower.)
+  const int q = tid & 15, rs = tid >> 4;
+  const float* et = a.e + (bg * a.n_tiles + ct) * static_cast<size_t>(R) * kT + 4 * q;
   double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-  int r = rg;
-  for (; r + 12 < R; r += 16) {
-    const float e0 = et[static_cast<size_t>(r) * kT];
-    const float e1 = et[static_cast<size_t>(r + 4) * kT];
-    const float e2 = et[static_cast<size_t>(r + 8) * kT];
-    const float e3 = et[static_cast<size_t>(r + 12) * kT];
-    s0 = fma(static_cast<double>(e0), coef[r], s0);
-    s1 = fma(static_cast<double>(e1), coef[r + 4], s1);
-    s2 = fma(static_cast<double>(e2), coef[r + 8], s2);
-    s3 = fma(static_cast<double>(e3), coef[r + 12], s3);
+  constexpr int kBatch = 8;
+  for (int rb = rs; rb < R; rb += 16 * kBatch) {
+    float4 v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int r = rb + 16 * u;
+      v[u] = r < R ? *reinterpret_cast<const float4*>(et + static_cast<size_t>(r) * kT)
+                   : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int r = rb + 16 * u;
+      const double c = r < R ? coef[r] : 0.0;
+      s0 = fma(static_cast<double>(v[u].x), c, s0);
+      s1 = fma(static_cast<double>(v[u].y), c, s1);
+      s2 = fma(static_cast<double>(v[u].z), c, s2);
+      s3 = fma(static_cast<double>(v[u].w), c, s3);
+    }
   }
-  for (; r < R; r += 4) s0 = fma(static_cast<double>(et[static_cast<size_t>(r) * kT]), coef[r], s0);
-  part[rg][col] = (s0 + s1) + (s2 + s3);
+  part[rs][q] = s0;
+  part[rs][q + 16] = s1;
+  part[rs][q + 32] = s2;
+  part[rs][q + 48] = s3;
   __syncthreads();
   if (tid < kT) {
     const int j = j0 + tid;
     if (j < pref) {
-      const double A = ((part[0][tid] + part[1][tid]) + part[2][tid]) + part[3][tid];
+      double A = part[0][tid];
+#pragma unroll
+      for (int k = 1; k < 16; ++k) A += part[k][tid];
       a.raw[bg * a.Lmax + j] = static_cast<float>(A);
     }
   }
