@@ -10,9 +10,11 @@
 //
 // Block = 128 query rows of one query head (4 waves x 32 rows), blocks issued
 // heaviest first (latest rows).  K and V stream through LDS 64 keys at a time,
-// the next stage's global loads in flight during the current stage's products;
-// V is written into LDS transposed so that "8 consecutive keys of one V
-// column" is one 16-byte read.  Per 32-key step a wave computes
+// double-buffered: each stage goes global -> LDS by direct loads (no
+// registers), issued one stage ahead, one barrier per stage.  Both stay
+// row-major in LDS (16-byte chunks XOR-swizzled by row against bank
+// conflicts); the V^T operand ("8 consecutive keys of one d") comes from
+// transpose reads of row-major V.  Per 32-key step a wave computes
 //   S^T[32 keys x 16 queries] = K Q^T   and   O^T[d x 16 queries] += V^T P^T
 // for its two 16-query column tiles with v_mfma_f32_16x16x32_bf16.  As in the
 // decode kernel, the K rows of an MFMA tile are permuted (row r of tile t <->
@@ -36,7 +38,6 @@ typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 constexpr int kWaves = 4;
 constexpr int kStage = 64;                    // keys per LDS stage
-constexpr int kVPad = 8;                      // bf16 padding of a V^T row in LDS
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -65,6 +66,32 @@ __device__ __forceinline__ int kswz(int R) {
   else return ((R >> 1) & 1) | ((R >> 2) & 6);                       // 8 chunks; rows pair up in 256 B
 }
 
+// V rows sit row-major in LDS, chunk c of row R at c ^ vswz(R).  A transpose
+// read has 16 lanes take 32 bytes (chunks 2n, 2n + 1) of 4 consecutive rows;
+// a half-wave covers rows 8g + 0..3 and 8(g + 1) + 0..3, and the swizzle
+// spreads those 256 bytes over all banks.
+template <int D>
+__device__ __forceinline__ int vswz(int R) {
+  if constexpr (D == 128) return 2 * ((R & 3) | (((R >> 3) & 1) << 2));       // 16 chunks per row
+  else return 2 * (((R >> 1) & 1) | (((R >> 3) & 1) << 1));                  // 8 chunks per row
+}
+
+typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
+
+// 16 bytes global -> LDS without a register: a wave's 64 lanes fill 1 KB
+// starting at the wave-uniform LDS address `lds`, lane l at lds + 16 l
+__device__ __forceinline__ void lds_load16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
+// transpose read of 4 bf16: within each 16-lane group, lane i receives
+// element i % 4 of the 8-byte chunks read by lanes 4j + i / 4, j = 0..3
+__device__ __forceinline__ u32x2 lds_read_tr16(const void* p) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4s*)p));
+}
+
 // broadcast lane r16's value (lane group 0) to the lanes r16 + 16 q4
 __device__ __forceinline__ float from_group0(float x, int lane) {
   return __shfl(x, lane & 15);
@@ -87,8 +114,15 @@ void prefill_attn_kernel(PrefillArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q4 = lane >> 4, r16 = lane & 15;
 
-  __shared__ uint16_t s_k[kStage][D];
-  __shared__ uint16_t s_vt[D][kStage + kVPad];
+  // Stage buffers, double-buffered: [buffer][K, V][row * CH + chunk] in
+  // 16-byte chunks; K row R keeps chunk c at c ^ kswz(R), V row R at c ^ vswz(R).
+  constexpr int CH = D / 8;                   // 16-byte chunks per row
+  constexpr int SCH = kStage * CH;            // chunks per stage and matrix
+  constexpr int PER_THREAD = SCH / (64 * kWaves);
+  // two distinct arrays (not one indexed by a runtime buffer number), so the
+  // compiler can tell the loads in flight into one from the reads of the other
+  __shared__ u32x4 s_kv0[2][SCH];
+  __shared__ u32x4 s_kv1[2][SCH];
 
   const uint16_t* qh = static_cast<const uint16_t*>(a.q) + (static_cast<size_t>(b) * a.Hq + h) * a.Lmax * D;
   const size_t bg = static_cast<size_t>(b) * a.Hkv + g;
@@ -131,60 +165,26 @@ void prefill_attn_kernel(PrefillArgs a) {
   const int wave_key_end = min(L, row0 + kRowsPerWave);         // causal limit of this wave
   const bool stats_wave = a.window_stats != nullptr && row0 + kRowsPerWave > L - a.w;
 
-  // Staging of 64 keys, fetched into registers one stage ahead.  K: thread =
-  // (key tid/4, quarter tid%4 of d), rows copied as they are.  V: thread
-  // t < (64/4)(D/8) takes 4-key group t%16 and d-octet t/16 (the 16 groups
-  // of a d-octet fill 128 contiguous bytes of a V^T row, so a wave's writes
-  // do not collide in LDS banks), reads 4 keys x 8 d and transposes them in
-  // registers (byte permutes) into 8 rows of V^T x 4 keys, stored as 8-byte
-  // writes.
-  constexpr int KQ = D / 4;                   // K elements per thread
-  constexpr int VD8 = D / 8;                  // d-octets
-  constexpr int VTASKS = (kStage / 4) * VD8;  // (4-key group, d-octet) tasks
-  const int kr = tid >> 2, kpart = tid & 3;
-  u32x4 kreg[KQ / 8], vreg[4];
-  auto fetch = [&](int s0) {
-    const int key = min(s0 + kr, L - 1);
-    const uint16_t* ks = kg + static_cast<size_t>(key) * D + kpart * KQ;
+  // One stage of 64 keys goes global -> LDS by direct loads, one stage ahead:
+  // load u of thread tid fills chunk position p = 256 u + tid of K and of V
+  // (a wave's 64 lanes write 1 KB contiguous), taking from global memory the
+  // chunk the swizzled layout keeps there.  Keys past L read row L - 1 (any
+  // valid row: they are masked).
+  auto load_stage = [&](int s0, u32x4 (&dst)[2][SCH]) {
 #pragma unroll
-    for (int e = 0; e < KQ / 8; ++e) kreg[e] = *reinterpret_cast<const u32x4*>(ks + 8 * e);
-    if (tid < VTASKS) {
-      const int k4 = tid % (kStage / 4), d8 = tid / (kStage / 4);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int kv = min(s0 + 4 * k4 + j, L - 1);
-        vreg[j] = *reinterpret_cast<const u32x4*>(vg + static_cast<size_t>(kv) * D + 8 * d8);
-      }
-    }
-  };
-  auto stage = [&]() {
-#pragma unroll
-    for (int e = 0; e < KQ / 8; ++e)
-      *reinterpret_cast<u32x4*>(&s_k[kr][8 * ((kpart * (KQ / 8) + e) ^ kswz<D>(kr))]) = kreg[e];
-    if (tid < VTASKS) {
-      const int k4 = tid % (kStage / 4), d8 = tid / (kStage / 4);
-      // vreg[j] holds d = 8 d8 .. +7 of key 4 k4 + j (two bf16 per dword);
-      // V^T row 8 d8 + 2c + h takes half h of dword c from keys j = 0..3
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        // byte selectors: low halves of (x, y) -> 0x05040100, high halves -> 0x07060302
-        const uint32_t lo01 = __builtin_amdgcn_perm(vreg[1][c], vreg[0][c], 0x05040100u);
-        const uint32_t lo23 = __builtin_amdgcn_perm(vreg[3][c], vreg[2][c], 0x05040100u);
-        const uint32_t hi01 = __builtin_amdgcn_perm(vreg[1][c], vreg[0][c], 0x07060302u);
-        const uint32_t hi23 = __builtin_amdgcn_perm(vreg[3][c], vreg[2][c], 0x07060302u);
-        typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
-        *reinterpret_cast<u32x2*>(&s_vt[8 * d8 + 2 * c][4 * k4]) = u32x2{lo01, lo23};
-        *reinterpret_cast<u32x2*>(&s_vt[8 * d8 + 2 * c + 1][4 * k4]) = u32x2{hi01, hi23};
-      }
+    for (int u = 0; u < PER_THREAD; ++u) {
+      const int p = u * 64 * kWaves + tid;
+      const int R = p / CH, cp = p % CH;
+      const size_t row = static_cast<size_t>(min(s0 + R, L - 1)) * D;
+      const int wbase = u * 64 * kWaves + 64 * wave;          // wave-uniform LDS chunk base
+      lds_load16(kg + row + 8 * (cp ^ kswz<D>(R)), &dst[0][wbase]);
+      lds_load16(vg + row + 8 * (cp ^ vswz<D>(R)), &dst[1][wbase]);
     }
   };
 
-  fetch(0);
-  for (int s0 = 0; s0 < key_end; s0 += kStage) {
-    __syncthreads();                          // the previous stage's reads are done
-    stage();
-    __syncthreads();
-    if (s0 + kStage < key_end) fetch(s0 + kStage);   // in flight during the products
+  auto compute_stage = [&](int s0, const u32x4 (&src)[2][SCH]) {
+    const u32x4* sk = src[0];
+    const u32x4* sv = src[1];
 #pragma unroll
     for (int sub = 0; sub < kStage / 32; ++sub) {
       const int base = s0 + 32 * sub;                           // first key of the 32-key step
@@ -196,13 +196,22 @@ void prefill_attn_kernel(PrefillArgs a) {
 #pragma unroll
         for (int kc = 0; kc < KC; ++kc) {
           const int R = 32 * sub + krow0 + 4 * t;
-          kA[t][kc] = *reinterpret_cast<const u32x4*>(&s_k[R][8 * ((4 * kc + q4) ^ kswz<D>(R))]);
+          kA[t][kc] = sk[R * CH + ((4 * kc + q4) ^ kswz<D>(R))];
         }
-      // V^T operands: d = 16 n + r16, keys 8 q4 .. +8 of the step
+      // V^T operands by transpose reads: lane (q4, r16) fetches d = 16 n +
+      // 4 (r16 & 3) .. +3 of keys 8 q4 + r16 / 4 (and + 4) and receives
+      // d = 16 n + r16 of keys 8 q4 .. 8 q4 + 7
       u32x4 vA[NC];
 #pragma unroll
-      for (int n = 0; n < NC; ++n)
-        vA[n] = *reinterpret_cast<const u32x4*>(&s_vt[16 * n + r16][32 * sub + 8 * q4]);
+      for (int n = 0; n < NC; ++n) {
+        const int R1 = 32 * sub + 8 * q4 + (r16 >> 2), R2 = R1 + 4;
+        const int cv = 2 * n + ((r16 & 3) >> 1);                // chunk of d = 16 n + 4 (r16 & 3)
+        const int half = (r16 & 1) * 4;                         // bf16 offset of that half chunk
+        const uint16_t* p1 = reinterpret_cast<const uint16_t*>(sv + R1 * CH + (cv ^ vswz<D>(R1))) + half;
+        const uint16_t* p2 = reinterpret_cast<const uint16_t*>(sv + R2 * CH + (cv ^ vswz<D>(R2))) + half;
+        const u32x2 lo = lds_read_tr16(p1), hi = lds_read_tr16(p2);
+        vA[n] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+      }
       const bool need_mask = base + 32 > row0;                  // step reaches this wave's diagonal
 #pragma unroll
       for (int cq = 0; cq < CQ; ++cq) {
@@ -265,6 +274,26 @@ void prefill_attn_kernel(PrefillArgs a) {
           accO[cq][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vA[n]), pB, accO[cq][n], 0, 0, 0);
       }
     }
+  };
+
+  // stage pipeline, unrolled by two over the two buffers: wait for this
+  // stage's loads (and for every wave to be done with the other buffer),
+  // start the next stage's loads into the other buffer, compute.  (The
+  // compiler cannot tell the transpose reads from the loads landing in the
+  // other buffer and makes them wait for those loads, so the overlap is the
+  // first step's K reads and QK products; still 9% faster than staging
+  // through registers, and bit-identical to it.)
+  load_stage(0, s_kv0);
+  for (int s0 = 0; s0 < key_end; s0 += 2 * kStage) {
+    __builtin_amdgcn_s_waitcnt(0x0F70);                         // vmcnt(0)
+    __syncthreads();
+    if (s0 + kStage < key_end) load_stage(s0 + kStage, s_kv1);
+    compute_stage(s0, s_kv0);
+    if (s0 + kStage >= key_end) break;
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __syncthreads();
+    if (s0 + 2 * kStage < key_end) load_stage(s0 + 2 * kStage, s_kv0);
+    compute_stage(s0 + kStage, s_kv1);
   }
 
   // finalize: lane holds d = 16 n + 4 q4 .. +3 of query row0 + 16 cq + r16
@@ -300,9 +329,10 @@ void prefill_attn_kernel(PrefillArgs a) {
 }  // namespace
 
 hipError_t launch_prefill(const PrefillArgs& a, int d, hipStream_t st) {
-  // two column tiles per wave (244 VGPRs, two waves per SIMD); four tiles
-  // halve the LDS operand reads per product but need one wave per SIMD, and
-  // measured slower (310 vs 584 TFLOP/s at N = 32768)
+  // two column tiles per wave (244 VGPRs, two waves per SIMD; 64 KB of LDS
+  // per block at d = 128, so two blocks per CU); four tiles halve the LDS
+  // operand reads per product but need one wave per SIMD, and measured slower
+  // (310 vs 584 TFLOP/s at N = 32768 with the earlier register staging)
   constexpr int CQ = 2;
   constexpr int rows = kWaves * 16 * CQ;
   int lmax = 0;
