@@ -96,8 +96,10 @@ def make_prompt(wl: Workload, layer: int = 0, L: Optional[List[int]] = None,
                 pad_value: float = 0.0):
     """Window queries and prompt K/V of one layer.
 
-    Returns dict(q_win [B,Hq,w,d], k [B,Hkv,Lmax,d], v [B,Hkv,Lmax,d], L list),
-    CPU tensors in the workload dtype.  Rows j >= L[b] hold ``pad_value``.
+    Returns dict(q_win [B,Hq,w,d], k [B,Hkv,Lmax,d], v [B,Hkv,Lmax,d], L list,
+    heavy), CPU tensors in the workload dtype; heavy[b][g] lists the planted
+    heavy-hitter positions (empty without structure).  Rows j >= L[b] hold
+    ``pad_value``.
     """
     if L is None:
         L, _ = lengths_and_alphas(wl)
@@ -108,6 +110,7 @@ def make_prompt(wl: Workload, layer: int = 0, L: Optional[List[int]] = None,
     k = torch.full((B, Hkv, Lmax, d), pad_value, dtype=torch.float32)
     v = torch.full((B, Hkv, Lmax, d), pad_value, dtype=torch.float32)
     q_win = torch.empty((B, Hq, w, d), dtype=torch.float32)
+    heavy = [[[] for _ in range(Hkv)] for _ in range(B)]
     for b in range(B):
         n = L[b]
         k[b, :, :n] = torch.randn((Hkv, n, d), generator=g0)
@@ -123,6 +126,7 @@ def make_prompt(wl: Workload, layer: int = 0, L: Optional[List[int]] = None,
                 u = u / u.norm()
                 pos = torch.randperm(n - w, generator=g1)[:n_heavy]
                 k[b, gk, pos] += (2.0 * math.sqrt(d)) * u
+                heavy[b][gk] = sorted(pos.tolist())
         elif wl.heavy == "aligned":
             # keys replaced by 4 sqrt(d) times the unit mean of the group's window queries
             qr = q_win[b].to(wl.dtype).to(torch.float32)
@@ -132,8 +136,9 @@ def make_prompt(wl: Workload, layer: int = 0, L: Optional[List[int]] = None,
                 u = c / c.norm()
                 pos = torch.randperm(n - w, generator=g1)[:n_heavy]
                 k[b, gk, pos] = (4.0 * math.sqrt(d)) * u
+                heavy[b][gk] = sorted(pos.tolist())
     return {"q_win": q_win.to(wl.dtype), "k": k.to(wl.dtype), "v": v.to(wl.dtype),
-            "L": list(L)}
+            "L": list(L), "heavy": heavy}
 
 
 def make_queries(wl: Workload, layer: int = 0, L: Optional[List[int]] = None):

@@ -50,3 +50,9 @@ def check_keep(gpu_keep: np.ndarray, pooled: np.ndarray, n_x: int, w: int, n_kee
 
 def score_rel_err(gpu: np.ndarray, ref: np.ndarray) -> float:
     return float(np.max(np.abs(gpu - ref) / np.maximum(np.abs(ref), 1e-300)))
+
+
+def score_rel_err_p99(gpu: np.ndarray, ref: np.ndarray) -> float:
+    """99th percentile of the per-position relative score error."""
+    e = np.abs(gpu - ref) / np.maximum(np.abs(ref), 1e-300)
+    return float(np.percentile(e, 99))
