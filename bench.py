@@ -511,12 +511,14 @@ def paged_serving(torch, _lib, synth, Evictor, dev, T=64, n_req=64, max_seqs=16,
     in [0, 0.9] per sequence, 28 q / 4 kv heads, d = 128) decoded for T steps
     from contiguous caches and from pages scattered through a pool, with the
     same launch plan; both replayed from graphs.
-    (2) A stream of n_req requests through the server (one layer): prompts of
-    1024..16384 tokens, ratios in [0, 0.9], 64..256 new tokens each, all
-    waiting at the start; up to max_admit are evicted per admission batch and
-    up to max_seqs decode together; a finished request frees its pages at
-    once.  Timed by the wall clock (host bookkeeping included) and by HIP
-    events around each admission and decode step."""
+    (2) A stream of n_req requests through the server (one layer, a library
+    call per step): prompts of 1024..16384 tokens, ratios in [0, 0.9],
+    64..256 new tokens each, all waiting at the start; up to max_admit are
+    evicted per admission batch and up to max_seqs decode together; a
+    finished request frees its pages at once.  Timed by the wall clock (host
+    bookkeeping included) and by HIP events around each admission and decode
+    step.  (3) The same with n_req / 2 requests through the 28-layer model
+    shape, each decode step's 28 launches replayed from a captured graph."""
     from paper_2512_21859_amd.serving import PAGE, Server
     wl = synth.WORKLOADS[4]
     B, Hq, Hkv, d, w, pool = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.pool
@@ -587,26 +589,43 @@ def paged_serving(torch, _lib, synth, Evictor, dev, T=64, n_req=64, max_seqs=16,
     del cache, k_pool, v_pool, g_c, g_p, q_win, k, v, qd, knd, vnd, ev, out_c, out_p
     torch.cuda.empty_cache()
 
-    # (2) the stream
+    # (2) the streams: one layer with a library call per layer and step, and
+    # the 28-layer model shape with each step's 28 launches replayed from a graph
+    stream_res = _serving_stream(torch, _lib, Server, dev, wl, n_layers=1, n_req=n_req,
+                                 max_seqs=max_seqs, max_admit=max_admit, graphed=False)
+    stream28 = _serving_stream(torch, _lib, Server, dev, wl, n_layers=28, n_req=n_req // 2,
+                               max_seqs=max_seqs, max_admit=max_admit, graphed=True)
+    return {"batch": batch, "stream": stream_res, "stream_28_layers": stream28}
+
+
+def _serving_stream(torch, _lib, Server, dev, wl, n_layers, n_req, max_seqs, max_admit,
+                    graphed):
+    """n_req requests (prompts 1024..16384, ratios 0..0.9, 64..256 new tokens,
+    all waiting at the start) through a server of n_layers layers; admission
+    evicts every layer of up to max_admit requests; one decode step runs every
+    layer of the running batch (graph-replayed when graphed).  The second of two
+    passes is timed; GPU figures sum HIP events around admissions and steps."""
+    from paper_2512_21859_amd.serving import PAGE
+    Hq, Hkv, d, w, pool = wl.Hq, wl.Hkv, wl.d, wl.w, wl.pool
+    stream = torch.cuda.current_stream()
     gen = torch.Generator().manual_seed(6464)
     rL = torch.randint(1024, 16385, (n_req,), generator=gen).tolist()
     ra = (0.9 * torch.rand(n_req, generator=gen, dtype=torch.float64)).tolist()
     rn = torch.randint(64, 257, (n_req,), generator=gen).tolist()
     Pmax = 16384
     max_pages = -(-(Pmax + 256) // PAGE)
-    srv = Server(1, n_pages=max_seqs * max_pages, max_seqs=max_seqs, max_pages=max_pages,
+    srv = Server(n_layers, n_pages=max_seqs * max_pages, max_seqs=max_seqs, max_pages=max_pages,
                  Hq=Hq, Hkv=Hkv, d=d, dtype=wl.dtype, w=w, pool=pool, max_admit=max_admit,
                  max_prompt=Pmax, device=dev)
     dg = torch.Generator(device=dev).manual_seed(77)
     kb = torch.randn((max_admit, Hkv, Pmax, d), generator=dg, device=dev).to(wl.dtype)
     vb = torch.randn((max_admit, Hkv, Pmax, d), generator=dg, device=dev).to(wl.dtype)
     qb = torch.randn((max_admit, Hq, w, d), generator=dg, device=dev).to(wl.dtype)
-    qs = torch.randn((1, max_seqs, Hq, d), generator=dg, device=dev).to(wl.dtype)
-    ks = torch.randn((1, max_seqs, Hkv, d), generator=dg, device=dev).to(wl.dtype)
-    vs = torch.randn((1, max_seqs, Hkv, d), generator=dg, device=dev).to(wl.dtype)
-    out = torch.empty_like(qs)
+    for buf in (srv.q_in, srv.k_in, srv.v_in):         # decode inputs (any values)
+        buf.copy_(torch.randn(buf.shape, generator=dg, device=dev).to(wl.dtype))
+    prompts = [{"q_win": qb, "k": kb, "v": vb}] * n_layers   # every layer evicts the same data
 
-    def run(timed):
+    def run():
         queue = list(range(n_req))
         ev_pairs, de_pairs = [], []
         steps = tokens = batch_sum = 0
@@ -623,9 +642,8 @@ def paged_serving(torch, _lib, synth, Evictor, dev, T=64, n_req=64, max_seqs=16,
                 b = len(adm)
                 e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                 e[0].record(stream)
-                srv.admit(adm, [rL[r] for r in adm], [ra[r] for r in adm],
-                          [rn[r] for r in adm],
-                          [{"q_win": qb[:b], "k": kb[:b], "v": vb[:b]}], stream=stream)
+                srv.admit(adm, [rL[r] for r in adm], [ra[r] for r in adm], [rn[r] for r in adm],
+                          [{k: x[:b] for k, x in p.items()} for p in prompts], stream=stream)
                 e[1].record(stream)
                 ev_pairs.append(e)
             n = srv.n_active
@@ -634,36 +652,43 @@ def paged_serving(torch, _lib, synth, Evictor, dev, T=64, n_req=64, max_seqs=16,
             lens = srv.slots.lengths()
             e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             e[0].record(stream)
-            srv.step(qs[:, :n], ks[:, :n], vs[:, :n], out[:, :n], stream=stream)
+            if graphed:
+                srv.step_graphed()
+            else:
+                srv.step(srv.q_in[:, :n], srv.k_in[:, :n], srv.v_in[:, :n], srv.o_out[:, :n],
+                         stream=stream)
             e[1].record(stream)
             de_pairs.append(e)
             steps += 1
             tokens += n
             batch_sum += n
-            dec_bytes += sum(_decode_bytes(Hq, Hkv, d, int(x) + 1) for x in lens)
+            dec_bytes += n_layers * sum(_decode_bytes(Hq, Hkv, d, int(x) + 1) for x in lens)
         torch.cuda.synchronize()
         return ev_pairs, de_pairs, steps, tokens, batch_sum, dec_bytes
 
-    run(False)                                   # warm-up pass over the whole stream
+    run()                                        # warm-up pass (and graph captures)
     t0 = time.perf_counter()
-    ev_pairs, de_pairs, steps, tokens, batch_sum, dec_bytes = run(True)
+    ev_pairs, de_pairs, steps, tokens, batch_sum, dec_bytes = run()
     wall = time.perf_counter() - t0
     ev_ms = sum(a.elapsed_time(b) for a, b in ev_pairs)
     de_ms = sum(a.elapsed_time(b) for a, b in de_pairs)
-    stream_res = {
-        "workload": f"{n_req} requests, 1 layer bf16, prompts 1024..16384, ratios 0..0.9, "
-                    f"64..256 new tokens, <= {max_seqs} decoding, <= {max_admit} per admission",
+    res = {
+        "workload": f"{n_req} requests, {n_layers} layer(s) bf16, prompts 1024..16384, ratios "
+                    f"0..0.9, 64..256 new tokens, <= {max_seqs} decoding, <= {max_admit} per "
+                    f"admission" + (", each step's launches replayed from a graph" if graphed else ""),
         "tokens": tokens, "decode_steps": steps, "admissions": len(ev_pairs),
         "mean_batch": round(batch_sum / steps, 2),
         "wall_s": round(wall, 4), "tokens_per_s_wall": round(tokens / wall, 1),
         "gpu_decode_ms": round(de_ms, 3), "gpu_evict_ms": round(ev_ms, 3),
+        "decode_tokens_per_s_gpu": round(tokens / (de_ms * 1e-3), 1),
         "tokens_per_s_gpu": round(tokens / ((de_ms + ev_ms) * 1e-3), 1),
         "decode_GBps": round(dec_bytes / (de_ms * 1e-3) / 1e9, 1),
         "timing": "second pass over the stream (the first warms up); GPU figures sum HIP "
                   "events around each admission and each decode step"}
     del srv, kb, vb, qb
     torch.cuda.empty_cache()
-    return {"batch": batch, "stream": stream_res}
+    return res
+
 
 
 def main():

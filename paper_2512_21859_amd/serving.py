@@ -155,6 +155,12 @@ class Server:
         sc = _lib.tb_workspace_bytes(_lib.TB_OP_SCORE, max_admit, max_prompt, Hq, Hkv, d, w, 0)
         self.score_ws = torch.empty((max(sc, 1),), dtype=torch.uint8, device=device)
         self.keep: Dict[int, List[torch.Tensor]] = {}       # rid -> per-layer keep_idx (kept on request)
+        # static decode inputs / outputs for graph replay: row i = slot i
+        self.q_in = torch.zeros((n_layers, max_seqs, Hq, d), dtype=dtype, device=device)
+        self.k_in = torch.zeros((n_layers, max_seqs, Hkv, d), dtype=dtype, device=device)
+        self.v_in = torch.zeros((n_layers, max_seqs, Hkv, d), dtype=dtype, device=device)
+        self.o_out = torch.zeros((n_layers, max_seqs, Hq, d), dtype=dtype, device=device)
+        self._graphs: Dict[int, torch.cuda.CUDAGraph] = {}
 
     @property
     def n_active(self) -> int:
@@ -227,6 +233,35 @@ class Server:
             _lib.tb_decode_attn_paged(q[layer], k_new[layer], v_new[layer], self.k_pool[layer],
                                       self.v_pool[layer], self.table, self.kv_len[layer],
                                       out[layer], self.dec_ws, stream)
+        self.slots.advance()
+
+    def step_graphed(self) -> None:
+        """One decode step of the running batch from the static buffers: reads
+        q_in / k_in / v_in[:, :n] and writes o_out[:, :n] (n = running
+        requests).  The n_layers launches of a batch size are captured once in
+        a graph and replayed on the current stream; the block table and the
+        lengths are read from device memory at replay, so membership changes
+        need no new capture."""
+        n = self.n_active
+        if n == 0:
+            raise RuntimeError("no running request")
+        if any(e.left <= 0 for e in self.slots.slots):
+            raise RuntimeError("retire finished requests before the next step")
+        g = self._graphs.get(n)
+        if g is None:
+            g = torch.cuda.CUDAGraph()
+            cs = torch.cuda.Stream()
+            cs.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.graph(g, stream=cs):
+                for layer in range(self.n_layers):
+                    _lib.tb_decode_attn_paged(self.q_in[layer, :n], self.k_in[layer, :n],
+                                              self.v_in[layer, :n], self.k_pool[layer],
+                                              self.v_pool[layer], self.table, self.kv_len[layer],
+                                              self.o_out[layer, :n], self.dec_ws, cs)
+            torch.cuda.current_stream().wait_stream(cs)
+            self._graphs[n] = g
+            # capture only records the launches: run this step now
+        g.replay()
         self.slots.advance()
 
     def retire(self, rids: Sequence[int]) -> None:

@@ -6,7 +6,8 @@ tile lives differs), with sequences' pages scattered through the pool, pages
 owned by nobody left untouched, and table entries past a sequence's length
 holding junk.  The server test runs a stream of requests with per-request
 ratios through admission, decode and retirement (slots move, pages are
-reused) and checks every output against the float64 oracle.
+reused) and checks every output against the float64 oracle; the
+graph-replayed server step must equal the per-call step bit for bit.
 """
 import numpy as np
 import pytest
@@ -207,3 +208,63 @@ def test_server_stream_matches_oracle():
                     ref = O.decode_step(dq[s, g * G:(g + 1) * G], rk, rv)
                     err = np.abs(got[g * G:(g + 1) * G] - ref).max()
                     assert err <= tol, f"r={r} layer={layer} g={g} step={s}: err {err}"
+
+
+def test_server_graph_step_equals_eager():
+    """The graph-replayed step (one captured graph per batch size, reused as
+    requests come and go) gives bit for bit what the per-call step gives."""
+    n_req, layers, Hq, Hkv, d, w, pool = 7, 3, 28, 4, 128, 32, 7
+    gen = torch.Generator().manual_seed(77)
+    L = torch.randint(200, 1500, (n_req,), generator=gen).tolist()
+    alphas = (0.8 * torch.rand(n_req, generator=gen, dtype=torch.float64)).tolist()
+    max_new = torch.randint(2, 12, (n_req,), generator=gen).tolist()
+    case(f"server graph vs eager L={L} max_new={max_new}")
+    wl = synth.custom(62, torch.bfloat16, n_req, L, Hq, Hkv, d, w, pool, max(max_new))
+    prompts = [synth.make_prompt(wl, layer, L) for layer in range(layers)]
+    dec = [synth.make_decode(wl, layer) for layer in range(layers)]
+    kw = dict(n_pages=200, max_seqs=4, max_pages=64, Hq=Hq, Hkv=Hkv, d=d, dtype=torch.bfloat16,
+              w=w, pool=pool, max_admit=2, max_prompt=max(L))
+    srv_e, srv_g = Server(layers, **kw), Server(layers, **kw)
+    queue, done_steps, steps = list(range(n_req)), {r: 0 for r in range(n_req)}, 0
+    sizes = set()
+    while queue or srv_e.n_active:
+        for r in srv_e.slots.finished():
+            srv_e.retire([r])
+            srv_g.retire([r])
+        batch = []
+        while (queue and len(batch) < 2 and srv_e.slots.fits(
+                [_lib.tb_keep_count(L[r], alphas[r], w) + max_new[r] for r in batch + [queue[0]]])):
+            batch.append(queue.pop(0))
+        if batch:
+            bl = [L[r] for r in batch]
+            pr = [{key: prompts[layer][key][batch][:, :, :max(bl)].contiguous().to(DEV)
+                   for key in ("k", "v")} for layer in range(layers)]
+            for layer in range(layers):
+                pr[layer]["q_win"] = prompts[layer]["q_win"][batch].contiguous().to(DEV)
+            for srv in (srv_e, srv_g):
+                srv.admit(batch, bl, [alphas[r] for r in batch], [max_new[r] for r in batch], pr)
+        if not srv_e.n_active:
+            continue
+        assert srv_e.rids() == srv_g.rids()
+        rid, n = srv_e.rids(), srv_e.n_active
+        sizes.add(n)
+        qs = torch.stack([torch.stack([dec[l]["q"][done_steps[r], r] for r in rid])
+                          for l in range(layers)]).to(DEV)
+        ks = torch.stack([torch.stack([dec[l]["k_new"][done_steps[r], r] for r in rid])
+                          for l in range(layers)]).to(DEV)
+        vs = torch.stack([torch.stack([dec[l]["v_new"][done_steps[r], r] for r in rid])
+                          for l in range(layers)]).to(DEV)
+        out = torch.empty_like(qs)
+        srv_e.step(qs, ks, vs, out)
+        srv_g.q_in[:, :n].copy_(qs)
+        srv_g.k_in[:, :n].copy_(ks)
+        srv_g.v_in[:, :n].copy_(vs)
+        srv_g.step_graphed()
+        torch.cuda.synchronize()
+        assert torch.equal(out, srv_g.o_out[:, :n]), f"step {steps}: graph replay differs"
+        for r in rid:
+            done_steps[r] += 1
+        steps += 1
+        assert steps < 200
+    assert len(sizes) >= 3, f"batch sizes seen: {sizes}"
+    assert torch.equal(srv_e.kv_len, srv_g.kv_len)
