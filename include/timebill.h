@@ -213,7 +213,8 @@ tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new,
  *   v_pool [n_pages][Hkv][d][32]   the tile's V^T
  *   block_table [B][max_pages]     int32 (device): row t/32 of sequence b is
  *                                  in page block_table[b][t / 32]
- * A sequence holds up to max_pages * 32 rows.  The pages a sequence writes
+ * A sequence holds up to max_pages * 32 rows (1 <= max_pages <= 2^25, else
+ * TB_EUNSUPPORTED; 1 <= n_pages).  The pages a sequence writes
  * (compaction: tiles below n_keep[b]; decode: the tile of row kv_len[b]) must
  * be its own; entries past its length may hold any value (out-of-range
  * entries are clamped into the pool before any read, so they never fault).

@@ -443,8 +443,9 @@ tb_status check_paging(const char* name, const int32_t* table, int32_t max_pages
   if (max_pages < 1 || n_pages < 1)
     return fail(TB_EINVAL, "%s: max_pages and n_pages must be >= 1 (got %d, %d)", name,
                 max_pages, n_pages);
-  if (max_pages > (1 << 26))
-    return fail(TB_EUNSUPPORTED, "%s: max_pages must be <= 2^26 (got %d)", name, max_pages);
+  // the capacity max_pages * 32 rows must stay a positive int32
+  if (max_pages > (1 << 25))
+    return fail(TB_EUNSUPPORTED, "%s: max_pages must be <= 2^25 (got %d)", name, max_pages);
   return TB_OK;
 }
 

@@ -241,6 +241,8 @@ def test_compact_paged_validation(lib):
     assert call(max_pages=0) == E.TB_EINVAL
     assert call(n_pages=0) == E.TB_EINVAL
     assert call(max_pages=1 << 27) == E.TB_EUNSUPPORTED
+    assert call(max_pages=(1 << 25) + 1) == E.TB_EUNSUPPORTED   # capacity would pass 2^30 rows
+    assert call(max_pages=1 << 26) == E.TB_EUNSUPPORTED         # 2^26 * 32 overflows int32
     assert call(n=65) == E.TB_EINVAL          # beyond max_pages * 32 rows
     assert call(kp=None) == E.TB_EINVAL
     assert call(d=32) == E.TB_EUNSUPPORTED
