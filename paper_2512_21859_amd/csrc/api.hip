@@ -142,7 +142,8 @@ size_t tb_workspace_bytes(int32_t op, int32_t B, int32_t Lmax, int32_t Hq, int32
   try {
     switch (op) {
       case TB_OP_SCORE: {
-        if (B < 1 || Lmax < 1 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0 || w < 1) {
+        if (B < 1 || Lmax < 1 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0 || w < 1 ||
+            static_cast<long long>(Hq / Hkv) * w > 1024) {
           fail(TB_EINVAL, "tb_workspace_bytes(SCORE): bad sizes");
           return 0;
         }
@@ -195,8 +196,9 @@ tb_status score_window_impl(const char* name, bool avg, const void* q_win, const
     if (w < 1) return fail(TB_EINVAL, "w must be >= 1 (got %d)", w);
     if (pool < 1 || pool % 2 == 0) return fail(TB_EINVAL, "pool must be odd and >= 1 (got %d)", pool);
     if (pool > 129) return fail(TB_EUNSUPPORTED, "pool must be <= 129 (got %d)", pool);
-    const int R = (Hq / Hkv) * w;
-    if (R > 1024) return fail(TB_EUNSUPPORTED, "(Hq/Hkv)*w must be <= 1024 (got %d)", R);
+    const long long R64 = static_cast<long long>(Hq / Hkv) * w;     // no int overflow for huge w
+    if (R64 > 1024) return fail(TB_EUNSUPPORTED, "(Hq/Hkv)*w must be <= 1024 (got %lld)", R64);
+    const int R = static_cast<int>(R64);
     for (int b = 0; b < B; ++b)
       if (!(L[b] > w && L[b] <= Lmax))
         return fail(TB_EINVAL, "need w < L[%d] <= Lmax (w=%d, L=%d, Lmax=%d)", b, w, L[b], Lmax);

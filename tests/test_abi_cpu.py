@@ -109,6 +109,9 @@ def test_score_validation(lib):
     assert _score(lib, w=100) == E.TB_EINVAL            # w must be < L
     assert _score(lib, L=_i32(101)) == E.TB_EINVAL      # L > Lmax
     assert _score(lib, Hq=40, Hkv=1, w=32) == E.TB_EUNSUPPORTED   # G*w > 1024
+    assert _score(lib, Hq=64, Hkv=1, w=1 << 27, L=_i32((1 << 27) + 1),
+                  Lmax=(1 << 27) + 1) == E.TB_EUNSUPPORTED          # G*w would wrap an int
+    assert _lib.tb_workspace_bytes(_lib.TB_OP_SCORE, 1, 1 << 28, 64, 1, 128, 1 << 27, 0) == 0
     assert _score(lib, wsb=16) == E.TB_EWORKSPACE
     assert b"workspace" in lib.tb_last_error()
 
