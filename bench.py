@@ -595,16 +595,27 @@ def paged_serving(torch, _lib, synth, Evictor, dev, T=64, n_req=64, max_seqs=16,
                                  max_seqs=max_seqs, max_admit=max_admit, graphed=False)
     stream28 = _serving_stream(torch, _lib, Server, dev, wl, n_layers=28, n_req=n_req // 2,
                                max_seqs=max_seqs, max_admit=max_admit, graphed=True)
-    return {"batch": batch, "stream": stream_res, "stream_28_layers": stream28}
+    stream28o = _serving_stream(torch, _lib, Server, dev, wl, n_layers=28, n_req=n_req // 2,
+                                max_seqs=max_seqs, max_admit=max_admit, graphed=True,
+                                overlap=True)
+    return {"batch": batch, "stream": stream_res, "stream_28_layers": stream28,
+            "stream_28_layers_overlapped": stream28o}
 
 
 def _serving_stream(torch, _lib, Server, dev, wl, n_layers, n_req, max_seqs, max_admit,
-                    graphed):
+                    graphed, overlap=False):
     """n_req requests (prompts 1024..16384, ratios 0..0.9, 64..256 new tokens,
     all waiting at the start) through a server of n_layers layers; admission
     evicts every layer of up to max_admit requests; one decode step runs every
-    layer of the running batch (graph-replayed when graphed).  The second of two
-    passes is timed; GPU figures sum HIP events around admissions and steps."""
+    layer of the running batch (graph-replayed when graphed).  With overlap the
+    eviction runs on its own stream beside the decode steps and the batch joins
+    at the first step after it has finished; otherwise it runs between two
+    steps.  As a server that samples each step's tokens must, the host queues
+    step t only once step t-2 has finished (one step in flight while the next
+    is prepared).  The second of two passes is timed; GPU figures sum HIP
+    events around admissions and steps, the token interval is the time between
+    the ends of consecutive steps on the decode stream, and the join delay is
+    the time from an admission's call to its requests' first step."""
     from paper_2512_21859_amd.serving import PAGE
     Hq, Hkv, d, w, pool = wl.Hq, wl.Hkv, wl.d, wl.w, wl.pool
     stream = torch.cuda.current_stream()
@@ -624,28 +635,46 @@ def _serving_stream(torch, _lib, Server, dev, wl, n_layers, n_req, max_seqs, max
     for buf in (srv.q_in, srv.k_in, srv.v_in):         # decode inputs (any values)
         buf.copy_(torch.randn(buf.shape, generator=dg, device=dev).to(wl.dtype))
     prompts = [{"q_win": qb, "k": kb, "v": vb}] * n_layers   # every layer evicts the same data
+    if graphed:
+        for n in range(1, max_seqs + 1):         # capture synchronises: keep it out of the passes
+            srv.capture(n)
 
     def run():
         queue = list(range(n_req))
-        ev_pairs, de_pairs = [], []
+        ev_pairs, de_pairs, waiting, just, joins = [], [], [], [], []
         steps = tokens = batch_sum = 0
         dec_bytes = 0.0
-        while queue or srv.n_active:
+        while queue or srv.n_active or srv.slots.pending:
             fin = srv.slots.finished()
             if fin:
                 srv.retire(fin)
+            if overlap and srv.promote_ready(wait=srv.n_active == 0):
+                just.append(waiting.pop(0))
             adm = []
-            while (queue and len(adm) < max_admit and srv.slots.fits(
+            while (queue and not srv.slots.pending and len(adm) < max_admit and srv.slots.fits(
                     [_lib.tb_keep_count(rL[r], ra[r], w) + rn[r] for r in adm + [queue[0]]])):
                 adm.append(queue.pop(0))
             if adm:
                 b = len(adm)
-                e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                e[0].record(stream)
-                srv.admit(adm, [rL[r] for r in adm], [ra[r] for r in adm], [rn[r] for r in adm],
-                          [{k: x[:b] for k, x in p.items()} for p in prompts], stream=stream)
-                e[1].record(stream)
-                ev_pairs.append(e)
+                args = (adm, [rL[r] for r in adm], [ra[r] for r in adm], [rn[r] for r in adm],
+                        [{k: x[:b] for k, x in p.items()} for p in prompts])
+                if overlap:
+                    e = torch.cuda.Event(enable_timing=True)
+                    e.record(stream)
+                    srv.admit_async(*args)
+                    waiting.append(e)
+                    if srv.n_active == 0:
+                        srv.promote_ready(wait=True)
+                        just.append(waiting.pop(0))
+                    ev_pairs.append(None)
+                else:
+                    e = (torch.cuda.Event(enable_timing=True),
+                         torch.cuda.Event(enable_timing=True))
+                    e[0].record(stream)
+                    srv.admit(*args, stream=stream)
+                    e[1].record(stream)
+                    ev_pairs.append(e)
+                    just.append(e[0])
             n = srv.n_active
             if n == 0:
                 continue                         # the last requests just retired
@@ -659,32 +688,46 @@ def _serving_stream(torch, _lib, Server, dev, wl, n_layers, n_req, max_seqs, max
                          stream=stream)
             e[1].record(stream)
             de_pairs.append(e)
+            joins += [(x, e[0]) for x in just]
+            just = []
+            if len(de_pairs) >= 2:
+                de_pairs[-2][1].synchronize()    # step t-1's tokens are read back
             steps += 1
             tokens += n
             batch_sum += n
             dec_bytes += n_layers * sum(_decode_bytes(Hq, Hkv, d, int(x) + 1) for x in lens)
         torch.cuda.synchronize()
-        return ev_pairs, de_pairs, steps, tokens, batch_sum, dec_bytes
+        return ev_pairs, de_pairs, joins, steps, tokens, batch_sum, dec_bytes
 
     run()                                        # warm-up pass (and graph captures)
     t0 = time.perf_counter()
-    ev_pairs, de_pairs, steps, tokens, batch_sum, dec_bytes = run()
+    ev_pairs, de_pairs, joins, steps, tokens, batch_sum, dec_bytes = run()
     wall = time.perf_counter() - t0
-    ev_ms = sum(a.elapsed_time(b) for a, b in ev_pairs)
     de_ms = sum(a.elapsed_time(b) for a, b in de_pairs)
+    gaps = sorted(de_pairs[i][1].elapsed_time(de_pairs[i + 1][1])
+                  for i in range(len(de_pairs) - 1))
+    jd = sorted(a.elapsed_time(b) for a, b in joins)
     res = {
         "workload": f"{n_req} requests, {n_layers} layer(s) bf16, prompts 1024..16384, ratios "
                     f"0..0.9, 64..256 new tokens, <= {max_seqs} decoding, <= {max_admit} per "
-                    f"admission" + (", each step's launches replayed from a graph" if graphed else ""),
+                    f"admission" + (", each step's launches replayed from a graph" if graphed else "")
+                    + (", eviction overlapped with decode on a second stream" if overlap else ""),
         "tokens": tokens, "decode_steps": steps, "admissions": len(ev_pairs),
         "mean_batch": round(batch_sum / steps, 2),
         "wall_s": round(wall, 4), "tokens_per_s_wall": round(tokens / wall, 1),
-        "gpu_decode_ms": round(de_ms, 3), "gpu_evict_ms": round(ev_ms, 3),
+        "gpu_decode_ms": round(de_ms, 3),
         "decode_tokens_per_s_gpu": round(tokens / (de_ms * 1e-3), 1),
-        "tokens_per_s_gpu": round(tokens / ((de_ms + ev_ms) * 1e-3), 1),
         "decode_GBps": round(dec_bytes / (de_ms * 1e-3) / 1e9, 1),
+        "token_interval_ms": {"p50": round(gaps[len(gaps) // 2], 4),
+                              "p99": round(gaps[int(0.99 * (len(gaps) - 1))], 4),
+                              "max": round(gaps[-1], 4)},
+        "join_delay_ms": {"mean": round(sum(jd) / len(jd), 3), "max": round(jd[-1], 3)},
         "timing": "second pass over the stream (the first warms up); GPU figures sum HIP "
                   "events around each admission and each decode step"}
+    if not overlap:
+        ev_ms = sum(a.elapsed_time(b) for a, b in ev_pairs)
+        res["gpu_evict_ms"] = round(ev_ms, 3)
+        res["tokens_per_s_gpu"] = round(tokens / ((de_ms + ev_ms) * 1e-3), 1)
     del srv, kb, vb, qb
     torch.cuda.empty_cache()
     return res

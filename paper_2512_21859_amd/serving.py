@@ -17,9 +17,18 @@ step is always one dense batch.
 
 Pages are reserved at admission for the retained prompt plus the request's
 whole response (max_new tokens), so a running request never waits for pages
-and nothing is preempted.  The host holds the bookkeeping (which pages, which
-slot, how long); this module allocates device buffers (torch) and sequences
-library calls; every computation runs in the kernels.
+and nothing is preempted.
+
+Admission can also overlap decoding (Server.admit_async): the new batch's
+eviction runs on a stream of its own into the top slots of the table, which
+no decode step reads (a step reads slots 0..n-1 only), and the batch joins the
+running one, at its end, once that eviction has finished (promote_ready).
+The two streams touch disjoint table rows, lengths, pages and scratch buffers,
+so a running request's step time is not held up by a whole admission.
+
+The host holds the bookkeeping (which pages, which slot, how long); this
+module allocates device buffers (torch) and sequences library calls; every
+computation runs in the kernels.
 """
 from __future__ import annotations
 
@@ -32,6 +41,30 @@ import torch
 from . import _lib
 
 PAGE = _lib.V_TILE          # rows per page: one 32-row tile of every KV head
+
+
+class _Staging:
+    """Pinned host buffers for asynchronous uploads of table rows and lengths.
+    A buffer is refilled only after the copy that last read it has finished,
+    so uploads never block on the stream they are queued on."""
+
+    def __init__(self, n: int, nbytes: int):
+        self.bufs = [torch.empty((nbytes,), dtype=torch.uint8, pin_memory=True) for _ in range(n)]
+        self.done: List[Optional[torch.cuda.Event]] = [None] * n
+        self.i = 0
+
+    def put(self, dst: torch.Tensor, src: np.ndarray, stream) -> None:
+        src = np.array(src, dtype=np.int32, order="C")          # an owned, writable copy
+        i, self.i = self.i, (self.i + 1) % len(self.bufs)
+        if self.done[i] is not None:
+            self.done[i].synchronize()
+        host = self.bufs[i][: src.nbytes].view(torch.int32).view(src.shape)
+        host.copy_(torch.from_numpy(src))
+        with torch.cuda.stream(stream):
+            dst.copy_(host, non_blocking=True)
+            ev = torch.cuda.Event()
+            ev.record(stream)
+        self.done[i] = ev
 
 
 @dataclass
@@ -55,6 +88,9 @@ class SlotTable:
         self.n_pages, self.max_seqs, self.max_pages = n_pages, max_seqs, max_pages
         self.free: List[int] = list(range(n_pages - 1, -1, -1))     # pop() gives page 0 first
         self.slots: List[Entry] = []
+        # a batch admitted asynchronously: its eviction is still running, so it
+        # holds the top slots [max_seqs - len(pending), max_seqs), which stay put
+        self.pending: List[Entry] = []
 
     @staticmethod
     def pages_for(rows: int) -> int:
@@ -63,26 +99,62 @@ class SlotTable:
     def fits(self, rows: Sequence[int]) -> bool:
         """Could requests needing these row counts all be admitted now?"""
         need = [self.pages_for(r) for r in rows]
-        return (len(self.slots) + len(rows) <= self.max_seqs and
+        return (len(self.slots) + len(self.pending) + len(rows) <= self.max_seqs and
                 all(n <= self.max_pages for n in need) and sum(need) <= len(self.free))
 
-    def admit(self, rid: int, n_keep: int, max_new: int, alpha: float = 0.0,
-              n_x: int = 0) -> int:
-        """Reserve pages for n_keep + max_new rows and append a slot; returns it."""
+    def _reserve(self, rid: int, n_keep: int, max_new: int, alpha: float, n_x: int) -> Entry:
         if n_keep < 1 or max_new < 0:
             raise ValueError("need n_keep >= 1 and max_new >= 0")
-        if any(e.rid == rid for e in self.slots):
+        if any(e.rid == rid for e in self.slots + self.pending):
             raise ValueError(f"request {rid} is already running")
         n = self.pages_for(n_keep + max_new)
         if n > self.max_pages:
             raise ValueError(f"request {rid}: {n_keep + max_new} rows need {n} pages "
                              f"> max_pages {self.max_pages}")
-        if len(self.slots) >= self.max_seqs:
+        if len(self.slots) + len(self.pending) >= self.max_seqs:
             raise MemoryError("no free slot")
         if n > len(self.free):
             raise MemoryError(f"request {rid}: {n} pages needed, {len(self.free)} free")
-        pages = [self.free.pop() for _ in range(n)]
-        self.slots.append(Entry(rid, pages, n_keep, max_new, alpha, n_x))
+        return Entry(rid, [self.free.pop() for _ in range(n)], n_keep, max_new, alpha, n_x)
+
+    def admit_pending(self, rids: Sequence[int], n_keep: Sequence[int], max_new: Sequence[int],
+                      alphas: Sequence[float], n_x: Sequence[int]) -> int:
+        """Reserve pages and the top slots for a batch whose eviction runs
+        asynchronously; returns its first slot.  One pending batch at a time."""
+        if self.pending:
+            raise RuntimeError("an admitted batch is still pending")
+        # checked whole first, so that a bad batch reserves nothing
+        if not (len(rids) == len(n_keep) == len(max_new) == len(alphas) == len(n_x)) or not rids:
+            raise ValueError("rids, n_keep, max_new, alphas and n_x must be non-empty and agree")
+        running = {e.rid for e in self.slots}
+        if len(set(rids)) != len(rids) or running & set(rids):
+            raise ValueError("a request appears twice or is already running")
+        if min(n_keep) < 1 or min(max_new) < 0:
+            raise ValueError("need n_keep >= 1 and max_new >= 0")
+        if any(self.pages_for(k + m) > self.max_pages for k, m in zip(n_keep, max_new)):
+            raise ValueError(f"a request needs more than max_pages {self.max_pages} pages")
+        if not self.fits([k + m for k, m in zip(n_keep, max_new)]):
+            raise MemoryError("not enough slots or pages for this batch")
+        for i, r in enumerate(rids):
+            self.pending.append(self._reserve(r, n_keep[i], max_new[i], alphas[i], n_x[i]))
+        return self.max_seqs - len(self.pending)
+
+    def pending_rows(self) -> np.ndarray:
+        """Block-table rows of the pending slots, in slot order."""
+        return self._rows(self.pending)
+
+    def promote(self) -> tuple:
+        """The pending batch joins the running one at its end; returns the slot
+        range [lo, hi) it now occupies."""
+        lo = len(self.slots)
+        self.slots.extend(self.pending)
+        self.pending = []
+        return lo, len(self.slots)
+
+    def admit(self, rid: int, n_keep: int, max_new: int, alpha: float = 0.0,
+              n_x: int = 0) -> int:
+        """Reserve pages for n_keep + max_new rows and append a slot; returns it."""
+        self.slots.append(self._reserve(rid, n_keep, max_new, alpha, n_x))
         return len(self.slots) - 1
 
     def slot_of(self, rid: int) -> int:
@@ -118,8 +190,11 @@ class SlotTable:
         """Block-table rows of slots lo..hi-1; entries past a request's pages
         repeat its last page (never read: decode stays within the length)."""
         hi = len(self.slots) if hi is None else hi
-        out = np.empty((hi - lo, self.max_pages), dtype=np.int32)
-        for i, e in enumerate(self.slots[lo:hi]):
+        return self._rows(self.slots[lo:hi])
+
+    def _rows(self, entries: Sequence[Entry]) -> np.ndarray:
+        out = np.empty((len(entries), self.max_pages), dtype=np.int32)
+        for i, e in enumerate(entries):
             out[i, :len(e.pages)] = e.pages
             out[i, len(e.pages):] = e.pages[-1]
         return out
@@ -161,30 +236,28 @@ class Server:
         self.v_in = torch.zeros((n_layers, max_seqs, Hkv, d), dtype=dtype, device=device)
         self.o_out = torch.zeros((n_layers, max_seqs, Hq, d), dtype=dtype, device=device)
         self._graphs: Dict[int, torch.cuda.CUDAGraph] = {}
+        self._staging = _Staging(8, 4 * max(n_layers, max_pages) * max_seqs)
+        self._adm_stream: Optional[torch.cuda.Stream] = None
+        self._adm_done: Optional[torch.cuda.Event] = None
+        self._adm_refs: List[torch.Tensor] = []
 
     @property
     def n_active(self) -> int:
         return len(self.slots.slots)
 
-    def _upload(self, lo: int, hi: int, lengths: bool) -> None:
+    def _upload(self, lo: int, hi: int, lengths: bool, stream=None) -> None:
+        """Table rows (and lengths, in every layer) of running slots lo..hi-1,
+        queued on the stream without blocking the host."""
         if hi <= lo:
             return
-        self.table[lo:hi].copy_(torch.from_numpy(self.slots.table_rows(lo, hi)))
+        stream = stream or torch.cuda.current_stream()
+        self._staging.put(self.table[lo:hi], self.slots.table_rows(lo, hi), stream)
         if lengths:
-            ln = torch.from_numpy(self.slots.lengths()[lo:hi])
-            self.kv_len[:, lo:hi].copy_(ln.unsqueeze(0).expand(self.n_layers, -1))
+            ln = self.slots.lengths()[lo:hi]
+            self._staging.put(self.kv_len[:, lo:hi],
+                              np.broadcast_to(ln, (self.n_layers, hi - lo)), stream)
 
-    def admit(self, rids: Sequence[int], L: Sequence[int], alphas: Sequence[float],
-              max_new: Sequence[int], prompts: Sequence[dict], keep_sets: bool = False,
-              stream=None) -> List[int]:
-        """Evict and admit a batch of requests.
-
-        prompts[l] holds layer l's q_win [b, Hq, w, d], k and v [b, Hkv, Lmax, d]
-        (device, padded to Lmax = max(L)).  Every request keeps
-        keep_count(L, alpha, w) rows (the same in every layer) and reserves
-        pages for max_new more.  Returns n_keep per request.  keep_sets=True
-        keeps each request's per-layer kept positions in self.keep.
-        """
+    def _check_admission(self, rids, L, alphas, max_new, prompts) -> List[int]:
         b = len(rids)
         if not (b == len(L) == len(alphas) == len(max_new)) or b == 0:
             raise ValueError("rids, L, alphas and max_new must be non-empty and agree")
@@ -197,10 +270,76 @@ class Server:
             raise ValueError("bad prompt length or ratio")
         if not self.slots.fits([k + m for k, m in zip(n_keep, max_new)]):
             raise MemoryError("not enough slots or pages for this batch")
+        return n_keep
+
+    def admit(self, rids: Sequence[int], L: Sequence[int], alphas: Sequence[float],
+              max_new: Sequence[int], prompts: Sequence[dict], keep_sets: bool = False,
+              stream=None) -> List[int]:
+        """Evict and admit a batch of requests.
+
+        prompts[l] holds layer l's q_win [b, Hq, w, d], k and v [b, Hkv, Lmax, d]
+        (device, padded to Lmax = max(L)).  Every request keeps
+        keep_count(L, alpha, w) rows (the same in every layer) and reserves
+        pages for max_new more.  Returns n_keep per request.  keep_sets=True
+        keeps each request's per-layer kept positions in self.keep.
+        """
+        if self.slots.pending:
+            raise RuntimeError("an asynchronous admission is pending: promote it first")
+        n_keep = self._check_admission(rids, L, alphas, max_new, prompts)
         lo = self.n_active
-        for i in range(b):
+        for i in range(len(rids)):
             self.slots.admit(rids[i], n_keep[i], max_new[i], alphas[i], L[i])
-        self._upload(lo, lo + b, lengths=False)
+        self._upload(lo, lo + len(rids), lengths=False, stream=stream)
+        self._evict(rids, L, alphas, n_keep, prompts, lo, keep_sets, stream)
+        return n_keep
+
+    def admit_async(self, rids: Sequence[int], L: Sequence[int], alphas: Sequence[float],
+                    max_new: Sequence[int], prompts: Sequence[dict],
+                    keep_sets: bool = False) -> List[int]:
+        """admit(), with the eviction on a separate stream so that decode steps
+        queued meanwhile run alongside it.  The eviction starts after the work
+        already queued on the current stream (which may have produced the
+        prompts, or still read pages freed by a retirement).  The new requests
+        hold the top slots of the table until promote_ready() moves them into
+        the running batch; only one such batch may be pending."""
+        if self.slots.pending:
+            raise RuntimeError("an asynchronous admission is already pending")
+        n_keep = self._check_admission(rids, L, alphas, max_new, prompts)
+        top = self.slots.admit_pending(rids, n_keep, max_new, alphas, L)
+        if self._adm_stream is None:
+            self._adm_stream = torch.cuda.Stream()
+        adm = self._adm_stream
+        adm.wait_stream(torch.cuda.current_stream())
+        self._staging.put(self.table[top:top + len(rids)], self.slots.pending_rows(), adm)
+        self._adm_refs = [x for p in prompts for x in p.values()]
+        for x in self._adm_refs:            # the allocator must not reuse them before adm is done
+            x.record_stream(adm)
+        with torch.cuda.stream(adm):
+            self._evict(rids, L, alphas, n_keep, prompts, top, keep_sets, adm)
+            self._adm_done = torch.cuda.Event()
+            self._adm_done.record(adm)
+        return n_keep
+
+    def promote_ready(self, wait: bool = False, stream=None) -> int:
+        """If the pending batch's eviction has finished (or wait=True), move it
+        into slots n..n+b-1 of the running batch and return b; else return 0.
+        The table rows and lengths are uploaded on the given (decode) stream,
+        which also waits for the eviction."""
+        if not self.slots.pending:
+            return 0
+        if not (wait or self._adm_done.query()):
+            return 0
+        stream = stream or torch.cuda.current_stream()
+        stream.wait_event(self._adm_done)
+        lo, hi = self.slots.promote()
+        self._upload(lo, hi, lengths=True, stream=stream)
+        self._adm_refs = []
+        return hi - lo
+
+    def _evict(self, rids, L, alphas, n_keep, prompts, lo, keep_sets, stream) -> None:
+        """Score, select and compact every layer of the requests in slots
+        lo..lo+b-1, whose table rows are already on the device."""
+        b = len(rids)
         Lmax = prompts[0]["k"].shape[2]
         scores = self.scores_buf[: b * self.Hkv * Lmax].view(b, self.Hkv, Lmax)
         keep = self.keep_buf[: b * self.Hkv * Lmax].view(b, self.Hkv, Lmax)
@@ -216,7 +355,6 @@ class Server:
             if keep_sets:
                 for i, r in enumerate(rids):
                     self.keep.setdefault(r, []).append(keep[i, :, : n_keep[i]].clone())
-        return n_keep
 
     def step(self, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
              out: torch.Tensor, stream=None) -> None:
@@ -235,18 +373,11 @@ class Server:
                                       out[layer], self.dec_ws, stream)
         self.slots.advance()
 
-    def step_graphed(self) -> None:
-        """One decode step of the running batch from the static buffers: reads
-        q_in / k_in / v_in[:, :n] and writes o_out[:, :n] (n = running
-        requests).  The n_layers launches of a batch size are captured once in
-        a graph and replayed on the current stream; the block table and the
-        lengths are read from device memory at replay, so membership changes
-        need no new capture."""
-        n = self.n_active
-        if n == 0:
-            raise RuntimeError("no running request")
-        if any(e.left <= 0 for e in self.slots.slots):
-            raise RuntimeError("retire finished requests before the next step")
+    def capture(self, n: int) -> torch.cuda.CUDAGraph:
+        """The graph of one decode step at batch size n (captured once, on a
+        side stream; capture records the launches and runs nothing)."""
+        if not 1 <= n <= self.slots.max_seqs:
+            raise ValueError(f"batch size {n} outside 1..{self.slots.max_seqs}")
         g = self._graphs.get(n)
         if g is None:
             g = torch.cuda.CUDAGraph()
@@ -260,16 +391,29 @@ class Server:
                                               self.o_out[layer, :n], self.dec_ws, cs)
             torch.cuda.current_stream().wait_stream(cs)
             self._graphs[n] = g
-            # capture only records the launches: run this step now
-        g.replay()
+        return g
+
+    def step_graphed(self) -> None:
+        """One decode step of the running batch from the static buffers: reads
+        q_in / k_in / v_in[:, :n] and writes o_out[:, :n] (n = running
+        requests).  The n_layers launches of a batch size are captured once in
+        a graph and replayed on the current stream; the block table and the
+        lengths are read from device memory at replay, so membership changes
+        need no new capture."""
+        n = self.n_active
+        if n == 0:
+            raise RuntimeError("no running request")
+        if any(e.left <= 0 for e in self.slots.slots):
+            raise RuntimeError("retire finished requests before the next step")
+        self.capture(n).replay()
         self.slots.advance()
 
-    def retire(self, rids: Sequence[int]) -> None:
+    def retire(self, rids: Sequence[int], stream=None) -> None:
         """Free finished requests; the last running requests move into their slots."""
         for r in rids:
             self.slots.retire(r)
             self.keep.pop(r, None)
-        self._upload(0, self.n_active, lengths=True)
+        self._upload(0, self.n_active, lengths=True, stream=stream)
 
     def rids(self) -> List[int]:
         return [e.rid for e in self.slots.slots]

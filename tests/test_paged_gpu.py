@@ -7,7 +7,8 @@ owned by nobody left untouched, and table entries past a sequence's length
 holding junk.  The server test runs a stream of requests with per-request
 ratios through admission, decode and retirement (slots move, pages are
 reused) and checks every output against the float64 oracle; the
-graph-replayed server step must equal the per-call step bit for bit.
+graph-replayed server step must equal the per-call step bit for bit, and so
+must a server whose admissions overlap its decode steps.
 """
 import numpy as np
 import pytest
@@ -268,3 +269,86 @@ def test_server_graph_step_equals_eager():
         assert steps < 200
     assert len(sizes) >= 3, f"batch sizes seen: {sizes}"
     assert torch.equal(srv_e.kv_len, srv_g.kv_len)
+
+
+def test_server_async_admission_equals_serialized():
+    """Admission on its own stream while the running batch keeps decoding
+    (graph-replayed) and retiring: with the batch promoted two steps after its
+    eviction was queued, every step's outputs, the kept positions and the
+    lengths equal, bit for bit, those of a server that admits the same batch
+    serially at the promotion step."""
+    n_req, layers, Hq, Hkv, d, w, pool = 9, 2, 28, 4, 128, 32, 7
+    lag = 2
+    gen = torch.Generator().manual_seed(4242)
+    L = torch.randint(300, 3000, (n_req,), generator=gen).tolist()
+    alphas = (0.9 * torch.rand(n_req, generator=gen, dtype=torch.float64)).tolist()
+    max_new = torch.randint(2, 14, (n_req,), generator=gen).tolist()
+    case(f"server async admission L={L} max_new={max_new}")
+    wl = synth.custom(63, torch.bfloat16, n_req, L, Hq, Hkv, d, w, pool, max(max_new))
+    prompts = [synth.make_prompt(wl, layer, L) for layer in range(layers)]
+    dec = [synth.make_decode(wl, layer) for layer in range(layers)]
+    kw = dict(n_pages=240, max_seqs=5, max_pages=96, Hq=Hq, Hkv=Hkv, d=d, dtype=torch.bfloat16,
+              w=w, pool=pool, max_admit=3, max_prompt=max(L))
+    srv_a, srv_s = Server(layers, **kw), Server(layers, **kw)
+    queue, done_steps, steps = list(range(n_req)), {r: 0 for r in range(n_req)}, 0
+    pend = None                                  # (batch, prompts, step it joins)
+    overlapped = retired_while_pending = 0
+    while queue or srv_a.n_active or pend:
+        for r in srv_a.slots.finished():
+            assert torch.equal(torch.stack(srv_a.keep[r]), torch.stack(srv_s.keep[r]))
+            srv_a.retire([r])
+            srv_s.retire([r])
+            retired_while_pending += pend is not None
+        if pend and steps == pend[2]:
+            batch, pr, _ = pend
+            torch.cuda.synchronize()             # the eviction has finished: the poll sees it
+            assert srv_a.promote_ready() == len(batch)
+            srv_s.admit(batch, [L[r] for r in batch], [alphas[r] for r in batch],
+                        [max_new[r] for r in batch], pr, keep_sets=True)
+            pend = None
+        if pend is None and queue:
+            batch = []
+            while (queue and len(batch) < 3 and srv_a.slots.fits(
+                    [_lib.tb_keep_count(L[r], alphas[r], w) + max_new[r]
+                     for r in batch + [queue[0]]])):
+                batch.append(queue.pop(0))
+            if batch:
+                bl = [L[r] for r in batch]
+                pr = [{key: prompts[layer][key][batch][:, :, :max(bl)].contiguous().to(DEV)
+                       for key in ("k", "v")} for layer in range(layers)]
+                for layer in range(layers):
+                    pr[layer]["q_win"] = prompts[layer]["q_win"][batch].contiguous().to(DEV)
+                srv_a.admit_async(batch, bl, [alphas[r] for r in batch],
+                                  [max_new[r] for r in batch], pr, keep_sets=True)
+                with pytest.raises(RuntimeError):
+                    srv_a.admit(batch, bl, [alphas[r] for r in batch],
+                                [max_new[r] for r in batch], pr)
+                pend = (batch, pr, steps + lag)
+        if srv_a.n_active:
+            assert srv_a.rids() == srv_s.rids()
+            rid, n = srv_a.rids(), srv_a.n_active
+            qs = torch.stack([torch.stack([dec[l]["q"][done_steps[r], r] for r in rid])
+                              for l in range(layers)]).to(DEV)
+            ks = torch.stack([torch.stack([dec[l]["k_new"][done_steps[r], r] for r in rid])
+                              for l in range(layers)]).to(DEV)
+            vs = torch.stack([torch.stack([dec[l]["v_new"][done_steps[r], r] for r in rid])
+                              for l in range(layers)]).to(DEV)
+            out = torch.empty_like(qs)
+            srv_s.step(qs, ks, vs, out)
+            srv_a.q_in[:, :n].copy_(qs)
+            srv_a.k_in[:, :n].copy_(ks)
+            srv_a.v_in[:, :n].copy_(vs)
+            srv_a.step_graphed()
+            overlapped += pend is not None
+            torch.cuda.synchronize()
+            assert torch.equal(out, srv_a.o_out[:, :n]), f"step {steps}: outputs differ"
+            assert torch.equal(srv_a.kv_len[:, :n], srv_s.kv_len[:, :n])
+            for r in rid:
+                done_steps[r] += 1
+        steps += 1
+        assert steps < 300, "stream did not drain"
+    torch.cuda.synchronize()
+    assert all(done_steps[r] == max_new[r] for r in range(n_req))
+    assert overlapped >= 3, "no decode step ran beside an eviction"
+    assert retired_while_pending >= 1, "no retirement happened while a batch was pending"
+    assert len(srv_a.slots.free) == srv_a.slots.n_pages

@@ -1,5 +1,6 @@
 """Host bookkeeping of the paged server (no device): page reservation, dense
-slots, retirement by moving the last request, and the block-table rows."""
+slots, retirement by moving the last request, the block-table rows, and a
+pending (asynchronously evicted) batch in the top slots."""
 import random
 
 import numpy as np
@@ -9,11 +10,12 @@ from paper_2512_21859_amd.serving import PAGE, SlotTable
 
 
 def _invariants(st: SlotTable):
-    owned = [p for e in st.slots for p in e.pages]
+    owned = [p for e in st.slots + st.pending for p in e.pages]
     assert len(owned) == len(set(owned)), "a page is owned twice"
     assert not set(owned) & set(st.free), "a page is both owned and free"
     assert sorted(owned + st.free) == list(range(st.n_pages)), "pages lost or invented"
-    assert len(st.slots) <= st.max_seqs
+    # the running slots [0, n) and the pending ones [max_seqs - p, max_seqs) are disjoint
+    assert len(st.slots) + len(st.pending) <= st.max_seqs
     rows = st.table_rows()
     assert rows.shape == (len(st.slots), st.max_pages)
     for i, e in enumerate(st.slots):
@@ -97,3 +99,69 @@ def test_random_stream_keeps_invariants():
             st.retire(rng.choice(st.slots).rid)
         _invariants(st)
     assert rid > 100
+
+
+def test_pending_batch_takes_top_slots_and_joins_at_the_end():
+    st = SlotTable(n_pages=16, max_seqs=6, max_pages=4)
+    st.admit(1, 40, 4)                                     # pages 0, 1
+    st.admit(2, 10, 4)                                     # page 2
+    top = st.admit_pending([5, 6], [31, 64], [1, 0], [0.5, 0.2], [62, 80])
+    assert top == 4                                        # slots 4, 5
+    assert st.pending_rows().tolist() == [[3, 3, 3, 3], [4, 5, 5, 5]]
+    assert [e.rid for e in st.pending] == [5, 6]
+    _invariants(st)
+    with pytest.raises(RuntimeError):
+        st.admit_pending([7], [1], [0], [0.0], [1])        # one pending batch at a time
+    with pytest.raises(ValueError):
+        st.admit(5, 1, 0)                                  # pending requests count as running
+    assert st.fits([32, 32]) and not st.fits([32, 32, 32])  # 2 free slots left
+    # the running batch keeps stepping and retiring meanwhile
+    st.advance()
+    assert st.retire(1) == 1                               # request 2 moves into slot 0
+    assert [e.rid for e in st.slots] == [2]
+    assert [e.length for e in st.pending] == [31, 64]      # untouched by advance
+    _invariants(st)
+    assert st.promote() == (1, 3)
+    assert [e.rid for e in st.slots] == [2, 5, 6] and not st.pending
+    assert st.lengths().tolist() == [11, 31, 64]
+    assert st.table_rows(1, 3).tolist() == [[3, 3, 3, 3], [4, 5, 5, 5]]
+    _invariants(st)
+
+
+def test_pending_batch_checked_whole():
+    st = SlotTable(n_pages=4, max_seqs=4, max_pages=4)
+    with pytest.raises(MemoryError):
+        st.admit_pending([1, 2], [64, 64], [32, 33], [0, 0], [64, 64])   # 3 + 4 pages > 4
+    assert not st.pending and len(st.free) == 4            # nothing reserved
+    with pytest.raises(ValueError):
+        st.admit_pending([1, 1], [1, 1], [0, 0], [0, 0], [1, 1])         # duplicate request
+    assert not st.pending and len(st.free) == 4
+
+
+def test_random_stream_with_pending_batches():
+    rng = random.Random(11)
+    st = SlotTable(n_pages=64, max_seqs=8, max_pages=12)
+    rid = joined = 0
+    for _ in range(2000):
+        op = rng.random()
+        if op < 0.2 and not st.pending:
+            b = rng.randint(1, 3)
+            nk = [rng.randint(1, 300) for _ in range(b)]
+            mn = [rng.randint(0, 80) for _ in range(b)]
+            if st.fits([k + m for k, m in zip(nk, mn)]):
+                st.admit_pending(list(range(rid, rid + b)), nk, mn, [0.0] * b, nk)
+                rid += b
+        elif op < 0.3 and st.pending:
+            n0 = len(st.slots)
+            lo, hi = st.promote()
+            assert lo == n0 and hi - lo >= 1
+            joined += hi - lo
+        elif op < 0.8 and st.slots:
+            for r in st.finished():
+                st.retire(r)
+            if st.slots:
+                st.advance()
+        elif st.slots:
+            st.retire(rng.choice(st.slots).rid)
+        _invariants(st)
+    assert joined > 100
