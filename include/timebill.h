@@ -164,7 +164,13 @@ tb_status tb_score_h2o(const void* q, const void* k, int32_t B, const int32_t* L
  * ascending to keep_idx followed by the window positions L[b]-w .. L[b]-1.
  * Scores may be any finite floats (-0 equals +0); NaN is not supported.
  * L, alpha: [host][B] inputs.  n_keep: [host][B] output, filled before return.
- * ws: tb_workspace_bytes(TB_OP_SELECT, ...) bytes (currently 0; may be NULL). */
+ * ws (optional): with ws given and some prefix L[b] - w longer than 32768
+ * positions, the prefix is split over several blocks per KV head (same
+ * keep_idx, shorter time); ws must then hold
+ * tb_workspace_bytes(TB_OP_SELECT, B, Lmax, 0, Hkv, 0, w, 0) bytes (4-byte
+ * aligned; contents on entry do not matter), else TB_EWORKSPACE.  With ws
+ * NULL, or every prefix at most 32768 positions, one block per KV head
+ * selects and ws is not touched. */
 tb_status tb_select_topk(const float* scores, int32_t B, const int32_t* L,
                          int32_t Lmax, int32_t Hkv, int32_t w,
                          const double* alpha, int32_t* keep_idx,

@@ -48,6 +48,13 @@ int32_t keep_count(int32_t L, double alpha, int32_t w) {
   return n < w ? w : n;
 }
 
+// Workspace of the several-blocks-per-head selection (prefixes longer than
+// tb::kSelMultiMinPrefix); 0 where every prefix is short enough for one block.
+size_t select_ws(int32_t B, int32_t Lmax, int32_t Hkv, int32_t w) {
+  if (Lmax - w <= tb::kSelMultiMinPrefix) return 0;
+  return static_cast<size_t>(B) * Hkv * tb::kSelWsWords * sizeof(uint32_t);
+}
+
 bool dtype_ok(tb_dtype dt) { return dt == TB_F32 || dt == TB_BF16; }
 int elem_bytes(tb_dtype dt) { return dt == TB_BF16 ? 2 : 4; }
 
@@ -149,7 +156,13 @@ size_t tb_workspace_bytes(int32_t op, int32_t B, int32_t Lmax, int32_t Hq, int32
         }
         return tb::score_ws_bytes(B, Lmax, Hkv, (Hq / Hkv) * w);
       }
-      case TB_OP_SELECT:
+      case TB_OP_SELECT: {
+        if (B < 1 || Lmax < 1 || Hkv < 1 || w < 1) {
+          fail(TB_EINVAL, "tb_workspace_bytes(SELECT): bad sizes");
+          return 0;
+        }
+        return select_ws(B, Lmax, Hkv, w);
+      }
       case TB_OP_COMPACT:
         return 0;
       case TB_OP_H2O: {
@@ -333,7 +346,6 @@ tb_status tb_score_knorm(const void* k, int32_t B, const int32_t* L, int32_t Lma
 tb_status tb_select_topk(const float* scores, int32_t B, const int32_t* L, int32_t Lmax,
                          int32_t Hkv, int32_t w, const double* alpha, int32_t* keep_idx,
                          int32_t* n_keep, void* ws, size_t ws_bytes, hipStream_t stream) {
-  (void)ws; (void)ws_bytes;
   try {
     if (!scores || !L || !alpha || !keep_idx || !n_keep)
       return fail(TB_EINVAL, "tb_select_topk: null pointer");
@@ -352,8 +364,17 @@ tb_status tb_select_topk(const float* scores, int32_t B, const int32_t* L, int32
     }
     a.scores = scores; a.keep_idx = keep_idx;
     a.B = B; a.Lmax = Lmax; a.Hkv = Hkv; a.w = w;
+    int max_pref = 0;
+    for (int b = 0; b < B; ++b) max_pref = std::max(max_pref, L[b] - w);
+    const size_t need = select_ws(B, Lmax, Hkv, w);
+    const bool multi = ws != nullptr && max_pref > tb::kSelMultiMinPrefix;
+    if (multi && ws_bytes < need)
+      return fail(TB_EWORKSPACE, "tb_select_topk: workspace %zu bytes < %zu", ws_bytes, need);
+    if (multi && reinterpret_cast<uintptr_t>(ws) % 4 != 0)
+      return fail(TB_EINVAL, "tb_select_topk: workspace must be 4-byte aligned");
     for (int b = 0; b < B; ++b) n_keep[b] = a.n_keep[b];
-    return hip_status(tb::launch_select(a, stream), "tb_select_topk launch");
+    return hip_status(multi ? tb::launch_select_multi(a, ws, stream) : tb::launch_select(a, stream),
+                      "tb_select_topk launch");
   } catch (...) {
     return fail(TB_EINTERNAL, "tb_select_topk: internal error");
   }

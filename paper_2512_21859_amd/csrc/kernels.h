@@ -78,6 +78,13 @@ struct SelectArgs {
   int32_t n_keep[kMaxB];
 };
 hipError_t launch_select(const SelectArgs& a, hipStream_t st);
+// Several blocks per (sequence, KV head); ws holds kSelWsWords 32-bit words per
+// unit, B * Hkv units.
+constexpr int kSelMaxChunks = 32;
+constexpr int kSelWsWords = 4 * kSelMaxChunks + 8 + 3 * 2048;
+constexpr int kSelMultiMinPrefix = 32768;   // longer prefixes go to several blocks
+int select_chunks(int max_pref);
+hipError_t launch_select_multi(const SelectArgs& a, void* ws, hipStream_t st);
 
 // ---------------------------------------------------------------- compaction
 struct CompactArgs {

@@ -44,6 +44,9 @@ class Evictor:
         else:
             nbytes = _lib.tb_workspace_bytes(_lib.TB_OP_SCORE, B, Lmax, Hq, Hkv, d, w, 0)
         self.ws = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=device)
+        # long prefixes select with several blocks per KV head, which needs this
+        sel = _lib.tb_workspace_bytes(_lib.TB_OP_SELECT, B, Lmax, Hq, Hkv, d, w, 0)
+        self.sel_ws = torch.empty((sel,), dtype=torch.uint8, device=device) if sel else None
 
     def score(self, q_win: torch.Tensor, k: torch.Tensor, L: Sequence[int], stream=None) -> None:
         if self.scorer == "knorm":
@@ -55,7 +58,8 @@ class Evictor:
                                  stream, avgpool=self.scorer == "snapkv_avg")
 
     def select(self, L: Sequence[int], alphas: Sequence[float], stream=None):
-        return _lib.tb_select_topk(self.scores, L, self.w, alphas, self.keep_idx, None, stream)
+        return _lib.tb_select_topk(self.scores, L, self.w, alphas, self.keep_idx, self.sel_ws,
+                                   stream)
 
     def evict(self, q_win, k, v, L, alphas, cache: "_lib.KVCache", stream=None):
         """Score, select and compact into ``cache``; returns n_keep per sequence."""

@@ -229,6 +229,8 @@ class Server:
         self.keep_buf = torch.empty((n,), dtype=torch.int32, device=device)
         sc = _lib.tb_workspace_bytes(_lib.TB_OP_SCORE, max_admit, max_prompt, Hq, Hkv, d, w, 0)
         self.score_ws = torch.empty((max(sc, 1),), dtype=torch.uint8, device=device)
+        sel = _lib.tb_workspace_bytes(_lib.TB_OP_SELECT, max_admit, max_prompt, Hq, Hkv, d, w, 0)
+        self.sel_ws = torch.empty((sel,), dtype=torch.uint8, device=device) if sel else None
         self.keep: Dict[int, List[torch.Tensor]] = {}       # rid -> per-layer keep_idx (kept on request)
         # static decode inputs / outputs for graph replay: row i = slot i
         self.q_in = torch.zeros((n_layers, max_seqs, Hq, d), dtype=dtype, device=device)
@@ -346,7 +348,7 @@ class Server:
         for layer, p in enumerate(prompts):
             _lib.tb_score_window(p["q_win"], p["k"], L, self.w, self.pool, scores, None,
                                  self.score_ws, stream)
-            got = _lib.tb_select_topk(scores, L, self.w, alphas, keep, None, stream)
+            got = _lib.tb_select_topk(scores, L, self.w, alphas, keep, self.sel_ws, stream)
             if got != n_keep:
                 raise RuntimeError(f"select kept {got}, expected {n_keep}")
             _lib.tb_compact_kv_paged(p["k"], p["v"], keep, n_keep, self.k_pool[layer],

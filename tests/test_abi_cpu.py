@@ -60,6 +60,12 @@ def test_workspace_sizes(lib):
     s = _lib.tb_workspace_bytes(_lib.TB_OP_SCORE, 1, 8192, 28, 4, 128, 32, 0)
     assert s >= 4 * 128 * 224 * 64 * 4                     # the per-tile exponentials
     assert _lib.tb_workspace_bytes(_lib.TB_OP_SELECT, 1, 8192, 28, 4, 128, 32, 0) == 0
+    # prefixes past 32768 positions may select with several blocks per head
+    assert _lib.tb_workspace_bytes(_lib.TB_OP_SELECT, 1, 32768 + 32, 0, 4, 0, 32, 0) == 0
+    sel = _lib.tb_workspace_bytes(_lib.TB_OP_SELECT, 3, 32768 + 33, 0, 4, 0, 32, 0)
+    assert sel > 0 and sel % (3 * 4) == 0
+    assert sel == _lib.tb_workspace_bytes(_lib.TB_OP_SELECT, 3, 131072, 0, 4, 0, 64, 0)
+    assert _lib.tb_workspace_bytes(_lib.TB_OP_SELECT, 0, 131072, 0, 4, 0, 64, 0) == 0
     d = _lib.tb_workspace_bytes(_lib.TB_OP_DECODE, 1, 0, 28, 4, 128, 0, 8448)
     assert d > 8 and d % 256 == 0
     assert _lib.tb_workspace_bytes(_lib.TB_OP_DECODE, 1, 0, 28, 5, 128, 0, 8448) == 0
@@ -198,6 +204,26 @@ def test_select_validation(lib):
     assert call(w=100) == E.TB_EINVAL
     assert call(B=0) == E.TB_EINVAL
     assert call(keep=None) == E.TB_EINVAL
+
+
+def test_select_workspace_validation(lib):
+    """A workspace is needed only where a prefix is long enough for several
+    blocks per head; then it must be large enough and aligned.  Checked
+    before anything is enqueued."""
+    E = _lib
+    n_keep = (ctypes.c_int32 * 2)()
+    L, w, Hkv = [40000, 20000], 32, 2            # the first prefix (39968) is long enough
+    need = _lib.tb_workspace_bytes(_lib.TB_OP_SELECT, 2, 40000, 0, Hkv, 0, w, 0)
+
+    def call(ws, nbytes, L=L):
+        a = (ctypes.c_double * 2)(0.5, 0.5)
+        return lib.tb_select_topk(FAKE, 2, _i32(*L), 40000, Hkv, w, a, FAKE, n_keep,
+                                  ws, nbytes, None)
+
+    assert call(FAKE, need - 1) == E.TB_EWORKSPACE
+    assert b"workspace" in lib.tb_last_error()
+    assert call(ctypes.c_void_p(0x1002), need) == E.TB_EINVAL          # misaligned
+    assert b"aligned" in lib.tb_last_error()
 
 
 def test_compact_validation(lib):

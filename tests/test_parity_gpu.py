@@ -117,19 +117,33 @@ def test_compact_exact(dtype, d):
 
 # ------------------------------------------------------------------ selection
 def _select_case(pooled64: np.ndarray, L, w, alphas, where):
-    """pooled64 [B, Hkv, Lmax] float64 (prefix entries valid); GPU selects on fp32."""
+    """pooled64 [B, Hkv, Lmax] float64 (prefix entries valid); GPU selects on fp32.
+    Where some prefix is long enough, the several-blocks-per-head path (given a
+    workspace) is run as well; both must give the oracle's keep_idx and leave
+    the entries past n_keep untouched."""
     B, Hkv, Lmax = pooled64.shape
     p32 = torch.from_numpy(pooled64).to(torch.float32)
-    keep = torch.full((B, Hkv, Lmax), -1, dtype=torch.int32, device=DEV)
-    n_keep = _lib.tb_select_topk(p32.to(DEV), L, w, alphas, keep)
-    torch.cuda.synchronize()
-    kk = keep.cpu().numpy()
     p32_64 = p32.to(torch.float64).numpy()
+    ref = {}
     for b in range(B):
-        assert n_keep[b] == O.keep_count(L[b], alphas[b], w)
+        nk = O.keep_count(L[b], alphas[b], w)
         for gg in range(Hkv):
-            ref = O.select_keep(p32_64[b, gg, : L[b] - w], L[b], w, n_keep[b])
-            assert np.array_equal(kk[b, gg, : n_keep[b]], ref), f"{where} b={b} g={gg}"
+            ref[b, gg] = O.select_keep(p32_64[b, gg, : L[b] - w], L[b], w, nk)
+    nbytes = _lib.tb_workspace_bytes(_lib.TB_OP_SELECT, B, Lmax, 0, Hkv, 0, w, 0)
+    multi = nbytes > 0 and max(L) - w > 32768
+    for ws in ([None, torch.full((nbytes,), 0xA5, dtype=torch.uint8, device=DEV)]
+               if multi else [None]):
+        keep = torch.full((B, Hkv, Lmax), -1, dtype=torch.int32, device=DEV)
+        n_keep = _lib.tb_select_topk(p32.to(DEV), L, w, alphas, keep, ws)
+        torch.cuda.synchronize()
+        kk = keep.cpu().numpy()
+        path = "one block per head" if ws is None else "several blocks per head"
+        for b in range(B):
+            assert n_keep[b] == O.keep_count(L[b], alphas[b], w)
+            for gg in range(Hkv):
+                assert np.array_equal(kk[b, gg, : n_keep[b]], ref[b, gg]), \
+                    f"{where} b={b} g={gg} ({path})"
+                assert (kk[b, gg, n_keep[b]:] == -1).all(), f"{where} b={b} g={gg}: wrote past n_keep"
 
 
 def test_select_exact_on_oracle_scores():
@@ -173,6 +187,43 @@ def test_select_exact_long_prefix_and_wide_range():
         pooled[b, :, :n] = x
     for alphas in ([0.0, 0.3], [0.5, 0.9], [0.999, 0.01]):
         _select_case(pooled, L, w, alphas, f"alphas={alphas}")
+
+
+def _pooled_heavy_tail(rng, n_rows, n, pool=7):
+    """Window-score-like prefixes: heavy-tailed attention mass, max-pooled."""
+    a = np.exp(3.0 * rng.standard_normal((n_rows, n)))
+    a[:, rng.integers(0, n, max(1, n // 500))] *= 100.0
+    a = a / a.sum(axis=1, keepdims=True) * 224.0
+    out = a.copy()
+    for s in range(1, pool // 2 + 1):
+        out[:, s:] = np.maximum(out[:, s:], a[:, :-s])
+        out[:, :-s] = np.maximum(out[:, :-s], a[:, s:])
+    return out
+
+
+@pytest.mark.parametrize("kind", ["window", "knorm", "levels3"])
+def test_select_several_blocks_per_head(kind):
+    """Long prefixes split over several blocks per KV head: a ragged batch in
+    which a short sequence and one just past the split threshold ride along
+    with a 131072-position one (the split applies above 32768 prefix
+    positions; shorter prefixes of the batch take it too); ratios from none evicted (every prefix
+    position kept) to a single selected position."""
+    case(f"select, several blocks per head, {kind} scores")
+    rng = np.random.default_rng({"window": 1, "knorm": 2, "levels3": 3}[kind])
+    B, Hkv, w = 3, 2, 32
+    L = [131072, 32768 + w + 1, 5000]
+    pooled = np.zeros((B, Hkv, max(L)))
+    for b in range(B):
+        n = L[b] - w
+        if kind == "window":
+            pooled[b, :, :n] = _pooled_heavy_tail(rng, Hkv, n)
+        elif kind == "knorm":        # negated key norms
+            pooled[b, :, :n] = -np.sqrt(rng.chisquare(128, (Hkv, n)))
+        else:
+            pooled[b, :, :n] = rng.integers(0, 3, (Hkv, n)) / 4.0
+    for alphas in ([0.5, 0.5, 0.5], [0.0, 0.9, 0.3], [0.95, 0.0, 0.999],
+                   [1.0 - (w + 1) / L[0] + 1e-12, 0.25, 0.75]):   # first: n_keep = w + 1
+        _select_case(pooled, L, w, alphas, f"{kind} alphas={alphas}")
 
 
 def test_select_exact_narrow_range():
