@@ -78,5 +78,11 @@ __device__ __forceinline__ uint4 ldg16(const void* p) {
 __device__ __forceinline__ void stg16(void* p, const uint4& v) {
   *reinterpret_cast<uint4*>(p) = v;
 }
+// Streaming (non-temporal) 16-byte store: for outputs written once and not
+// read back soon, so they do not displace cached data on their way to HBM.
+__device__ __forceinline__ void stg16_stream(void* p, const uint4& v) {
+  typedef unsigned int u32x4n __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store(__builtin_bit_cast(u32x4n, v), static_cast<u32x4n*>(p));
+}
 
 }  // namespace tb

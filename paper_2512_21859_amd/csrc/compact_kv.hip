@@ -9,7 +9,10 @@
 //     [d][32] (contiguous 16-byte stores of 8 (bf16) or 4 (fp32) keys of one
 //     column); slots past n_keep are zero-filled.
 // All loads of a thread are issued before its stores.  HBM traffic is one read
-// and one write of each kept row of K and V.
+// and one write of each kept row of K and V.  The cache writes are streaming
+// (non-temporal) stores: measured at L = 131072, 8 KV heads, half the rows
+// kept, 80 us against 104 us with ordinary stores (6.7 against 5.2 TB/s);
+// non-temporal loads of the gathered rows did not help.
 
 #include "common.h"
 #include "kernels.h"
@@ -62,7 +65,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
 #pragma unroll
   for (int p = 0; p < PASSES; ++p) {
     const int rr = r0 + p * ROWS_PER_PASS;
-    if (i0 + rr < n) stg16(kd + static_cast<size_t>(rr) * ROW_BYTES, kr[p]);
+    if (i0 + rr < n) stg16_stream(kd + static_cast<size_t>(rr) * ROW_BYTES, kr[p]);
     *reinterpret_cast<uint4*>(&s_v[rr][part * EPV]) = vr[p];   // zero past n_keep
   }
   __syncthreads();
@@ -73,8 +76,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
     T vals[EPV];
 #pragma unroll
     for (int e = 0; e < EPV; ++e) vals[e] = s_v[k0 + e][d];
-    *reinterpret_cast<uint4*>(vtile + static_cast<size_t>(d) * kVT + k0) =
-        *reinterpret_cast<const uint4*>(vals);
+    stg16_stream(vtile + static_cast<size_t>(d) * kVT + k0, *reinterpret_cast<const uint4*>(vals));
   }
 }
 
