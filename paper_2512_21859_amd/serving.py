@@ -32,6 +32,7 @@ computation runs in the kernels.
 """
 from __future__ import annotations
 
+import contextlib
 from dataclasses import dataclass
 from typing import Dict, List, Optional, Sequence
 
@@ -138,6 +139,12 @@ class SlotTable:
         for i, r in enumerate(rids):
             self.pending.append(self._reserve(r, n_keep[i], max_new[i], alphas[i], n_x[i]))
         return self.max_seqs - len(self.pending)
+
+    def cancel_pending(self) -> None:
+        """Drop the pending batch and free its pages."""
+        for e in reversed(self.pending):
+            self.free.extend(reversed(e.pages))
+        self.pending = []
 
     def pending_rows(self) -> np.ndarray:
         """Block-table rows of the pending slots, in slot order."""
@@ -303,7 +310,9 @@ class Server:
         already queued on the current stream (which may have produced the
         prompts, or still read pages freed by a retirement).  The new requests
         hold the top slots of the table until promote_ready() moves them into
-        the running batch; only one such batch may be pending."""
+        the running batch (their kept sets, with keep_sets, are complete by
+        then); only one such batch may be pending.  If queueing the eviction
+        fails, the batch is dropped and its pages freed."""
         if self.slots.pending:
             raise RuntimeError("an asynchronous admission is already pending")
         n_keep = self._check_admission(rids, L, alphas, max_new, prompts)
@@ -311,15 +320,25 @@ class Server:
         if self._adm_stream is None:
             self._adm_stream = torch.cuda.Stream()
         adm = self._adm_stream
-        adm.wait_stream(torch.cuda.current_stream())
-        self._staging.put(self.table[top:top + len(rids)], self.slots.pending_rows(), adm)
-        self._adm_refs = [x for p in prompts for x in p.values()]
-        for x in self._adm_refs:            # the allocator must not reuse them before adm is done
-            x.record_stream(adm)
-        with torch.cuda.stream(adm):
+        cur = torch.cuda.current_stream()
+        adm.wait_stream(cur)
+        try:
+            self._staging.put(self.table[top:top + len(rids)], self.slots.pending_rows(), adm)
+            self._adm_refs = [x for p in prompts for x in p.values()]
+            for x in self._adm_refs:        # the allocator must not reuse them before adm is done
+                x.record_stream(adm)
             self._evict(rids, L, alphas, n_keep, prompts, top, keep_sets, adm)
             self._adm_done = torch.cuda.Event()
             self._adm_done.record(adm)
+        except BaseException:
+            # whatever was queued may still write the batch's pages: later work
+            # on the current stream waits for it before the pages are reused
+            cur.wait_stream(adm)
+            for r in rids:
+                self.keep.pop(r, None)
+            self.slots.cancel_pending()
+            self._adm_refs = []
+            raise
         return n_keep
 
     def promote_ready(self, wait: bool = False, stream=None) -> int:
@@ -340,7 +359,12 @@ class Server:
 
     def _evict(self, rids, L, alphas, n_keep, prompts, lo, keep_sets, stream) -> None:
         """Score, select and compact every layer of the requests in slots
-        lo..lo+b-1, whose table rows are already on the device."""
+        lo..lo+b-1, whose table rows are already on the device; everything,
+        the copies of the kept sets included, is queued on `stream`."""
+        with torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext():
+            self._evict_layers(rids, L, alphas, n_keep, prompts, lo, keep_sets, stream)
+
+    def _evict_layers(self, rids, L, alphas, n_keep, prompts, lo, keep_sets, stream) -> None:
         b = len(rids)
         Lmax = prompts[0]["k"].shape[2]
         scores = self.scores_buf[: b * self.Hkv * Lmax].view(b, self.Hkv, Lmax)

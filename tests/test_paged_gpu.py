@@ -352,3 +352,42 @@ def test_server_async_admission_equals_serialized():
     assert overlapped >= 3, "no decode step ran beside an eviction"
     assert retired_while_pending >= 1, "no retirement happened while a batch was pending"
     assert len(srv_a.slots.free) == srv_a.slots.n_pages
+
+
+def test_server_async_admission_rolls_back_on_error():
+    """An admission whose eviction fails while being queued (layer 1's keys
+    in the wrong dtype, caught on the host after layer 0 was queued) leaves
+    nothing pending and every page free; the same batch admitted correctly
+    afterwards decodes exactly as on a server that never saw the failure."""
+    n_req, layers, Hq, Hkv, d, w, pool = 3, 2, 28, 4, 128, 32, 7
+    L, alphas, max_new = [900, 1500, 700], [0.5, 0.2, 0.8], [3, 3, 3]
+    case(f"server async admission rollback L={L}")
+    wl = synth.custom(64, torch.bfloat16, n_req, L, Hq, Hkv, d, w, pool, max(max_new))
+    prompts = [synth.make_prompt(wl, layer, L) for layer in range(layers)]
+    dec = [synth.make_decode(wl, layer) for layer in range(layers)]
+    kw = dict(n_pages=120, max_seqs=4, max_pages=48, Hq=Hq, Hkv=Hkv, d=d, dtype=torch.bfloat16,
+              w=w, pool=pool, max_admit=3, max_prompt=max(L))
+    srv, ref = Server(layers, **kw), Server(layers, **kw)
+    rids = list(range(n_req))
+    pr = [{key: prompts[layer][key].contiguous().to(DEV) for key in ("q_win", "k", "v")}
+          for layer in range(layers)]
+    bad = [dict(pr[0]), dict(pr[1])]
+    bad[1]["k"] = bad[1]["k"].float()
+    with pytest.raises(ValueError):
+        srv.admit_async(rids, L, alphas, max_new, bad, keep_sets=True)
+    assert not srv.slots.pending and not srv.keep
+    assert len(srv.slots.free) == srv.slots.n_pages
+    srv.admit_async(rids, L, alphas, max_new, pr, keep_sets=True)
+    assert srv.promote_ready(wait=True) == n_req
+    ref.admit(rids, L, alphas, max_new, pr, keep_sets=True)
+    for t in range(max(max_new)):
+        qs = torch.stack([dec[l]["q"][t, :n_req] for l in range(layers)]).to(DEV)
+        ks = torch.stack([dec[l]["k_new"][t, :n_req] for l in range(layers)]).to(DEV)
+        vs = torch.stack([dec[l]["v_new"][t, :n_req] for l in range(layers)]).to(DEV)
+        o1, o2 = torch.empty_like(qs), torch.empty_like(qs)
+        srv.step(qs, ks, vs, o1)
+        ref.step(qs, ks, vs, o2)
+        torch.cuda.synchronize()
+        assert torch.equal(o1, o2), f"step {t}"
+    for r in rids:
+        assert torch.equal(torch.stack(srv.keep[r]), torch.stack(ref.keep[r]))

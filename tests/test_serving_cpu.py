@@ -128,6 +128,18 @@ def test_pending_batch_takes_top_slots_and_joins_at_the_end():
     _invariants(st)
 
 
+def test_pending_batch_cancel_frees_its_pages():
+    st = SlotTable(n_pages=8, max_seqs=4, max_pages=4)
+    st.admit(1, 40, 0)                                     # pages 0, 1
+    free0 = list(st.free)
+    st.admit_pending([2, 3], [64, 1], [0, 31], [0.0, 0.0], [64, 1])
+    assert not set(free0) <= set(st.free)
+    st.cancel_pending()
+    assert not st.pending and sorted(st.free) == sorted(free0)
+    _invariants(st)
+    assert st.admit_pending([2], [1], [0], [0.0], [1]) == 3   # a new batch may follow
+
+
 def test_pending_batch_checked_whole():
     st = SlotTable(n_pages=4, max_seqs=4, max_pages=4)
     with pytest.raises(MemoryError):
