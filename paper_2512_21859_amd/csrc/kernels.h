@@ -26,6 +26,7 @@ struct ScoreArgs {
   float* raw;             // raw scores: raw_scores if given, else ws [B][Hkv][Lmax]
   int32_t B, Lmax, Hq, Hkv, w, pool, R, n_tiles, row_chunks;
   int32_t pool_avg;       // 0: max-pool, 1: mean over the window (zeros outside the prefix)
+  int32_t stream_e;       // set by launch_score: e written with streaming stores
   double scale;           // 1/sqrt(d)
   int32_t L[kMaxB];
 };

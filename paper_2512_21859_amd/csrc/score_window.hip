@@ -40,6 +40,7 @@ namespace tb {
 namespace {
 
 typedef __attribute__((ext_vector_type(4))) double f64x4;
+typedef __attribute__((ext_vector_type(4))) float f32x4n;
 
 constexpr int kThreads = 256;
 constexpr int kT = kScoreTile;     // keys per tile (64)
@@ -236,8 +237,10 @@ __global__ __launch_bounds__(kTilesThreads, 2) void score_tiles_kernel(ScoreArgs
       const double z = row16_sum_f64(static_cast<double>(zs));
       const int rg = row0 + rl;
       if (rg < R) {
-        *reinterpret_cast<float4*>(ebase + static_cast<size_t>(rg) * kT + 4 * r16) =
-            make_float4(ev[0], ev[1], ev[2], ev[3]);
+        float* dst = ebase + static_cast<size_t>(rg) * kT + 4 * r16;
+        if (a.stream_e) __builtin_nontemporal_store(f32x4n{ev[0], ev[1], ev[2], ev[3]},
+                                                    reinterpret_cast<f32x4n*>(dst));
+        else            *reinterpret_cast<float4*>(dst) = make_float4(ev[0], ev[1], ev[2], ev[3]);
         if (r16 == 0) {
           const size_t o = (bg * R + rg) * a.n_tiles + tile;
           a.tile_m[o] = md * a.scale;       // -inf when the whole row-tile is masked
@@ -380,7 +383,14 @@ size_t score_ws_bytes(int B, int Lmax, int Hkv, int R) {
   return bytes;
 }
 
-hipError_t launch_score(const ScoreArgs& a, int d, bool bf16, hipStream_t st) {
+hipError_t launch_score(const ScoreArgs& args, int d, bool bf16, hipStream_t st) {
+  // Exponentials larger than the 256 MB last-level cache cannot stay there for
+  // K3 anyway: write them with streaming stores (at L = 131072, 8 KV heads,
+  // 1.07 GB: K1 ~4% faster); smaller ones are written normally so that K3
+  // finds them cached (streaming them cost ~2 us per call at L = 8192).
+  ScoreArgs a = args;
+  const double e_bytes = 4.0 * kT * a.R * a.n_tiles * a.Hkv * a.B;
+  a.stream_e = e_bytes > 256.0 * (1 << 20);
   const dim3 g1(a.n_tiles * a.row_chunks, a.Hkv, a.B);
   if (bf16) {
     if (d == 128) score_tiles_kernel<bf16_t, 128><<<g1, kTilesThreads, 0, st>>>(a);

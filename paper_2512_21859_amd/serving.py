@@ -246,7 +246,13 @@ class Server:
         self.o_out = torch.zeros((n_layers, max_seqs, Hq, d), dtype=dtype, device=device)
         self._graphs: Dict[int, torch.cuda.CUDAGraph] = {}
         self._staging = _Staging(8, 4 * max(n_layers, max_pages) * max_seqs)
-        self._adm_stream: Optional[torch.cuda.Stream] = None
+        # Two streams taken together for overlapped admission: decode steps on
+        # decode_stream, evictions on the admission stream.  Streams share a
+        # few hardware queues, and two streams on one queue run one after the
+        # other; streams taken one after the other from torch's pool sit on
+        # different queues, where streams taken at unrelated times may not.
+        self.decode_stream = torch.cuda.Stream(device=device)
+        self._adm_stream = torch.cuda.Stream(device=device)
         self._adm_done: Optional[torch.cuda.Event] = None
         self._adm_refs: List[torch.Tensor] = []
 
@@ -306,7 +312,9 @@ class Server:
                     max_new: Sequence[int], prompts: Sequence[dict],
                     keep_sets: bool = False) -> List[int]:
         """admit(), with the eviction on a separate stream so that decode steps
-        queued meanwhile run alongside it.  The eviction starts after the work
+        queued meanwhile run alongside it (queue them on decode_stream: a
+        stream created at another time may share the admission stream's
+        hardware queue and then runs after it).  The eviction starts after the work
         already queued on the current stream (which may have produced the
         prompts, or still read pages freed by a retirement).  The new requests
         hold the top slots of the table until promote_ready() moves them into
@@ -317,8 +325,6 @@ class Server:
             raise RuntimeError("an asynchronous admission is already pending")
         n_keep = self._check_admission(rids, L, alphas, max_new, prompts)
         top = self.slots.admit_pending(rids, n_keep, max_new, alphas, L)
-        if self._adm_stream is None:
-            self._adm_stream = torch.cuda.Stream()
         adm = self._adm_stream
         cur = torch.cuda.current_stream()
         adm.wait_stream(cur)

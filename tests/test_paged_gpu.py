@@ -290,6 +290,12 @@ def test_server_async_admission_equals_serialized():
     kw = dict(n_pages=240, max_seqs=5, max_pages=96, Hq=Hq, Hkv=Hkv, d=d, dtype=torch.bfloat16,
               w=w, pool=pool, max_admit=3, max_prompt=max(L))
     srv_a, srv_s = Server(layers, **kw), Server(layers, **kw)
+    with torch.cuda.stream(srv_a.decode_stream):  # steps on a queue of their own
+        _async_vs_serial(srv_a, srv_s, L, alphas, max_new, prompts, dec, layers, w, lag)
+
+
+def _async_vs_serial(srv_a, srv_s, L, alphas, max_new, prompts, dec, layers, w, lag):
+    n_req = len(L)
     queue, done_steps, steps = list(range(n_req)), {r: 0 for r in range(n_req)}, 0
     pend = None                                  # (batch, prompts, step it joins)
     overlapped = retired_while_pending = 0
