@@ -226,6 +226,24 @@ def test_select_several_blocks_per_head(kind):
         _select_case(pooled, L, w, alphas, f"{kind} alphas={alphas}")
 
 
+def test_select_several_blocks_max_batch():
+    """64 sequences (the largest batch) with prefixes from 1 to 40000
+    positions, so most rows of the launch grid are short or early-exit units
+    beside a few long ones, under one shared workspace."""
+    case("select, several blocks per head, 64 ragged sequences")
+    rng = np.random.default_rng(64)
+    B, Hkv, w = 64, 2, 16
+    L = [int(x) for x in rng.integers(w + 1, 40001, B)]
+    L[0], L[1] = 40000, w + 1
+    pooled = np.zeros((B, Hkv, max(L)))
+    for b in range(B):
+        n = L[b] - w
+        pooled[b, :, :n] = rng.integers(0, 1000, (Hkv, n)) / 64.0   # many ties
+    alphas = [float(a) for a in rng.uniform(0.0, 0.99, B)]
+    alphas[2] = 0.0
+    _select_case(pooled, L, w, alphas, "max batch")
+
+
 def test_select_exact_narrow_range():
     case("select on keys that share all but their lowest bits")
     rng = np.random.default_rng(5)
