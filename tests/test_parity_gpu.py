@@ -244,6 +244,33 @@ def test_select_several_blocks_max_batch():
     _select_case(pooled, L, w, alphas, "max batch")
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_select_several_blocks_random_shapes(seed):
+    """Seeded random batches whose longest prefix needs several blocks per
+    head: batch size, heads, window, lengths, ratios and the score
+    distribution (continuous, heavy ties, negative, all equal) drawn per case."""
+    rng = np.random.default_rng(1000 + seed)
+    B, Hkv, w = int(rng.integers(1, 5)), int(rng.integers(1, 4)), int(rng.integers(1, 65))
+    L = [int(x) for x in rng.integers(w + 1, 90001, B)]
+    L[int(rng.integers(0, B))] = int(rng.integers(32768 + w + 1, 90001))
+    kind = ["normal", "ties", "negative", "equal"][seed % 4]
+    case(f"select random shapes seed={seed} B={B} Hkv={Hkv} w={w} L={L} kind={kind}")
+    pooled = np.zeros((B, Hkv, max(L)))
+    for b in range(B):
+        n = L[b] - w
+        if kind == "normal":
+            x = np.exp(rng.normal(0.0, 2.0, (Hkv, n)))
+        elif kind == "ties":
+            x = rng.integers(0, 7, (Hkv, n)) * 0.25
+        elif kind == "negative":
+            x = -np.abs(rng.normal(0.0, 1.0, (Hkv, n)))
+        else:
+            x = np.full((Hkv, n), 0.375)
+        pooled[b, :, :n] = x
+    alphas = [float(a) for a in rng.uniform(0.0, 0.999, B)]
+    _select_case(pooled, L, w, alphas, f"seed={seed}")
+
+
 def test_select_exact_narrow_range():
     case("select on keys that share all but their lowest bits")
     rng = np.random.default_rng(5)
