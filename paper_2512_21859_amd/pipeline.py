@@ -8,7 +8,8 @@ retained length follows Eq. N_kv).  This module only allocates device buffers
 """
 from __future__ import annotations
 
-from typing import Optional, Sequence
+from dataclasses import dataclass
+from typing import List, Optional, Sequence, Tuple
 
 import torch
 
@@ -92,3 +93,31 @@ def choose_alpha(prefill_abc, step_pq, n_x: int, n_hat: int, bucket: int, k: int
     alpha, feasible = _lib.tb_alpha_star(prefill_abc, step_pq, float(n_x), n_hat_w, budget,
                                          t_predict, alpha_max)
     return alpha, feasible, n_hat_w
+
+
+@dataclass(frozen=True)
+class TimeModel:
+    """What the controller plans with (Sec. 5.1, Sec. 5.2): the prefill time
+    a N^2 + b N + c and the decode-step time p N_kv + q (coefficients from
+    tb_ete_fit over measured runs), the predictor's bucket size, the pessimism
+    factor k, the response-length cap N_max, the predictor's own time and the
+    largest ratio the deployment allows."""
+    prefill_abc: Tuple[float, float, float]
+    step_pq: Tuple[float, float]
+    bucket: int
+    k: int
+    n_max: int
+    t_predict: float = 0.0
+    alpha_max: float = 0.95
+
+
+def plan_requests(model: TimeModel, n_x: Sequence[int], budgets: Sequence[float],
+                  n_hat: Sequence[int]) -> List[Tuple[float, bool, int]]:
+    """choose_alpha for each request: (alpha*, feasible, N_hat_W).  A request
+    whose budget cannot be met gets alpha_max with feasible False (it runs
+    with the most eviction the deployment allows)."""
+    if not (len(n_x) == len(budgets) == len(n_hat)):
+        raise ValueError("n_x, budgets and n_hat must have one entry per request")
+    return [choose_alpha(model.prefill_abc, model.step_pq, int(n), int(nh), model.bucket,
+                         model.k, model.n_max, float(T), model.t_predict, model.alpha_max)
+            for n, T, nh in zip(n_x, budgets, n_hat)]

@@ -19,6 +19,10 @@ Pages are reserved at admission for the retained prompt plus the request's
 whole response (max_new tokens), so a running request never waits for pages
 and nothing is preempted.
 
+Requests can be admitted by time budget (Server.admit_budgets): the
+controller gives each its ratio alpha* and pessimistic response length, as the
+paper does for a single request.
+
 Admission can also overlap decoding (Server.admit_async): the new batch's
 eviction runs on a stream of its own into the top slots of the table, which
 no decode step reads (a step reads slots 0..n-1 only), and the batch joins the
@@ -40,6 +44,7 @@ import numpy as np
 import torch
 
 from . import _lib
+from .pipeline import TimeModel, plan_requests
 
 PAGE = _lib.V_TILE          # rows per page: one 32-row tile of every KV head
 
@@ -362,6 +367,24 @@ class Server:
         self._upload(lo, hi, lengths=True, stream=stream)
         self._adm_refs = []
         return hi - lo
+
+    def admit_budgets(self, rids: Sequence[int], L: Sequence[int], budgets: Sequence[float],
+                      n_hat: Sequence[int], model: TimeModel, prompts: Sequence[dict],
+                      keep_sets: bool = False, overlap: bool = False):
+        """Admit requests by time budget (Sec. 5.2, applied per request): each
+        gets the smallest ratio alpha* whose worst-case time (prefill, then
+        N_hat_W decode steps over the retained KV) fits its budget, and pages
+        for N_hat_W new tokens (the pessimistic response length from its
+        predicted bucket n_hat).  overlap=True admits through admit_async.
+        Returns [(alpha, feasible, N_hat_W)] per request."""
+        plan = plan_requests(model, L, budgets, n_hat)
+        alphas = [a for a, _, _ in plan]
+        max_new = [w for _, _, w in plan]
+        if overlap:
+            self.admit_async(rids, L, alphas, max_new, prompts, keep_sets=keep_sets)
+        else:
+            self.admit(rids, L, alphas, max_new, prompts, keep_sets=keep_sets)
+        return plan
 
     def _evict(self, rids, L, alphas, n_keep, prompts, lo, keep_sets, stream) -> None:
         """Score, select and compact every layer of the requests in slots

@@ -397,3 +397,56 @@ def test_server_async_admission_rolls_back_on_error():
         assert torch.equal(o1, o2), f"step {t}"
     for r in rids:
         assert torch.equal(torch.stack(srv.keep[r]), torch.stack(ref.keep[r]))
+
+
+@pytest.mark.parametrize("overlap", [False, True])
+def test_server_admits_by_budget(overlap):
+    """Requests admitted by time budget carry the controller's ratio and
+    pessimistic length: each keeps keep_count(L, alpha*) rows under the
+    selection acceptance rule, reserves N_hat_W steps, and its first decode
+    step matches the oracle over the kept rows."""
+    from paper_2512_21859_amd.pipeline import TimeModel
+    n_req, layers, Hq, Hkv, d, w, pool = 4, 1, 28, 4, 128, 32, 7
+    L = [1200, 2600, 900, 3100]
+    budgets = [60.0, 40.0, 1.0e4, 25.0]                    # tight to loose
+    n_hat = [2, 3, 1, 2]
+    model = TimeModel(prefill_abc=(1e-7, 2e-3, 1.0), step_pq=(2e-3, 0.5), bucket=4, k=2,
+                      n_max=16, t_predict=0.5, alpha_max=0.9)
+    case(f"server admission by budget overlap={overlap}")
+    wl = synth.custom(65, torch.bfloat16, n_req, L, Hq, Hkv, d, w, pool, 16)
+    prompts = [synth.make_prompt(wl, 0, L)]
+    dec = synth.make_decode(wl, 0)
+    srv = Server(layers, n_pages=400, max_seqs=4, max_pages=120, Hq=Hq, Hkv=Hkv, d=d,
+                 dtype=torch.bfloat16, w=w, pool=pool, max_admit=4, max_prompt=max(L))
+    pr = [{key: prompts[0][key].contiguous().to(DEV) for key in ("q_win", "k", "v")}]
+    rids = list(range(n_req))
+    with torch.cuda.stream(srv.decode_stream):
+        plan = srv.admit_budgets(rids, L, budgets, n_hat, model, pr, keep_sets=True,
+                                 overlap=overlap)
+        if overlap:
+            assert srv.promote_ready(wait=True) == n_req
+        alphas = [a for a, _, _ in plan]
+        assert len(set(alphas)) > 1, f"budgets should give different ratios: {plan}"
+        for i, (a, feas, nw) in enumerate(plan):
+            e = srv.slots.slots[i]
+            assert e.rid == i and e.alpha == a and e.left == nw
+            assert e.length == _lib.tb_keep_count(L[i], a, w)
+        qs = dec["q"][0, :n_req].unsqueeze(0).to(DEV)
+        ks = dec["k_new"][0, :n_req].unsqueeze(0).to(DEV)
+        vs = dec["v_new"][0, :n_req].unsqueeze(0).to(DEV)
+        out = torch.empty_like(qs)
+        srv.step(qs, ks, vs, out)
+        torch.cuda.synchronize()
+    G = Hq // Hkv
+    for i in range(n_req):
+        n_keep = _lib.tb_keep_count(L[i], alphas[i], w)
+        k64, v64, q64 = (f64(prompts[0][x][i]) for x in ("k", "v", "q_win"))
+        pooled = O.max_pool(O.window_scores(q64, k64, L[i], w), pool)
+        keep = srv.keep[i][0].cpu().numpy()
+        got = f64(out[0, i])
+        for g in range(Hkv):
+            check_keep(keep[g], pooled[g], L[i], w, n_keep, f"r={i} g={g}")
+            rk = np.concatenate([k64[g, keep[g]], f64(dec["k_new"][0, i, g])[None]])
+            rv = np.concatenate([v64[g, keep[g]], f64(dec["v_new"][0, i, g])[None]])
+            ref = O.decode_step(f64(dec["q"][0, i, g * G:(g + 1) * G]), rk, rv)
+            assert np.abs(got[g * G:(g + 1) * G] - ref).max() <= DECODE_TOL[torch.bfloat16]

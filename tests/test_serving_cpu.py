@@ -177,3 +177,33 @@ def test_random_stream_with_pending_batches():
             st.retire(rng.choice(st.slots).rid)
         _invariants(st)
     assert joined > 100
+
+
+def test_budget_planning_follows_the_controller():
+    """Admission by time budget hands every request the controller's alpha*
+    and pessimistic length (checked against the oracle's closed forms), and a
+    larger budget never asks for more eviction."""
+    from oracle import controller as C
+    from paper_2512_21859_amd.pipeline import TimeModel, plan_requests
+    model = TimeModel(prefill_abc=(2e-9, 6e-5, 12.0), step_pq=(2.5e-4, 21.0), bucket=16, k=3,
+                      n_max=512, t_predict=3.0, alpha_max=0.95)
+    rng = random.Random(3)
+    n_x = [rng.randint(500, 32000) for _ in range(40)]
+    n_hat = [rng.randint(1, 40) for _ in range(40)]
+    budgets = [rng.uniform(300.0, 15000.0) for _ in range(40)]
+    plan = plan_requests(model, n_x, budgets, n_hat)
+    for (a, feas, w), n, nh, T in zip(plan, n_x, n_hat, budgets):
+        w_ref = C.pessimistic_length(C.predicted_length(nh, model.bucket, model.n_max), model.k,
+                                     model.n_max)
+        a_ref, f_ref = C.alpha_star(model.prefill_abc, model.step_pq, n, w_ref, T,
+                                    model.t_predict, model.alpha_max)
+        assert w == w_ref and feas == f_ref
+        assert abs(a - a_ref) <= 1e-12
+        if feas:
+            t = model.t_predict + C.t_wcet(model.prefill_abc, model.step_pq, n, a, w)
+            assert t <= T * (1 + 1e-9)
+    assert any(f for _, f, _ in plan) and not all(f for _, f, _ in plan)
+    more = plan_requests(model, n_x, [2 * T for T in budgets], n_hat)
+    assert all(m[0] <= p[0] for m, p in zip(more, plan))
+    with pytest.raises(ValueError):
+        plan_requests(model, n_x, budgets[:-1], n_hat)
