@@ -330,9 +330,9 @@ void prefill_attn_kernel(PrefillArgs a) {
 
 hipError_t launch_prefill(const PrefillArgs& a, int d, hipStream_t st) {
   // two column tiles per wave (244 VGPRs, two waves per SIMD; 64 KB of LDS
-  // per block at d = 128, so two blocks per CU); four tiles halve the LDS
-  // operand reads per product but need one wave per SIMD, and measured slower
-  // (310 vs 584 TFLOP/s at N = 32768 with the earlier register staging)
+  // per block at d = 128, so two blocks per CU); three or four tiles cut the
+  // LDS operand reads per product but need one wave per SIMD, and measured
+  // slower (530 and 462 against 900 TFLOP/s at N = 32768)
   constexpr int CQ = 2;
   constexpr int rows = kWaves * 16 * CQ;
   int lmax = 0;
