@@ -739,7 +739,7 @@ def _serving_stream(torch, _lib, Server, dev, wl, n_layers, n_req, max_seqs, max
 def main():
     args = _parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not "
+        print(f"bench.py: the benchmark runs on exactly one GPU; --gpus {args.gpus} is not "
               f"supported (the path shards by sequence / KV head with no exchange).",
               file=sys.stderr)
         sys.exit(2)
