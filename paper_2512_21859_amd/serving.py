@@ -418,8 +418,8 @@ class Server:
         n = self.n_active
         if n == 0:
             raise RuntimeError("no running request")
-        if q.shape[:2] != (self.n_layers, n) or k_new.shape[:2] != (self.n_layers, n):
-            raise ValueError(f"inputs must be [{self.n_layers}, {n}, ...]")
+        if any(x.shape[:2] != (self.n_layers, n) for x in (q, k_new, v_new, out)):
+            raise ValueError(f"q, k_new, v_new and out must be [{self.n_layers}, {n}, ...]")
         if any(e.left <= 0 for e in self.slots.slots):
             raise RuntimeError("retire finished requests before the next step")
         for layer in range(self.n_layers):
