@@ -122,6 +122,16 @@ def test_rows_are_distributions_and_mass_is_Gw(hkv, G, w, extra, d, seed):
        st.sampled_from([2, 8]), st.integers(0, 10_000))
 def test_window_probs_match_torch_sdpa(G, w, extra, d, seed):
     """p @ V of the oracle equals torch's attention with an explicit causal mask."""
+    _check_window_probs(G, w, extra, d, seed)
+
+
+@pytest.mark.parametrize("G,w,extra,d,seed", [(2, 3, 9, 8, 1), (4, 5, 20, 2, 7), (1, 1, 3, 8, 2)])
+def test_window_probs_match_torch_sdpa_fixed(G, w, extra, d, seed):
+    """Fixed instances of the check above (two KV groups, d > 1)."""
+    _check_window_probs(G, w, extra, d, seed)
+
+
+def _check_window_probs(G, w, extra, d, seed):
     rng = np.random.default_rng(seed)
     n_x = w + extra
     hkv = 2
@@ -253,6 +263,16 @@ def test_decode_special_cases():
 @settings(max_examples=30, deadline=None)
 @given(st.integers(1, 80), st.integers(1, 9), st.integers(0, 10_000))
 def test_split_merge_equals_direct(N, n_chunks, seed):
+    _check_split_merge(N, n_chunks, seed)
+
+
+@pytest.mark.parametrize("N,n_chunks,seed", [(50, 7, 3), (9, 3, 11), (80, 1, 5)])
+def test_split_merge_equals_direct_fixed(N, n_chunks, seed):
+    """Fixed instances of the check above."""
+    _check_split_merge(N, n_chunks, seed)
+
+
+def _check_split_merge(N, n_chunks, seed):
     rng = np.random.default_rng(seed)
     d, G = 16, 7
     q = rng.standard_normal((G, d)) * 2
