@@ -79,6 +79,20 @@ def test_printed_second_term_disagrees():
     assert abs(printed - e["alpha_star"]) > 1.0
 
 
+def test_prefill_and_step_time_hand_values():
+    """The time model's terms at hand-computed points (the worked example
+    above has a = b = 0, so the prefill's N^2 and N terms are pinned here):
+    1e-8 * 10000^2 + 1e-4 * 10000 + 0.5 = 1 + 1 + 0.5 = 2.5 s;
+    2e-9 * 30000^2 = 1.8 s; 1e-4 * 5000 + 0.01 = 0.51 s; the retained length at
+    step i is (1 - alpha) N_x + i - 1: 7500 at i = 1 and 7502 at i = 3 for
+    alpha = 0.25, N_x = 10000."""
+    assert abs(C.t_prefill((1e-8, 1e-4, 0.5), 10000) - 2.5) < 1e-12
+    assert abs(C.t_prefill((2e-9, 0.0, 0.0), 30000) - 1.8) < 1e-12
+    assert abs(C.t_step((1e-4, 0.01), 5000) - 0.51) < 1e-12
+    assert C.kv_length(10000, 0.25, 1) == 7500.0
+    assert C.kv_length(10000, 0.25, 3) == 7502.0
+
+
 def test_decoding_phase_explicit_sum():
     pq = (2e-5, 3e-3)
     for n_x, alpha, nh in [(1000, 0.0, 1), (1000, 0.3, 2), (4096, 0.5, 65), (32768, 0.95, 257)]:

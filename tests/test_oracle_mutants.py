@@ -12,13 +12,21 @@ import math
 import numpy as np
 import pytest
 
+from oracle import controller as C
+from oracle import scorers as S
 from oracle import timebill_oracle as O
+from tests import test_controller as PC
 from tests import test_oracle_pins as P
+from tests import test_oracle_pins_scorers as PS
 
 _orig = {name: getattr(O, name) for name in (
     "window_logits", "window_probs", "window_scores", "max_pool", "select_keep",
     "decode_step", "merge_partials", "keep_count", "prefill_attention",
     "prefill_window_stats", "window_column_mass")}
+_orig_s = {name: getattr(S, name) for name in ("knorm_scores", "avg_pool", "h2o_scores")}
+_orig_c = {name: getattr(C, name) for name in (
+    "kv_length", "t_prefill", "t_decoding_phase", "t_wcet", "alpha_star", "predicted_length",
+    "pessimistic_length", "fit_poly", "predictor_length")}
 
 
 # ---------------------------------------------------------------- mutants
@@ -165,6 +173,96 @@ def _fixed(test, cases):
 _WINDOW_FIXED = _fixed(P.test_window_probs_match_torch_sdpa_fixed,
                        [(2, 3, 9, 8, 1), (4, 5, 20, 2, 7), (1, 1, 3, 8, 2)])
 _MERGE_FIXED = _fixed(P.test_split_merge_equals_direct_fixed, [(50, 7, 3), (9, 3, 11), (80, 1, 5)])
+# ---- scorer variants
+def knorm_positive(k, n_x, w):
+    return -_orig_s["knorm_scores"](k, n_x, w)
+
+
+def knorm_squared(k, n_x, w):
+    return -_orig_s["knorm_scores"](k, n_x, w) ** 2
+
+
+def knorm_shifted(k, n_x, w):
+    return _orig_s["knorm_scores"](np.asarray(k)[:, 1:], n_x - 1, w - 1)[:, :n_x - w]
+
+
+def avg_pool_valid_divisor(a, pool):
+    a = np.asarray(a, dtype=np.float64)
+    ones = np.ones_like(a)
+    return _orig_s["avg_pool"](a, pool) / _orig_s["avg_pool"](ones, pool)
+
+
+def avg_pool_wrapping(a, pool):
+    a = np.asarray(a, dtype=np.float64)
+    h = pool // 2
+    return sum(np.roll(a, s, axis=-1) for s in range(-h, h + 1)) / pool
+
+
+def _h2o(q, k, n_x, diag=0, scale=True):
+    hq, hkv = q.shape[0], k.shape[0]
+    G, d = hq // hkv, q.shape[-1]
+    out = np.zeros((hkv, n_x))
+    allowed = np.tril(np.ones((n_x, n_x), dtype=bool), k=diag)
+    for h in range(hq):
+        s = np.asarray(q[h, :n_x], dtype=np.float64) @ np.asarray(k[h // G, :n_x], dtype=np.float64).T
+        s = s / np.sqrt(d) if scale else s
+        s = np.where(allowed, s, -np.inf)
+        p = np.exp(s - s.max(axis=1, keepdims=True))
+        out[h // G] += (p / p.sum(axis=1, keepdims=True)).sum(axis=0)
+    return out
+
+
+def h2o_sees_next(q, k, n_x):
+    return _h2o(q, k, n_x, diag=1)
+
+
+def h2o_no_scale(q, k, n_x):
+    return _h2o(q, k, n_x, scale=False)
+
+
+# ---- time-budget controller
+def kv_length_no_minus_one(n_x, alpha, i):
+    return (1.0 - alpha) * n_x + i
+
+
+def decoding_phase_one_more(pq, n_x, alpha, n_hat):
+    return _orig_c["t_decoding_phase"](pq, n_x, alpha, n_hat + 1)
+
+
+def wcet_without_prefill(abc, pq, n_x, alpha, n_hat_w):
+    return C.t_decoding_phase(pq, n_x, alpha, n_hat_w)
+
+
+def prefill_linear_only(abc, n_x):
+    return abc[1] * n_x + abc[2]
+
+
+def alpha_star_printed(abc, pq, n_x, n_hat_w, budget, t_predict, alpha_max):
+    if n_hat_w <= 1:
+        return 0.0, t_predict + C.t_prefill(abc, n_x) <= budget
+    p, q = pq
+    m = n_hat_w - 1
+    raw = (1.0 - (budget - C.t_prefill(abc, n_x) - t_predict) / (p * n_x * m)
+           + (n_hat_w - 2) / (2.0 * p * n_x) + q / (p * n_x))
+    return float(min(alpha_max, max(0.0, raw))), bool(raw <= alpha_max)
+
+
+def predicted_no_cap(n_hat, bucket, n_max):
+    return n_hat * bucket
+
+
+def pessimistic_no_cap(n_hat, k, n_max):
+    return k * n_hat
+
+
+def fit_poly_reversed(n, t, degree):
+    return _orig_c["fit_poly"](n, t, degree)[::-1]
+
+
+def predictor_length_one_short(prefill_abc, predict_abc, n_x, max_len):
+    return _orig_c["predictor_length"](prefill_abc, predict_abc, n_x, max(max_len - 1, 0))
+
+
 _WINDOW_PINS = [P.test_hand_example_column_mass_and_mask, P.test_hand_example_scores_and_pool,
                 _WINDOW_FIXED, P.test_rows_are_distributions_and_mass_is_Gw,
                 P.test_window_probs_match_torch_sdpa, P.test_alpha_zero_is_identity_and_full_attention]
@@ -174,6 +272,15 @@ _DECODE_PINS = [P.test_hand_example_decode, P.test_decode_matches_torch_sdpa,
                 P.test_decode_special_cases, P.test_decode_append_order,
                 P.test_alpha_zero_is_identity_and_full_attention]
 _KEEP_PINS = [P.test_keep_count_table, P.test_keep_count_edges]
+_KNORM_PINS = [PS.test_knorm_hand_example, PS.test_knorm_matches_torch_norm]
+_AVG_PINS = [PS.test_avg_pool_hand_example, _fixed(PS.test_avg_pool_matches_torch,
+                                                   [(1,), (3,), (5,), (7,), (9,)]),
+             PS.test_avg_pool_constant_closed_form]
+_H2O_PINS = [PS.test_h2o_hand_example, PS.test_h2o_total_mass_and_torch,
+             PS.test_h2o_last_row_only_matches_window_mass]
+_CTRL_PINS = [PC.test_hand_example, PC.test_prefill_and_step_time_hand_values,
+              PC.test_decoding_phase_explicit_sum, PC.test_predictor_length_golden_and_abi,
+              PC.test_closed_form_equals_bisection]
 
 MUTANTS = {
     "causal mask one key late": ("window_logits", logits_mask_late, _WINDOW_PINS),
@@ -202,6 +309,27 @@ MUTANTS = {
     "window statistics without 1/sqrt(d)": ("prefill_window_stats", stats_no_scale,
                                             [P.test_prefill_attention_matches_torch_sdpa]),
 }
+MUTANTS = {k: (O,) + v for k, v in MUTANTS.items()}
+MUTANTS.update({
+    "KNorm keeps the largest norms": (S, "knorm_scores", knorm_positive, _KNORM_PINS),
+    "KNorm without the square root": (S, "knorm_scores", knorm_squared, _KNORM_PINS),
+    "KNorm one key off": (S, "knorm_scores", knorm_shifted, _KNORM_PINS),
+    "mean pool divides by the in-range count": (S, "avg_pool", avg_pool_valid_divisor, _AVG_PINS),
+    "mean pool wraps around": (S, "avg_pool", avg_pool_wrapping, _AVG_PINS),
+    "H2O query sees the next key": (S, "h2o_scores", h2o_sees_next, _H2O_PINS),
+    "H2O without 1/sqrt(d)": (S, "h2o_scores", h2o_no_scale, _H2O_PINS),
+    "retained length without the -1": (C, "kv_length", kv_length_no_minus_one, _CTRL_PINS),
+    "one decode step too many": (C, "t_decoding_phase", decoding_phase_one_more, _CTRL_PINS),
+    "WCET without the prefill": (C, "t_wcet", wcet_without_prefill, _CTRL_PINS),
+    "prefill time without the N^2 term": (C, "t_prefill", prefill_linear_only, _CTRL_PINS),
+    "alpha* with the printed second term": (C, "alpha_star", alpha_star_printed, _CTRL_PINS),
+    "predicted length not capped": (C, "predicted_length", predicted_no_cap, _CTRL_PINS),
+    "pessimistic length not capped": (C, "pessimistic_length", pessimistic_no_cap, _CTRL_PINS),
+    "fit coefficients in the wrong order": (C, "fit_poly", fit_poly_reversed,
+                                            [PC.test_fit_poly_recovers_exact_and_matches_polyfit]),
+    "predictor length search one short": (C, "predictor_length", predictor_length_one_short,
+                                          [PC.test_predictor_length_golden_and_abi]),
+})
 
 
 # pins driven by hypothesis draw their cases at random; each mutant must also
@@ -209,13 +337,14 @@ MUTANTS = {
 # on the draw
 _RANDOM = {P.test_rows_are_distributions_and_mass_is_Gw, P.test_window_probs_match_torch_sdpa,
            P.test_max_pool_matches_torch, P.test_select_matches_brute_force,
-           P.test_decode_matches_torch_sdpa, P.test_split_merge_equals_direct}
+           P.test_decode_matches_torch_sdpa, P.test_split_merge_equals_direct,
+           PC.test_closed_form_equals_bisection}
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_pins_catch_planted_mistake(name, monkeypatch):
-    attr, mutant, pins = MUTANTS[name]
-    monkeypatch.setattr(O, attr, mutant)
+    module, attr, mutant, pins = MUTANTS[name]
+    monkeypatch.setattr(module, attr, mutant)
     caught = []
     for pin in [p for p in pins if p not in _RANDOM]:
         try:
@@ -227,6 +356,6 @@ def test_pins_catch_planted_mistake(name, monkeypatch):
 
 def test_pins_pass_on_the_oracle():
     """The same pins, run the same way, pass on the unmodified oracle."""
-    pins = {p for _, _, ps in MUTANTS.values() for p in ps if p not in _RANDOM}
+    pins = {p for _, _, _, ps in MUTANTS.values() for p in ps if p not in _RANDOM}
     for pin in sorted(pins, key=lambda p: p.__name__):
         pin()
