@@ -7,8 +7,6 @@
 
 namespace tb {
 
-constexpr int kMaxBatch = 64;
-
 // bf16 is carried as its raw 16-bit pattern.
 struct bf16_t {
   uint16_t bits;
@@ -74,9 +72,6 @@ __device__ __forceinline__ float row16_sum(float x) {
 
 __device__ __forceinline__ uint4 ldg16(const void* p) {
   return *reinterpret_cast<const uint4*>(p);
-}
-__device__ __forceinline__ void stg16(void* p, const uint4& v) {
-  *reinterpret_cast<uint4*>(p) = v;
 }
 // Streaming (non-temporal) 16-byte store: for outputs written once and not
 // read back soon, so they do not displace cached data on their way to HBM.

@@ -145,7 +145,6 @@ struct DecodePlan {
 DecodePlan decode_plan(int B, int Hkv, int cap, bool bf16);
 int decode_chunk_unit(int waves, bool bf16);
 int decode_max_chunks();
-size_t decode_ws_bytes(int B, int Hkv, int G, int d, int cap);
 hipError_t launch_decode(const DecodeArgs& a, int G, int d, bool bf16, hipStream_t st);
 
 }  // namespace tb
