@@ -76,15 +76,8 @@ __device__ __forceinline__ double dpp_f64(double x) {
   return __longlong_as_double((static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) |
                               static_cast<uint32_t>(lo));
 }
-// Max / sum over the 16 lanes of a DPP row; every lane gets the result, in a
-// fixed order (deterministic).
-__device__ __forceinline__ double row16_max_f64(double x) {
-  x = fmax(x, dpp_f64<kDppQuadXor1>(x));
-  x = fmax(x, dpp_f64<kDppQuadXor2>(x));
-  x = fmax(x, dpp_f64<kDppRowHalfMirror>(x));
-  x = fmax(x, dpp_f64<kDppRowMirror>(x));
-  return x;
-}
+// Sum over the 16 lanes of a DPP row; every lane gets the result, in a fixed
+// order (deterministic).
 __device__ __forceinline__ double row16_sum_f64(double x) {
   x += dpp_f64<kDppQuadXor1>(x);
   x += dpp_f64<kDppQuadXor2>(x);
