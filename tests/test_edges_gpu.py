@@ -133,3 +133,31 @@ def test_equal_keys_select_by_position():
         # every window row sees all prefix positions with the same weight, so the
         # prefix scores all tie and the lowest n_sel positions are kept
         assert kk[0, g, :n_sel].tolist() == list(range(n_sel))
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_compact_clamps_out_of_range_indices(dtype):
+    """Kept indices outside [0, Lmax) are clamped into the prompt (the ABI's
+    stated behaviour for bad indices): -3 reads row 0, 250 and Lmax read row
+    Lmax - 1; valid ones gather exactly."""
+    case(f"compaction with out-of-range kept indices {dtype}")
+    B, Hkv, Lmax, d, cap = 2, 2, 100, 128, 64
+    gen = torch.Generator().manual_seed(9)
+    k = torch.randn((B, Hkv, Lmax, d), generator=gen).to(dtype)
+    v = torch.randn((B, Hkv, Lmax, d), generator=gen).to(dtype)
+    idx = [5, -3, 99, 250, 7, Lmax, 0, -2147483648]
+    keep = torch.zeros((B, Hkv, Lmax), dtype=torch.int32)
+    keep[:, :, : len(idx)] = torch.tensor(idx, dtype=torch.int32)
+    n_keep = [len(idx), 3]
+    kc = torch.zeros((B, Hkv, cap, d), dtype=dtype, device=DEV)
+    vc = torch.zeros((B, Hkv, cap // 32, d, 32), dtype=dtype, device=DEV)
+    kv_len = torch.zeros((B,), dtype=torch.int32, device=DEV)
+    _lib.tb_compact_kv(k.to(DEV), v.to(DEV), keep.to(DEV), n_keep, kc, vc, kv_len)
+    torch.cuda.synchronize()
+    clamped = [min(max(i, 0), Lmax - 1) for i in idx]
+    v_rows = vc.cpu().transpose(-1, -2).reshape(B, Hkv, cap, d)
+    for b in range(B):
+        rows = clamped[: n_keep[b]]
+        assert torch.equal(kc[b, :, : n_keep[b]].cpu(), k[b][:, rows])
+        assert torch.equal(v_rows[b, :, : n_keep[b]], v[b][:, rows])
+    assert kv_len.cpu().tolist() == n_keep
