@@ -450,3 +450,39 @@ def test_server_admits_by_budget(overlap):
             rv = np.concatenate([v64[g, keep[g]], f64(dec["v_new"][0, i, g])[None]])
             ref = O.decode_step(f64(dec["q"][0, i, g * G:(g + 1) * G]), rk, rv)
             assert np.abs(got[g * G:(g + 1) * G] - ref).max() <= DECODE_TOL[torch.bfloat16]
+
+
+def test_paged_decode_clamps_table_entries():
+    """Block-table entries outside the pool are clamped into it before use
+    (the ABI's stated behaviour): a sequence whose table names pages -7 and 9
+    in a 6-page pool attends over pages 0 and 5 there.  The appended row lands
+    in a valid page."""
+    case("paged decode with out-of-pool table entries")
+    Hkv, G, d, n_pages, max_pages, n0 = 2, 4, 128, 6, 4, 100
+    Hq = Hkv * G
+    gen = torch.Generator().manual_seed(31)
+    k_pool = torch.randn((n_pages, Hkv, PAGE, d), generator=gen).to(torch.bfloat16)
+    v_pool = torch.randn((n_pages, Hkv, d, PAGE), generator=gen).to(torch.bfloat16)
+    q = torch.randn((1, Hq, d), generator=gen).to(torch.bfloat16)
+    kn = torch.randn((1, Hkv, d), generator=gen).to(torch.bfloat16)
+    vn = torch.randn((1, Hkv, d), generator=gen).to(torch.bfloat16)
+    table = torch.tensor([[-7, 9, 2, 3]], dtype=torch.int32)
+    used = [0, 5, 2, 3]                                    # the clamped pages, tile by tile
+    kp, vp = k_pool.to(DEV), v_pool.to(DEV)
+    kv_len = torch.tensor([n0], dtype=torch.int32, device=DEV)
+    out = torch.empty((1, Hq, d), dtype=torch.bfloat16, device=DEV)
+    cap = max_pages * PAGE
+    ws = torch.zeros((_lib.tb_workspace_bytes(_lib.TB_OP_DECODE, 1, 0, Hq, Hkv, d, 0, cap),),
+                     dtype=torch.uint8, device=DEV)
+    _lib.tb_decode_attn_paged(q.to(DEV), kn.to(DEV), vn.to(DEV), kp, vp, table.to(DEV), kv_len,
+                              out, ws)
+    torch.cuda.synchronize()
+    assert kv_len.cpu().tolist() == [n0 + 1]
+    got = f64(out[0])
+    for g in range(Hkv):
+        k_rows = torch.cat([k_pool[p, g] for p in used])[:n0]
+        v_rows = torch.cat([v_pool[p, g].transpose(0, 1) for p in used])[:n0]
+        rk = np.concatenate([f64(k_rows), f64(kn[0, g])[None]])
+        rv = np.concatenate([f64(v_rows), f64(vn[0, g])[None]])
+        ref = O.decode_step(f64(q[0, g * G:(g + 1) * G]), rk, rv)
+        assert np.abs(got[g * G:(g + 1) * G] - ref).max() <= DECODE_TOL[torch.bfloat16]
