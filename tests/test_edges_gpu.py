@@ -161,3 +161,35 @@ def test_compact_clamps_out_of_range_indices(dtype):
         assert torch.equal(kc[b, :, : n_keep[b]].cpu(), k[b][:, rows])
         assert torch.equal(v_rows[b, :, : n_keep[b]], v[b][:, rows])
     assert kv_len.cpu().tolist() == n_keep
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_decode_full_cache_drops_the_append(dtype):
+    """kv_len == cap with a new row given: the append would overflow, so it is
+    dropped on the device (the ABI's stated behaviour); the step attends over
+    the cap cached rows and leaves the caches and kv_len as they were."""
+    case(f"decode on a full cache {dtype}")
+    B, Hkv, G, d, cap = 2, 2, 3, 64, 64
+    Hq = Hkv * G
+    gen = torch.Generator().manual_seed(12)
+    kc = torch.randn((B, Hkv, cap, d), generator=gen).to(dtype)
+    vc = torch.randn((B, Hkv, cap, d), generator=gen).to(dtype)
+    q = torch.randn((B, Hq, d), generator=gen).to(dtype)
+    kn = torch.randn((B, Hkv, d), generator=gen).to(dtype)
+    vn = torch.randn((B, Hkv, d), generator=gen).to(dtype)
+    cache = _lib.KVCache(B, Hq, Hkv, cap, d, dtype)
+    cache.k.copy_(kc)
+    cache.v.copy_(_lib.v_rows_to_tiles(vc))
+    cache.kv_len.fill_(cap)
+    k_before, v_before = cache.k.clone(), cache.v.clone()
+    out = torch.empty((B, Hq, d), dtype=dtype, device=DEV)
+    _lib.tb_decode_attn(q.to(DEV), kn.to(DEV), vn.to(DEV), cache.k, cache.v, cache.kv_len, out,
+                        cache.ws)
+    torch.cuda.synchronize()
+    assert cache.kv_len.cpu().tolist() == [cap] * B
+    assert torch.equal(cache.k, k_before) and torch.equal(cache.v, v_before)
+    got = f64(out)
+    for b in range(B):
+        for g in range(Hkv):
+            ref = O.decode_step(f64(q[b, g * G:(g + 1) * G]), f64(kc[b, g]), f64(vc[b, g]))
+            assert np.abs(got[b, g * G:(g + 1) * G] - ref).max() <= DECODE_TOL[dtype]
