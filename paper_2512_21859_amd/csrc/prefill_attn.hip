@@ -25,9 +25,10 @@
 // products, the scale folded into each exponent's FMA); P is rounded to bf16
 // for the PV product.  O^T is rescaled only in steps where some row's max
 // moved.  Each step runs its two column tiles phase by phase (both QK
-// products, both softmaxes, one rescale test, both PV products), so one
-// tile's products overlap the other's exponentials: +3% at N = 16384-32768
-// over one tile at a time, bit-identical output.
+// products, one mask branch, both softmaxes, one statistics branch, one
+// rescale test, both PV products), so one tile's products overlap the
+// other's exponentials: +4% at N = 16384-32768 over one tile at a time,
+// bit-identical output.
 
 #include "common.h"
 #include "kernels.h"
@@ -216,11 +217,11 @@ void prefill_attn_kernel(PrefillArgs a) {
         vA[n] = u32x4{lo[0], lo[1], hi[0], hi[1]};
       }
       const bool need_mask = base + 32 > row0;                  // step reaches this wave's diagonal
-      // The step runs in three phases over the column tiles: every tile's QK
-      // products, then every tile's softmax, then every tile's PV products.
-      // Kept apart, the products of one tile can issue beside the other
-      // tile's exponentials, which a per-tile loop (split into blocks by the
-      // rescale branch) does not allow.
+      // The step runs in phases over the column tiles: every tile's QK
+      // products, the mask, every tile's softmax, the window statistics, one
+      // rescale test, every tile's PV products.  Kept apart (each wave-uniform
+      // branch taken once per step, not once per tile), the products of one
+      // tile can issue beside the other tile's exponentials.
       f32x4 S[CQ][2];
 #pragma unroll
       for (int cq = 0; cq < CQ; ++cq)
@@ -232,46 +233,53 @@ void prefill_attn_kernel(PrefillArgs a) {
             acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kA[t][kc]), as_bf16x8(qB[cq][kc]), acc, 0, 0, 0);
           S[cq][t] = acc;
         }
+      // lane holds keys base + 8 q4 + j (j = 4t + i) of query row0 + 16 cq + r16
+      if (need_mask) {
+#pragma unroll
+        for (int cq = 0; cq < CQ; ++cq) {
+          const int qi = row0 + 16 * cq + r16;
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            if (base + 8 * q4 + j > qi) S[cq][j >> 2][j & 3] = -INFINITY;
+        }
+      }
       float corr[CQ];
-      bf16x8 pB[CQ];
+      float p[CQ][8];
 #pragma unroll
       for (int cq = 0; cq < CQ; ++cq) {
-        // lane holds keys base + 8 q4 + j (j = 4t + i) of query row0 + 16 cq + r16;
-        // the running max is kept on the raw dot products (the scale is
-        // positive) and the scale enters each exponent through one FMA
-        const int qi = row0 + 16 * cq + r16;
         float s[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) s[j] = S[cq][j >> 2][j & 3];
-        if (need_mask) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            if (base + 8 * q4 + j > qi) s[j] = -INFINITY;
-        }
         float mt = fmax2(fmax2(fmax2(s[0], s[1]), fmax2(s[2], s[3])),
                          fmax2(fmax2(s[4], s[5]), fmax2(s[6], s[7])));
         mt = group_max(mt);
+        // the running max is kept on the raw dot products (the scale is
+        // positive) and the scale enters each exponent through one FMA;
         // finite: every wave's first step holds key 0, which no query masks
         const float m_new = fmax2(m_run[cq], mt);
         const float mc = m_new * a.scale_log2;
         // 1 when the max did not move; 0 on the first step (m_run = -inf)
         corr[cq] = __builtin_amdgcn_exp2f((m_run[cq] - m_new) * a.scale_log2);
         m_run[cq] = m_new;
-        float p[8];
+        // hardware exp2: results below 2^-126 flush to zero, far below a
+        // softmax term that can matter next to the row max's term of 1
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          // hardware exp2: results below 2^-126 flush to zero, far below a
-          // softmax term that can matter next to the row max's term of 1
-          p[j] = __builtin_amdgcn_exp2f(fmaf(s[j], a.scale_log2, -mc));
-          pB[cq][j] = static_cast<__bf16>(p[j]);
-        }
-        if (stats_wave) {                                     // wave-uniform
+        for (int j = 0; j < 8; ++j) p[cq][j] = __builtin_amdgcn_exp2f(fmaf(s[j], a.scale_log2, -mc));
+      }
+      if (stats_wave) {                                       // wave-uniform
+#pragma unroll
+        for (int cq = 0; cq < CQ; ++cq) {
           float psum = 0.f;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) psum += p[j];
+          for (int j = 0; j < 8; ++j) psum += p[cq][j];
           l_part[cq] = l_part[cq] * corr[cq] + psum;
         }
       }
+      bf16x8 pB[CQ];
+#pragma unroll
+      for (int cq = 0; cq < CQ; ++cq)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) pB[cq][j] = static_cast<__bf16>(p[cq][j]);
       // rescaling by exactly 1 changes nothing: skip it unless some lane's max
       // moved in some tile (the tiles whose max stayed are multiplied by 1)
       bool moved = false;
