@@ -40,6 +40,7 @@ def _run(wl, L, w=0):
     (128, 14, 2, [300, 129], 32),
     (64, 8, 2, [1, 64, 200], 1),
     (128, 7, 1, [1000], 64),
+    (64, 16, 2, [777, 2049], 32),      # d = 64 over many blocks, ragged tails
 ])
 def test_prefill_matches_oracle(d, Hq, Hkv, L, w):
     case(f"prefill d={d} Hq={Hq} Hkv={Hkv} L={L} w={w}")
