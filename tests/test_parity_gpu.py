@@ -401,6 +401,28 @@ def test_workload4_ragged():
     _run_layer(wl, 0, L, alphas, wl.T, _steps(wl.T, 64))
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_full_chain_random_shapes(seed):
+    """Score, select, compact and decode on seeded random shapes: batch size,
+    heads and group size, head dimension, dtype, window, pool width, ragged
+    lengths, one ratio per sequence and the decode step count all drawn."""
+    rs = np.random.RandomState(7000 + seed)
+    dtype = [torch.bfloat16, torch.float32][rs.randint(2)]
+    d = [64, 128][rs.randint(2)]
+    Hkv = int(rs.choice([1, 2, 4]))
+    G = int(rs.choice([1, 2, 3, 4, 7, 8]))
+    B = int(rs.randint(1, 5))
+    w = int(rs.choice([1, 8, 31, 32, 64]))
+    pool = int(rs.choice([1, 3, 5, 7]))
+    T = int(rs.randint(1, 7))
+    L = [int(x) for x in rs.randint(w + 1, 2600, size=B)]
+    alphas = [float(x) for x in np.round(rs.uniform(0.0, 0.95, size=B), 3)]
+    wl = synth.custom(7000 + seed, dtype, B, L, G * Hkv, Hkv, d, w, pool, T)
+    case(f"random chain seed={seed} {dtype} d={d} Hkv={Hkv} G={G} w={w} pool={pool} "
+         f"T={T} L={L} alphas={alphas}")
+    _run_layer(wl, 0, L, alphas, T, range(T))
+
+
 def test_workload3_layers_and_sweep():
     wl = synth.WORKLOADS[3]
     case(f"{wl.name}: eviction on every layer at 5 ratios, decode checked on 3 layers")
