@@ -44,7 +44,25 @@ def _run(wl, L, w=0):
 ])
 def test_prefill_matches_oracle(d, Hq, Hkv, L, w):
     case(f"prefill d={d} Hq={Hq} Hkv={Hkv} L={L} w={w}")
-    wl = synth.custom(1300 + d + Hq, torch.bfloat16, len(L), L, Hq, Hkv, d, w, 1, 1)
+    _check_against_oracle(synth.custom(1300 + d + Hq, torch.bfloat16, len(L), L, Hq, Hkv, d, w, 1, 1), L, w)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_prefill_random_shapes(seed):
+    """Seeded random shapes: head dimension, KV heads, group size, batch,
+    ragged lengths (including lengths below the window) and window size."""
+    rs = np.random.RandomState(9100 + seed)
+    d = [64, 128][rs.randint(2)]
+    Hkv = int(rs.choice([1, 2, 4]))
+    G = int(rs.choice([1, 2, 3, 4, 7, 8]))
+    B = int(rs.randint(1, 4))
+    w = int(rs.choice([0, 1, 16, 32, 64]))
+    L = [int(x) for x in rs.randint(max(w, 1), 1500, size=B)]
+    case(f"prefill random seed={seed} d={d} Hkv={Hkv} G={G} L={L} w={w}")
+    _check_against_oracle(synth.custom(9100 + seed, torch.bfloat16, B, L, G * Hkv, Hkv, d, w, 1, 1), L, w)
+
+
+def _check_against_oracle(wl, L, w):
     pr, q, out, ws = _run(wl, L, w)
     got = f64(out)
     wst = ws.cpu().numpy() if ws is not None else None
