@@ -257,3 +257,53 @@ def test_h2o_end_to_end_decode():
                             kc, vc)
     want = np.stack([res[t] for t in range(T)])
     assert float(np.max(np.abs(f64(out[:, 0]) - want))) <= DECODE_TOL[wl.dtype]
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("scorer", ["knorm", "snapkv_avg"])
+def test_scorer_chain_random_shapes(scorer, seed):
+    """Variant scores through select, compact and decode on seeded random
+    shapes: dtype, head dimension, KV heads and group size, window, pool
+    width, ragged lengths with one ratio per sequence, decode step count."""
+    rs = np.random.RandomState(9300 + seed + (100 if scorer == "knorm" else 0))
+    dtype = [torch.bfloat16, torch.float32][rs.randint(2)]
+    d = [64, 128][rs.randint(2)]
+    Hkv = int(rs.choice([1, 2, 4]))
+    G = int(rs.choice([1, 2, 4, 7, 8]))
+    B = int(rs.randint(1, 4))
+    w = int(rs.choice([1, 8, 32]))
+    pool = int(rs.choice([1, 3, 7]))
+    T = int(rs.randint(1, 5))
+    L = [int(x) for x in rs.randint(w + 1, 3000, size=B)]
+    alphas = [float(x) for x in np.round(rs.uniform(0.0, 0.95, size=B), 3)]
+    case(f"{scorer} random chain seed={seed} {dtype} d={d} Hkv={Hkv} G={G} w={w} "
+         f"pool={pool} T={T} L={L} alphas={alphas}")
+    wl = synth.custom(9300 + seed, dtype, B, L, G * Hkv, Hkv, d, w, pool, T)
+    pr = synth.make_prompt(wl, L=L)
+    dc = synth.make_decode(wl, T=T)
+    ev = Evictor(B, max(L), wl.Hq, Hkv, d, w, pool, scorer=scorer)
+    n_host = [_lib.tb_keep_count(L[b], alphas[b], w) for b in range(B)]
+    cache = _lib.KVCache(B, wl.Hq, Hkv, max(n_host) + T, d, dtype)
+    n_keep = ev.evict(pr["q_win"].to(DEV), pr["k"].to(DEV), pr["v"].to(DEV), L, alphas, cache)
+    assert n_keep == n_host
+    out = run_decode(cache, dc["q"].to(DEV), dc["k_new"].to(DEV), dc["v_new"].to(DEV))
+    torch.cuda.synchronize()
+    kk = ev.keep_idx.cpu().numpy()
+    worst = 0.0
+    for b in range(B):
+        q64, k64, v64 = f64(pr["q_win"][b]), f64(pr["k"][b]), f64(pr["v"][b])
+        if scorer == "knorm":
+            ref = S.knorm_scores(k64, L[b], w)
+        else:
+            ref = S.avg_pool(O.window_scores(q64, k64, L[b], w), pool)
+        for g in range(Hkv):
+            check_keep(kk[b, g, :n_keep[b]], ref[g], L[b], w, n_keep[b], f"{scorer} b={b} g={g}")
+        kept = kk[b, :, :n_keep[b]]
+        kc = np.stack([k64[g, kept[g]] for g in range(Hkv)])
+        vc = np.stack([v64[g, kept[g]] for g in range(Hkv)])
+        res = O.decode_sequence(f64(dc["q"][:, b]), f64(dc["k_new"][:, b]), f64(dc["v_new"][:, b]),
+                                kc, vc)
+        for t in range(T):
+            worst = max(worst, float(np.max(np.abs(f64(out[t, b]) - res[t]))))
+    print(f"{scorer}: max decode abs err {worst:.2e}", flush=True)
+    assert worst <= DECODE_TOL[dtype]
