@@ -280,11 +280,26 @@ double tb_wcet(const double* prefill_abc, const double* step_pq, double n_x, dou
  * (n_hat_w - 2) / (2 n_x); the printed version also divides it by p, which is
  * dimensionally inconsistent).  *feasible (nullable) is 1 when the budget can
  * be met at or below alpha_max, else 0 and alpha_max is returned.
- * n_hat_w <= 1 (no decode step) gives 0.  NaN for n_x <= 0 or alpha_max
- * outside [0, 1). */
+ * n_hat_w <= 1 (no decode step) gives 0.
+ * p = step_pq[0] = 0 (step time independent of the cache length): WCET does
+ * not depend on alpha, so the result is 0 with *feasible = 1 when
+ * t_predict + prefill + (n_hat_w - 1) q <= budget, else alpha_max with
+ * *feasible = 0 (the closed form's limit as p -> 0 from above).
+ * Returns NaN with *feasible = 0 for null pointers, n_x <= 0, alpha_max
+ * outside [0, 1), p < 0 (not a decode-step model), a non-finite p, q or
+ * t_predict, or a NaN budget (+inf means no limit). */
 double tb_alpha_star(const double* prefill_abc, const double* step_pq, double n_x,
                      int32_t n_hat_w, double budget, double t_predict, double alpha_max,
                      int32_t* feasible);
+
+/* [host] Response lengths the controller plans with: the predicted length
+ * N_hat = min(n_max, n_hat * bucket) from the predictor's bucket index n_hat
+ * and bucket size (Sec. 4.1, Eq. predictor_inference), written to *n_hat_len
+ * (nullable), and the returned pessimistic length N_hat_W = min(k N_hat, n_max)
+ * (Sec. 4.2, the worst-case length ahead of Eq. wcet).  -1 on bad arguments
+ * (n_hat < 0, bucket < 1, k < 1, n_max < 0). */
+int32_t tb_response_length(int32_t n_hat, int32_t bucket, int32_t k, int32_t n_max,
+                           int32_t* n_hat_len);
 
 /* [host] Longest predictor input that runs within the prefill phase
  * (Sec. 5.2, deployment: the response-length predictor runs beside the

@@ -25,7 +25,10 @@ Reading: substituting the equations gives a second term (N_hat_W - 2)/(2 N_x);
 the printed formula divides it by p as well, which is dimensionally
 inconsistent (1/time) and disagrees with solving the constraint, so the
 derived form is used.  The paper gives no lower clamp; alpha* is clamped to
-[0, alpha_max], and N_hat_W <= 1 (no decode step) gives alpha* = 0.
+[0, alpha_max], and N_hat_W <= 1 (no decode step) gives alpha* = 0.  The
+closed form needs a positive slope p; p = 0 and p < 0 are handled in
+alpha_star (the constraint itself, Eq. problem_converted, is well defined at
+p = 0).
 """
 from __future__ import annotations
 
@@ -73,11 +76,22 @@ def alpha_star(abc, pq, n_x: float, n_hat_w: int, budget: float, t_predict: floa
 
     With M = n_hat_w - 1 decode steps the constraint is
     t_predict + t_prefill + M p (1 - alpha) N_x + p M (M - 1) / 2 + M q <= T.
+
+    The closed form divides by p.  With p = 0 the left side does not depend on
+    alpha: every alpha meets the constraint or none does, and the result is the
+    closed form's limit as p -> 0 from above (0 when feasible, alpha_max
+    otherwise).  A negative slope is not a decode-step model: (nan, False).
     """
-    if n_hat_w <= 1:
-        return 0.0, t_predict + t_prefill(abc, n_x) <= budget
     p, q = pq
+    if not p >= 0:
+        return float("nan"), False
+    fixed = t_predict + t_prefill(abc, n_x)
+    if n_hat_w <= 1:
+        return 0.0, fixed <= budget
     m = n_hat_w - 1
+    if p == 0:
+        ok = fixed + m * q <= budget
+        return (0.0 if ok else float(alpha_max)), bool(ok)
     raw = (1.0 - (budget - t_prefill(abc, n_x) - t_predict) / (p * n_x * m)
            + (n_hat_w - 2) / (2.0 * n_x) + q / (p * n_x))
     feasible = raw <= alpha_max

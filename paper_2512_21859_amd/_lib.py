@@ -24,7 +24,7 @@ V_TILE = 32          # the compact V cache is stored as transposed tiles of 32 r
 EXPORTED = ("tb_keep_count", "tb_last_error", "tb_workspace_bytes", "tb_score_window",
             "tb_score_window_avgpool", "tb_score_knorm", "tb_score_h2o", "tb_prefill_attn",
             "tb_select_topk", "tb_compact_kv_paged", "tb_decode_attn_paged", "tb_compact_kv", "tb_decode_attn", "tb_ete_fit", "tb_wcet",
-            "tb_alpha_star", "tb_predictor_length")
+            "tb_alpha_star", "tb_response_length", "tb_predictor_length")
 
 _lib = None
 
@@ -84,6 +84,8 @@ def load() -> ctypes.CDLL:
     lib.tb_wcet.restype = dbl
     lib.tb_alpha_star.argtypes = [p_dbl, p_dbl, dbl, i32, dbl, dbl, dbl, p_i32]
     lib.tb_alpha_star.restype = dbl
+    lib.tb_response_length.argtypes = [i32, i32, i32, i32, p_i32]
+    lib.tb_response_length.restype = i32
     lib.tb_predictor_length.argtypes = [p_dbl, p_dbl, dbl, ctypes.c_int64]
     lib.tb_predictor_length.restype = ctypes.c_int64
     _lib = lib
@@ -242,6 +244,15 @@ def tb_alpha_star(prefill_abc: Sequence[float], step_pq: Sequence[float], n_x: f
     a = load().tb_alpha_star(_dbl_array(prefill_abc), _dbl_array(step_pq), n_x, n_hat_w, budget,
                              t_predict, alpha_max, ctypes.byref(feas))
     return float(a), bool(feas.value)
+
+
+def tb_response_length(n_hat: int, bucket: int, k: int, n_max: int):
+    """Returns (N_hat, N_hat_W) for predicted bucket index n_hat."""
+    nh = ctypes.c_int32(0)
+    nw = load().tb_response_length(int(n_hat), int(bucket), int(k), int(n_max), ctypes.byref(nh))
+    if nw < 0:
+        raise ValueError("tb_response_length: bad arguments")
+    return int(nh.value), int(nw)
 
 
 def v_rows_to_tiles(v_rows: torch.Tensor) -> torch.Tensor:

@@ -11,11 +11,14 @@
 //              + (N_hat_W - 2) / (2 N_x) + q / (p N_x),
 // i.e. the paper's closed form with the second term divided by 2 N_x (the
 // printed form also divides it by p, which is dimensionally inconsistent).
+// The closed form needs p > 0; p = 0 (a step time that does not grow with the
+// cache) makes WCET independent of alpha, and p < 0 is rejected.
 
 #include <math.h>
 #include <stdint.h>
 
 #include <algorithm>
+#include <cmath>
 
 #include "../../include/timebill.h"
 
@@ -88,20 +91,41 @@ double tb_wcet(const double* prefill_abc, const double* step_pq, double n_x, dou
 double tb_alpha_star(const double* prefill_abc, const double* step_pq, double n_x,
                      int32_t n_hat_w, double budget, double t_predict, double alpha_max,
                      int32_t* feasible) {
-  if (!prefill_abc || !step_pq || !(n_x > 0) || !(alpha_max >= 0 && alpha_max < 1)) {
-    if (feasible) *feasible = 0;
+  if (feasible) *feasible = 0;
+  if (!prefill_abc || !step_pq || !(n_x > 0) || !(alpha_max >= 0 && alpha_max < 1)) return NAN;
+  const double p = step_pq[0], q = step_pq[1];
+  // A step time that falls as the cache grows is not a model of decoding
+  // (Eq. decoding_step_time_raw is linear in N_kv with a non-negative slope).
+  if (!(p >= 0) || !std::isfinite(p) || !std::isfinite(q) || std::isnan(budget) ||
+      !std::isfinite(t_predict))
     return NAN;
-  }
+  const double fixed = t_predict + prefill(prefill_abc, n_x);
   if (n_hat_w <= 1) {
-    if (feasible) *feasible = (t_predict + prefill(prefill_abc, n_x) <= budget) ? 1 : 0;
+    if (feasible) *feasible = fixed <= budget ? 1 : 0;
     return 0.0;
   }
-  const double p = step_pq[0], q = step_pq[1];
   const double m = static_cast<double>(n_hat_w - 1);
-  const double raw = 1.0 - (budget - prefill(prefill_abc, n_x) - t_predict) / (p * n_x * m) +
-                     (n_hat_w - 2) / (2.0 * n_x) + q / (p * n_x);
+  if (p == 0) {
+    // WCET does not depend on alpha: the constraint of Eq. problem_converted
+    // holds for every alpha or for none.  The closed form's limit p -> 0+ gives
+    // 0 in the first case and alpha_max (clamped) in the second.
+    const bool ok = fixed + m * q <= budget;
+    if (feasible) *feasible = ok ? 1 : 0;
+    return ok ? 0.0 : alpha_max;
+  }
+  const double raw = 1.0 - (budget - fixed) / (p * n_x * m) + (n_hat_w - 2) / (2.0 * n_x) +
+                     q / (p * n_x);
   if (feasible) *feasible = raw <= alpha_max ? 1 : 0;
   return std::min(alpha_max, std::max(0.0, raw));
+}
+
+int32_t tb_response_length(int32_t n_hat, int32_t bucket, int32_t k, int32_t n_max,
+                           int32_t* n_hat_len) {
+  if (n_hat < 0 || bucket < 1 || k < 1 || n_max < 0) return -1;
+  // N_hat = min(N_max, n_hat B) (Eq. predictor_inference); N_hat_W = min(k N_hat, N_max)
+  const int64_t nh = std::min<int64_t>(n_max, static_cast<int64_t>(n_hat) * bucket);
+  if (n_hat_len) *n_hat_len = static_cast<int32_t>(nh);
+  return static_cast<int32_t>(std::min<int64_t>(static_cast<int64_t>(k) * nh, n_max));
 }
 
 int64_t tb_predictor_length(const double* prefill_abc, const double* predict_abc, double n_x,

@@ -86,10 +86,9 @@ def choose_alpha(prefill_abc, step_pq, n_x: int, n_hat: int, bucket: int, k: int
     """Per-request eviction ratio (Sec. 5.2 deployment): the predicted bucket
     n_hat gives N_hat = min(N_max, n_hat * B) (Eq. predictor_inference), the
     pessimistic length N_hat_W = min(k * N_hat, N_max), and alpha* is the
-    smallest ratio meeting the budget (computed by tb_alpha_star).
+    smallest ratio meeting the budget (tb_response_length and tb_alpha_star).
     Returns (alpha, feasible, N_hat_W)."""
-    n_hat_len = min(n_max, n_hat * bucket)
-    n_hat_w = min(k * n_hat_len, n_max)
+    _, n_hat_w = _lib.tb_response_length(n_hat, bucket, k, n_max)
     alpha, feasible = _lib.tb_alpha_star(prefill_abc, step_pq, float(n_x), n_hat_w, budget,
                                          t_predict, alpha_max)
     return alpha, feasible, n_hat_w

@@ -36,7 +36,6 @@ computation runs in the kernels.
 """
 from __future__ import annotations
 
-import contextlib
 from dataclasses import dataclass
 from typing import Dict, List, Optional, Sequence
 
@@ -260,17 +259,32 @@ class Server:
         self._adm_stream = torch.cuda.Stream(device=device)
         self._adm_done: Optional[torch.cuda.Event] = None
         self._adm_refs: List[torch.Tensor] = []
+        # every stream a decode step has been queued on: steps read the block
+        # table and append into pages, so work that rewrites either waits for them
+        self._step_streams: Dict[int, torch.cuda.Stream] = {}
 
     @property
     def n_active(self) -> int:
         return len(self.slots.slots)
+
+    def _ordered(self, stream=None) -> torch.cuda.Stream:
+        """The stream to queue server work on (decode_stream unless one is
+        given), made to wait for the current stream (which may have produced
+        the inputs) and for every stream a decode step was queued on (a
+        queued step may still read the table rows or append into the pages
+        this work rewrites)."""
+        s = self.decode_stream if stream is None else stream
+        for o in (torch.cuda.current_stream(), *self._step_streams.values()):
+            if o.cuda_stream != s.cuda_stream:
+                s.wait_stream(o)
+        return s
 
     def _upload(self, lo: int, hi: int, lengths: bool, stream=None) -> None:
         """Table rows (and lengths, in every layer) of running slots lo..hi-1,
         queued on the stream without blocking the host."""
         if hi <= lo:
             return
-        stream = stream or torch.cuda.current_stream()
+        stream = self._ordered(stream)
         self._staging.put(self.table[lo:hi], self.slots.table_rows(lo, hi), stream)
         if lengths:
             ln = self.slots.lengths()[lo:hi]
@@ -306,6 +320,7 @@ class Server:
         if self.slots.pending:
             raise RuntimeError("an asynchronous admission is pending: promote it first")
         n_keep = self._check_admission(rids, L, alphas, max_new, prompts)
+        stream = self._ordered(stream)
         lo = self.n_active
         for i in range(len(rids)):
             self.slots.admit(rids[i], n_keep[i], max_new[i], alphas[i], L[i])
@@ -321,7 +336,8 @@ class Server:
         stream created at another time may share the admission stream's
         hardware queue and then runs after it).  The eviction starts after the work
         already queued on the current stream (which may have produced the
-        prompts, or still read pages freed by a retirement).  The new requests
+        prompts) and after every decode step queued so far, on whatever stream
+        (a queued step may still read pages freed by a retirement).  The new requests
         hold the top slots of the table until promote_ready() moves them into
         the running batch (their kept sets, with keep_sets, are complete by
         then); only one such batch may be pending.  If queueing the eviction
@@ -332,7 +348,8 @@ class Server:
         top = self.slots.admit_pending(rids, n_keep, max_new, alphas, L)
         adm = self._adm_stream
         cur = torch.cuda.current_stream()
-        adm.wait_stream(cur)
+        for o in (cur, self.decode_stream, *self._step_streams.values()):
+            adm.wait_stream(o)
         try:
             self._staging.put(self.table[top:top + len(rids)], self.slots.pending_rows(), adm)
             self._adm_refs = [x for p in prompts for x in p.values()]
@@ -361,7 +378,7 @@ class Server:
             return 0
         if not (wait or self._adm_done.query()):
             return 0
-        stream = stream or torch.cuda.current_stream()
+        stream = self._ordered(stream)
         stream.wait_event(self._adm_done)
         lo, hi = self.slots.promote()
         self._upload(lo, hi, lengths=True, stream=stream)
@@ -390,7 +407,7 @@ class Server:
         """Score, select and compact every layer of the requests in slots
         lo..lo+b-1, whose table rows are already on the device; everything,
         the copies of the kept sets included, is queued on `stream`."""
-        with torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext():
+        with torch.cuda.stream(stream):
             self._evict_layers(rids, L, alphas, n_keep, prompts, lo, keep_sets, stream)
 
     def _evict_layers(self, rids, L, alphas, n_keep, prompts, lo, keep_sets, stream) -> None:
@@ -414,7 +431,9 @@ class Server:
     def step(self, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
              out: torch.Tensor, stream=None) -> None:
         """One decode step of the running batch: q, out [n_layers, n, Hq, d],
-        k_new, v_new [n_layers, n, Hkv, d], row i = the request in slot i."""
+        k_new, v_new [n_layers, n, Hkv, d], row i = the request in slot i.
+        Queued on decode_stream unless a stream is given; either way after the
+        current stream's work and after every earlier step."""
         n = self.n_active
         if n == 0:
             raise RuntimeError("no running request")
@@ -422,10 +441,15 @@ class Server:
             raise ValueError(f"q, k_new, v_new and out must be [{self.n_layers}, {n}, ...]")
         if any(e.left <= 0 for e in self.slots.slots):
             raise RuntimeError("retire finished requests before the next step")
+        s = self._ordered(stream)
+        self._step_streams[s.cuda_stream] = s
+        if s.cuda_stream != torch.cuda.current_stream().cuda_stream:
+            for x in (q, k_new, v_new, out):    # not reused before the step has run
+                x.record_stream(s)
         for layer in range(self.n_layers):
             _lib.tb_decode_attn_paged(q[layer], k_new[layer], v_new[layer], self.k_pool[layer],
                                       self.v_pool[layer], self.table, self.kv_len[layer],
-                                      out[layer], self.dec_ws, stream)
+                                      out[layer], self.dec_ws, s)
         self.slots.advance()
 
     def capture(self, n: int) -> torch.cuda.CUDAGraph:
@@ -448,23 +472,29 @@ class Server:
             self._graphs[n] = g
         return g
 
-    def step_graphed(self) -> None:
+    def step_graphed(self, stream=None) -> None:
         """One decode step of the running batch from the static buffers: reads
         q_in / k_in / v_in[:, :n] and writes o_out[:, :n] (n = running
         requests).  The n_layers launches of a batch size are captured once in
-        a graph and replayed on the current stream; the block table and the
-        lengths are read from device memory at replay, so membership changes
-        need no new capture."""
+        a graph and replayed on decode_stream (or the given stream); the block
+        table and the lengths are read from device memory at replay, so
+        membership changes need no new capture."""
         n = self.n_active
         if n == 0:
             raise RuntimeError("no running request")
         if any(e.left <= 0 for e in self.slots.slots):
             raise RuntimeError("retire finished requests before the next step")
-        self.capture(n).replay()
+        g = self.capture(n)
+        s = self._ordered(stream)
+        self._step_streams[s.cuda_stream] = s
+        with torch.cuda.stream(s):
+            g.replay()
         self.slots.advance()
 
     def retire(self, rids: Sequence[int], stream=None) -> None:
-        """Free finished requests; the last running requests move into their slots."""
+        """Free finished requests; the last running requests move into their
+        slots (table rows and lengths re-uploaded on decode_stream, or the
+        given stream, after every queued step)."""
         for r in rids:
             self.slots.retire(r)
             self.keep.pop(r, None)

@@ -53,7 +53,8 @@ def test_hand_example():
 
 @settings(max_examples=200, deadline=None)
 @given(st.floats(1e-9, 1e-6), st.floats(1e-6, 1e-3), st.floats(0.0, 1.0),
-       st.floats(1e-6, 1e-3), st.floats(1e-4, 0.1), st.integers(100, 32768),
+       st.one_of(st.just(0.0), st.floats(1e-6, 1e-3)), st.floats(1e-4, 0.1),
+       st.integers(100, 32768),
        st.integers(1, 600), st.floats(0.5, 60.0), st.floats(0.0, 0.5), st.floats(0.5, 0.99))
 def test_closed_form_equals_bisection(a, b, c, p, q, n_x, n_hat_w, budget, t_pred, amax):
     abc, pq = (a, b, c), (p, q)
@@ -64,6 +65,53 @@ def test_closed_form_equals_bisection(a, b, c, p, q, n_x, n_hat_w, budget, t_pre
         return
     assert feas == rfeas
     assert abs(got - ref) < 1e-9
+
+
+def test_zero_slope_hand_case():
+    """p = 0: the WCET does not depend on alpha (Eq. problem_converted).  With
+    prefill c = 2 s, q = 1/128 s, N_hat_W = 129 (128 decode steps) and
+    t_predict = 0.5 s the worst case is 0.5 + 2 + 128 / 128 = 3.5 s at every
+    alpha (all exact in binary): a budget of 3.5 s is met with no eviction,
+    3.49 s by none."""
+    abc, pq = (0.0, 0.0, 2.0), (0.0, 1.0 / 128)
+    for impl in (C.alpha_star, _lib.tb_alpha_star):
+        assert impl(abc, pq, 1000.0, 129, 3.5, 0.5, 0.95) == (0.0, True)
+        assert impl(abc, pq, 1000.0, 129, 3.49, 0.5, 0.95) == (0.95, False)
+        assert impl(abc, pq, 1000.0, 129, float("inf"), 0.5, 0.95) == (0.0, True)
+    for T in (3.5, 3.49):                       # the constraint by bisection agrees
+        assert _bisect_alpha(abc, pq, 1000.0, 129, T, 0.5, 0.95) == C.alpha_star(
+            abc, pq, 1000.0, 129, T, 0.5, 0.95)
+    assert C.t_wcet(abc, pq, 1000.0, 0.0, 129) == 3.0
+    assert C.t_wcet(abc, pq, 1000.0, 0.9, 129) == 3.0
+
+
+def test_negative_slope_is_rejected():
+    """A step time that falls as the cache grows is not a decode-step model:
+    both implementations return (nan, infeasible), whatever the budget (the
+    closed form would return alpha_max for a budget met at alpha = 0, and 0
+    for one that no alpha meets)."""
+    abc, pq = (0.0, 0.0, 2.0), (-1e-6, 0.01)
+    for impl in (C.alpha_star, _lib.tb_alpha_star):
+        for T in (12.0, 2.5):
+            a, feas = impl(abc, pq, 1000.0, 100, T, 0.0, 0.95)
+            assert math.isnan(a) and not feas
+
+
+def test_response_length_matches_reference():
+    e = _ex()
+    L = e["lengths"]
+    for c in L["cases"]:
+        assert _lib.tb_response_length(c["n_hat"], L["bucket"], L["k"], L["n_max"]) == (
+            c["N_hat"], c["N_hat_W"])
+    rng = np.random.default_rng(11)
+    for _ in range(500):
+        nh, b, k, nmax = (int(rng.integers(0, 600)), int(rng.integers(1, 64)),
+                          int(rng.integers(1, 9)), int(rng.integers(0, 40000)))
+        want = C.predicted_length(nh, b, nmax)
+        assert _lib.tb_response_length(nh, b, k, nmax) == (want, C.pessimistic_length(want, k, nmax))
+    for bad in ((-1, 16, 5, 8192), (3, 0, 5, 8192), (3, 16, 0, 8192), (3, 16, 5, -1)):
+        with pytest.raises(ValueError):
+            _lib.tb_response_length(*bad)
 
 
 def test_printed_second_term_disagrees():
@@ -129,7 +177,8 @@ def test_abi_fit_matches_reference(degree):
 
 @settings(max_examples=200, deadline=None)
 @given(st.floats(0.0, 1e-6), st.floats(0.0, 1e-3), st.floats(0.0, 1.0),
-       st.floats(1e-6, 1e-3), st.floats(1e-4, 0.1), st.integers(100, 32768),
+       st.one_of(st.just(0.0), st.floats(1e-6, 1e-3)), st.floats(1e-4, 0.1),
+       st.integers(100, 32768),
        st.integers(0, 600), st.floats(0.1, 60.0), st.floats(0.0, 0.5), st.floats(0.5, 0.99),
        st.floats(0.0, 0.99))
 def test_abi_wcet_and_alpha_match_reference(a, b, c, p, q, n_x, n_hat_w, budget, t_pred, amax,

@@ -360,6 +360,114 @@ def _async_vs_serial(srv_a, srv_s, L, alphas, max_new, prompts, dec, layers, w, 
     assert len(srv_a.slots.free) == srv_a.slots.n_pages
 
 
+def _rows(srv, r, layers):
+    """The K and V rows of request r in every layer, gathered from its pages
+    (queued on its server's decode stream, after the work queued there)."""
+    e = next(x for x in srv.slots.slots if x.rid == r)
+    with torch.cuda.stream(srv.decode_stream):
+        out = []
+        for layer in range(layers):
+            for g in range(srv.Hkv):
+                out.append(_gather_k(srv.k_pool[layer], e.pages, g, e.length).clone())
+                out.append(torch.cat([srv.v_pool[layer][p, g] for p in e.pages], dim=1)
+                           [:, : e.length].clone())
+        return out
+
+
+def test_server_explicit_stream_admission_after_retire():
+    """Decode steps queued with an explicit stream= outside any stream
+    context, and each retirement followed at once, with no host
+    synchronisation, by an overlapped admission whose batch reuses the pages
+    just freed: the admission must wait for the queued steps (one may still
+    append into a freed page).  Every step's outputs and the new requests'
+    kept rows in their pages equal, bit for bit, those of a server that
+    synchronises and admits serially."""
+    n_req, layers, Hq, Hkv, d, w, pool = 8, 2, 28, 4, 128, 32, 7
+    gen = torch.Generator().manual_seed(515)
+    L = torch.randint(2000, 6000, (n_req,), generator=gen).tolist()
+    alphas = (0.5 * torch.rand(n_req, generator=gen, dtype=torch.float64)).tolist()
+    max_new = torch.randint(3, 9, (n_req,), generator=gen).tolist()
+    case(f"server explicit-stream admission after retire L={L} max_new={max_new}")
+    wl = synth.custom(65, torch.bfloat16, n_req, L, Hq, Hkv, d, w, pool, max(max_new))
+    prompts = [synth.make_prompt(wl, layer, L) for layer in range(layers)]
+    dec = [synth.make_decode(wl, layer) for layer in range(layers)]
+    need = max(_lib.tb_keep_count(n, a, w) + m for n, a, m in zip(L, alphas, max_new))
+    pages = -(-need // PAGE)
+    kw = dict(n_pages=3 * pages, max_seqs=3, max_pages=pages, Hq=Hq, Hkv=Hkv, d=d,
+              dtype=torch.bfloat16, w=w, pool=pool, max_admit=2, max_prompt=max(L))
+    srv_a, srv_s = Server(layers, **kw), Server(layers, **kw)
+
+    def prompt_of(batch):
+        bl = max(L[r] for r in batch)
+        pr = [{key: prompts[layer][key][batch][:, :, :bl].contiguous().to(DEV)
+               for key in ("k", "v")} for layer in range(layers)]
+        for layer in range(layers):
+            pr[layer]["q_win"] = prompts[layer]["q_win"][batch].contiguous().to(DEV)
+        return pr
+
+    def args(batch):
+        return (batch, [L[r] for r in batch], [alphas[r] for r in batch],
+                [max_new[r] for r in batch], prompt_of(batch))
+
+    queue, done = list(range(n_req)), {r: 0 for r in range(n_req)}
+    outs_a, outs_s, rows_a, rows_s = [], [], {}, {}
+    first = [queue.pop(0), queue.pop(0)]
+    srv_a.admit(*args(first))
+    srv_s.admit(*args(first))
+    pend, steps, reused = None, 0, 0
+    while queue or srv_a.n_active or pend:
+        fin = srv_a.slots.finished()
+        if fin:
+            freed = {p for e in srv_a.slots.slots if e.rid in fin for p in e.pages}
+            srv_a.retire(fin)                    # queued behind the steps, no sync
+            srv_s.retire(fin)
+        else:
+            freed = set()
+        if pend is not None and steps >= pend[1]:
+            assert srv_a.promote_ready(wait=True) == len(pend[0])
+            torch.cuda.synchronize()
+            srv_s.admit(*args(pend[0]))
+            torch.cuda.synchronize()
+            for r in pend[0]:
+                rows_a[r], rows_s[r] = _rows(srv_a, r, layers), _rows(srv_s, r, layers)
+            pend = None
+        if pend is None and queue and srv_a.slots.fits(
+                [_lib.tb_keep_count(L[queue[0]], alphas[queue[0]], w) + max_new[queue[0]]]):
+            batch = [queue.pop(0)]
+            srv_a.admit_async(*args(batch))      # right behind the retirement
+            taken = set(srv_a.slots.pending[0].pages)
+            reused += bool(taken & freed)
+            pend = (batch, steps + 1)
+        n = srv_a.n_active
+        if n:
+            rid = srv_a.rids()
+            assert rid == srv_s.rids()
+            qs = torch.stack([torch.stack([dec[l]["q"][done[r], r] for r in rid])
+                              for l in range(layers)]).to(DEV)
+            ks = torch.stack([torch.stack([dec[l]["k_new"][done[r], r] for r in rid])
+                              for l in range(layers)]).to(DEV)
+            vs = torch.stack([torch.stack([dec[l]["v_new"][done[r], r] for r in rid])
+                              for l in range(layers)]).to(DEV)
+            oa, os_ = torch.empty_like(qs), torch.empty_like(qs)
+            srv_a.step(qs, ks, vs, oa, stream=srv_a.decode_stream)    # explicit, no context
+            srv_s.step(qs, ks, vs, os_)
+            outs_a.append(oa)
+            outs_s.append(os_)
+            for r in rid:
+                done[r] += 1
+        steps += 1
+        assert steps < 200, "stream did not drain"
+    torch.cuda.synchronize()
+    assert reused >= 1, "no admission took a page freed by the retirement before it"
+    for t, (a, b) in enumerate(zip(outs_a, outs_s)):
+        assert torch.equal(a, b), f"step {t}: outputs differ"
+    assert set(rows_a) == set(range(2, n_req))
+    for r in rows_a:
+        for x, y in zip(rows_a[r], rows_s[r]):
+            assert torch.equal(x, y), f"request {r}: kept rows differ"
+    assert all(done[r] == max_new[r] for r in range(n_req))
+
+
 def test_server_async_admission_rolls_back_on_error():
     """An admission whose eviction fails while being queued (layer 1's keys
     in the wrong dtype, caught on the host after layer 0 was queued) leaves
