@@ -78,26 +78,26 @@ size_t decode_ws(int32_t B, int32_t Hkv, int32_t G, int32_t d, int32_t cap, bool
 
 namespace tb {
 
-// How a decode step splits the cache (bf16; measured over 410..32768 rows
-// per KV head at 1, 4 and 16 sequences of 4 KV heads, graph-replayed steps):
-// * A CU that holds two partial blocks sets the step time, so a KV head gets
-//   floor(256 / units) blocks (one per CU over the whole grid) and a block
-//   takes as many rows as that needs, however many.  (Capping a block at 1024
-//   rows, as before, put 272 blocks on 256 CUs at 4 x 16k rows: 33 us per
-//   step instead of 24.)
-// * The block's rows are split over 1, 2, 4 or 8 waves: rounding a chunk up to
-//   a multiple of 32 rows per wave can cost blocks, so among the shapes that
-//   keep at least 80% of the best block count, the one with the most waves
-//   that still gives each wave >= 64 rows (more loads in flight per CU,
-//   shorter per-wave chains).
+// How a decode step splits the cache (bf16).  Measured on one layer (cache
+// resident in the last-level cache) and on the 28-layer shape (each layer's
+// cache streamed from HBM), 410..32768 rows per KV head, graph-replayed steps:
+// * One partial block per CU: a KV head gets C = floor(256 / units) blocks,
+//   and its cap/32 tiles are split between them as evenly as whole tiles
+//   allow (blocks of a fixed row count left up to 48 CUs idle; a second
+//   round of blocks past 256 doubles the step time).
+// * A block's tiles are shared by the most waves (1, 2, 4 or 8) that still
+//   give every wave a tile: with two waves per SIMD (the register budget)
+//   more waves keep more tiles in flight per CU.  At 28 layers, 32768 rows:
+//   18.4-18.7 us per layer-step with 8 waves against 19.3 (4) and 20.5 (2);
+//   16384 rows: 13.4 against 13.8 (4); 8192 rows: 10.9 (4) against 11.2 (2).
 // * Small caches (<= 2560 rows) keep at most 32 partials per KV head, which
 //   one wave per query head merges in a single round of loads.
 // * Batches (B > 1) are usually ragged, and the plan sees only the capacity:
 //   blocks past a sequence's length exit at once, so small blocks (one wave,
-//   at most 384 rows) balance the real work across CUs.  On ragged batches and
+//   about 12 tiles) balance the real work across CUs.  On ragged batches and
 //   a 64-request serving stream this was 11-28% faster than one block per CU
 //   per KV head; on uniform batches it costs 2-6%.
-// fp32 runs the vector-ALU kernel at a fixed block shape, sized the old way.
+// fp32 runs the vector-ALU kernel over blocks of `chunk` rows.
 DecodePlan decode_plan(int B, int Hkv, int cap, bool bf16) {
   const long long units = static_cast<long long>(B) * Hkv;
   DecodePlan p{};
@@ -111,28 +111,21 @@ DecodePlan decode_plan(int B, int Hkv, int cap, bool bf16) {
     p.n_chunks = (cap + p.chunk - 1) / p.chunk;
     return p;
   }
-  const long long per_unit = std::max<long long>(1, 256 / units);
-  long long rows = (cap + per_unit - 1) / per_unit;
-  if (cap <= 2560) rows = std::max<long long>(rows, (cap + 31) / 32);
-  long long chunk[4], blocks[4], best_blocks = 0;
-  for (int i = 0; i < 4; ++i) {
-    const long long unit = static_cast<long long>(kVTile) << i;      // 32 rows per wave
-    chunk[i] = (rows + unit - 1) / unit * unit;
-    blocks[i] = units * ((cap + chunk[i] - 1) / chunk[i]);
-    best_blocks = std::max(best_blocks, blocks[i]);
-  }
-  int pick = 0;
-  for (int i = 1; i < 4; ++i)
-    if (blocks[i] * 5 >= best_blocks * 4 && (chunk[i] >> i) >= 64) pick = i;
-  p.waves = 1 << pick;
-  p.chunk = static_cast<int32_t>(chunk[pick]);
-  constexpr int kBatchChunk = 384;
-  if (B > 1 && p.chunk > kBatchChunk) {
-    const long long floor_rows = (static_cast<long long>(cap) + decode_max_chunks() - 1) / decode_max_chunks();
-    p.waves = 1;
-    p.chunk = static_cast<int32_t>(std::max<long long>(kBatchChunk, (floor_rows + 31) / 32 * 32));
-  }
-  p.n_chunks = (cap + p.chunk - 1) / p.chunk;
+  const long long tiles = std::max<long long>(1, cap / kVTile);
+  long long C = std::max<long long>(1, 256 / units);
+  if (cap <= 2560) C = std::min<long long>(C, 32);
+  C = std::min(C, tiles);
+  constexpr long long kBatchTiles = 12;
+  const bool batch = B > 1 && tiles / C > kBatchTiles;
+  if (batch) C = (tiles + kBatchTiles - 1) / kBatchTiles;
+  C = std::max<long long>(1, std::min<long long>({C, tiles, decode_max_chunks()}));
+  const long long per_block = tiles / C;       // every block holds per_block or per_block + 1
+  int waves = 1;
+  if (!batch)
+    while (waves < 8 && 2 * waves <= per_block) waves *= 2;
+  p.waves = waves;
+  p.n_chunks = static_cast<int32_t>(C);
+  p.chunk = static_cast<int32_t>((tiles + C - 1) / C * kVTile);   // rows of the largest block
   return p;
 }
 

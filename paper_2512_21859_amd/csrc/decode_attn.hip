@@ -9,12 +9,16 @@
 // 32-row step then starts with one table lookup.
 //
 // Two launches per decode step and layer (both capturable in a HIP graph):
-//   partial kernel, grid = (n_chunks, Hkv, B): block (c, g, b) covers key
-//     rows [c*chunk, (c+1)*chunk) of KV head g of sequence b for all
+//   partial kernel, grid = (n_chunks, Hkv, B): block (c, g, b) covers a
+//     share of the 32-row tiles of KV head g of sequence b for all
 //     G = Hq/Hkv query heads of the group, so every K/V byte is read from HBM
-//     once per step, and writes one partial (m, l, o[G][d]).  A block has one
-//     wave (the wave stores its partial from registers) or 2, 4 or 8 (each
-//     takes an equal share of the rows; the block combines them through LDS).
+//     once per step, and writes one partial (m, l, o[G][d]).  bf16: the cap/32
+//     tiles are split as evenly as whole tiles allow (block c takes tiles
+//     [c T / C, (c + 1) T / C), T tiles, C blocks), so one block per CU covers
+//     the cache with no CU left idle; fp32: blocks of `chunk` rows.  A block
+//     has one wave (the wave stores its partial from registers) or 2, 4 or 8
+//     (bf16: wave w takes every WAVES-th tile of the block from its w-th on;
+//     the block combines the waves through LDS).
 //   merge kernel, grid = (Hq, B): combines a query head's chunk partials by
 //     log-sum-exp in a fixed order, writes the output; the block of query
 //     head 0 advances kv_len[b].  One wave per query head when one round of
@@ -75,10 +79,10 @@ void decode_mfma_kernel(DecodeArgs a) {
   const uint16_t* kn = static_cast<const uint16_t*>(a.k_new) + bg * D;
   const uint16_t* vn = static_cast<const uint16_t*>(a.v_new) + bg * D;
   const int cap = a.cap;
-  const int lo = c * a.chunk;
-  const int per_wave = a.chunk / WAVES;          // multiple of 32
-  const int wlo = lo + wave * per_wave;
-  const int wend = min(wlo + per_wave, cap);     // static bound: no length needed
+  const int n_tiles = cap / kVT;
+  const int t_lo = static_cast<int>(static_cast<long long>(c) * n_tiles / a.n_chunks);
+  const int t_hi = static_cast<int>(static_cast<long long>(c + 1) * n_tiles / a.n_chunks);
+  const int t_first = t_lo + wave;               // this wave: t_first, t_first + WAVES, ...
   // K tile row permutation: MFMA row r of tile t <-> key 8*(r/4) + 4*t + r%4.
   const int krow0 = 8 * (r16 >> 2) + (r16 & 3);
 
@@ -99,7 +103,7 @@ void decode_mfma_kernel(DecodeArgs a) {
     for (int n = 0; n < NC; ++n) vr[n] = ld16(vtile + (16 * n + r16) * kVT + 8 * q4);
   };
   int n0 = a.kv_len[b];
-  if (wlo < wend) load_block(wlo);
+  if (t_first < t_hi) load_block(kVT * t_first);
 
   // Q^T operand: lane holds head r16, d = 32*kc + 8*q4 .. +8 (zero past G).
   bf16x8 qB[KC];
@@ -126,12 +130,11 @@ void decode_mfma_kernel(DecodeArgs a) {
   n0 = n0 < 0 ? 0 : (n0 > cap ? cap : n0);
   const int app = (a.append && n0 < cap) ? 1 : 0;
   const int N = n0 + app;
-  const int hi = min(lo + a.chunk, N);
-  const int whi = min(wend, N);
+  const int t_end = min(t_hi, (N + kVT - 1) / kVT);   // tiles holding a row below N
 
   // The block owning row n0 stores the appended row (K row, V^T column) from
   // the registers that already hold it: no reload, nothing waits on it.
-  if (app && n0 >= lo && n0 < hi && wave == 0) {
+  if (app && n0 / kVT >= t_lo && n0 / kVT < t_hi && wave == 0) {
     const size_t off = cache_tile_off<PAGED>(a, b, g, n0 / kVT, D);
     if (r16 == 0) {
       uint16_t* kd = static_cast<uint16_t*>(a.k_cache) + off + static_cast<size_t>(n0 % kVT) * D;
@@ -151,7 +154,8 @@ void decode_mfma_kernel(DecodeArgs a) {
   float m_run = -INFINITY;   // running max of head r16 (same in the 4 lane groups)
   float l_part = 0.f;        // this lane's share of the running sum of head r16
 
-  for (int base = wlo; base < whi; base += kVT) {
+  for (int t = t_first; t < t_end; t += WAVES) {
+    const int base = kVT * t;
     u32x4 ck[2][KC], cv[NC];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -159,11 +163,11 @@ void decode_mfma_kernel(DecodeArgs a) {
       for (int k = 0; k < KC; ++k) ck[t][k] = kr[t][k];
 #pragma unroll
     for (int n = 0; n < NC; ++n) cv[n] = vr[n];
-    if (base + kVT < whi) load_block(base + kVT);     // prefetch the next block
+    if (t + WAVES < t_end) load_block(kVT * (t + WAVES));   // prefetch the next tile
 
-    // wave-uniform: does this block hold the appended row, or run past the end?
+    // wave-uniform: does this tile hold the appended row, or run past the end?
     const bool has_new = app && n0 >= base && n0 < base + kVT;
-    const bool tail = base + kVT > whi;
+    const bool tail = base + kVT > N;
     // ---- the appended row's K slices replace the (stale) cache rows
     if (has_new) {
 #pragma unroll
@@ -189,7 +193,7 @@ void decode_mfma_kernel(DecodeArgs a) {
     if (tail) {
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        if (base + 8 * q4 + j >= whi) s[j] = -INFINITY;
+        if (base + 8 * q4 + j >= N) s[j] = -INFINITY;
     }
     float mt = s[0];
 #pragma unroll
@@ -197,7 +201,7 @@ void decode_mfma_kernel(DecodeArgs a) {
     mt = fmaxf(mt, __shfl_xor(mt, 16));
     mt = fmaxf(mt, __shfl_xor(mt, 32));
     const float m_new = fmaxf(m_run, mt);
-    // m_new is finite: every block has at least one valid key (base < whi)
+    // m_new is finite: every tile visited has at least one valid key (base < N)
     const float corr = exp2f(m_run - m_new);
     m_run = m_new;
     float p[8];
@@ -213,7 +217,7 @@ void decode_mfma_kernel(DecodeArgs a) {
     // (branch-free word masks over this lane's 8 keys)
     if (tail || has_new) {
       const int kq = base + 8 * q4;               // first key of this lane's 8
-      const int cnt = min(max(whi - kq, 0), 8);   // valid keys among the 8
+      const int cnt = min(max(N - kq, 0), 8);     // valid keys among the 8
       const int pos = n0 - kq;                    // slot of the appended row
       const bool inr = app && pos >= 0 && pos < cnt;
       const int pw = pos >> 1;

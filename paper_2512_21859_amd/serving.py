@@ -279,6 +279,14 @@ class Server:
                 s.wait_stream(o)
         return s
 
+    @staticmethod
+    def _publish(s: torch.cuda.Stream) -> None:
+        """Order the caller's current stream after the work just queued on s,
+        so outputs, lengths and the table are read there in program order."""
+        cur = torch.cuda.current_stream()
+        if cur.cuda_stream != s.cuda_stream:
+            cur.wait_stream(s)
+
     def _upload(self, lo: int, hi: int, lengths: bool, stream=None) -> None:
         """Table rows (and lengths, in every layer) of running slots lo..hi-1,
         queued on the stream without blocking the host."""
@@ -326,6 +334,7 @@ class Server:
             self.slots.admit(rids[i], n_keep[i], max_new[i], alphas[i], L[i])
         self._upload(lo, lo + len(rids), lengths=False, stream=stream)
         self._evict(rids, L, alphas, n_keep, prompts, lo, keep_sets, stream)
+        self._publish(stream)
         return n_keep
 
     def admit_async(self, rids: Sequence[int], L: Sequence[int], alphas: Sequence[float],
@@ -382,6 +391,7 @@ class Server:
         stream.wait_event(self._adm_done)
         lo, hi = self.slots.promote()
         self._upload(lo, hi, lengths=True, stream=stream)
+        self._publish(stream)
         self._adm_refs = []
         return hi - lo
 
@@ -433,7 +443,8 @@ class Server:
         """One decode step of the running batch: q, out [n_layers, n, Hq, d],
         k_new, v_new [n_layers, n, Hkv, d], row i = the request in slot i.
         Queued on decode_stream unless a stream is given; either way after the
-        current stream's work and after every earlier step."""
+        current stream's work and after every earlier step, and the current
+        stream is ordered after it (out can be read there)."""
         n = self.n_active
         if n == 0:
             raise RuntimeError("no running request")
@@ -450,6 +461,7 @@ class Server:
             _lib.tb_decode_attn_paged(q[layer], k_new[layer], v_new[layer], self.k_pool[layer],
                                       self.v_pool[layer], self.table, self.kv_len[layer],
                                       out[layer], self.dec_ws, s)
+        self._publish(s)
         self.slots.advance()
 
     def capture(self, n: int) -> torch.cuda.CUDAGraph:
@@ -489,6 +501,7 @@ class Server:
         self._step_streams[s.cuda_stream] = s
         with torch.cuda.stream(s):
             g.replay()
+        self._publish(s)
         self.slots.advance()
 
     def retire(self, rids: Sequence[int], stream=None) -> None:
@@ -498,7 +511,9 @@ class Server:
         for r in rids:
             self.slots.retire(r)
             self.keep.pop(r, None)
-        self._upload(0, self.n_active, lengths=True, stream=stream)
+        s = self._ordered(stream)
+        self._upload(0, self.n_active, lengths=True, stream=s)
+        self._publish(s)
 
     def rids(self) -> List[int]:
         return [e.rid for e in self.slots.slots]

@@ -1,7 +1,8 @@
 """Single-sequence decode at cache sizes chosen to hit every launch shape of
-the split (one-, two-, four- and eight-wave partial blocks, and the small-cache
-split with at most 32 partials merged by one wave per query head), checked
-against the float64 oracle at both head dimensions."""
+the split (one-, two-, four- and eight-wave partial blocks over an even share
+of the tiles, and the small-cache split with at most 32 partials merged by
+one wave per query head), checked against the float64 oracle at both head
+dimensions."""
 import numpy as np
 import pytest
 import torch
@@ -22,12 +23,15 @@ def _gpu():
     torch.cuda.init()
 
 
-# capacities (rows) and the block shape the plan gives 4 KV heads at each
-CAPS = [672,      # <= 2560 rows: one-wave blocks, <= 32 partials
-        4352,     # one-wave blocks of 96 rows
-        8448,     # two-wave blocks
-        12352,    # four-wave blocks
-        24640]    # eight-wave blocks
+# capacities (rows) and the block shape the plan gives 4 KV heads at each:
+# one block per CU (64 per KV head), the cap/32 tiles split evenly, one wave
+# per tile up to 8
+CAPS = [672,      # <= 2560 rows: 21 one-tile blocks per KV head, <= 32 partials
+        2816,     # 64 blocks of 1-2 tiles, one wave
+        4352,     # two-wave blocks of 2-3 tiles
+        8448,     # four-wave blocks of 4-5 tiles
+        24640,    # eight-wave blocks of 12-13 tiles (a wave takes 1-2)
+        33024]    # eight-wave blocks of 16-17 tiles (a wave takes 2-3)
 
 
 @pytest.mark.parametrize("d", [128, 64])
