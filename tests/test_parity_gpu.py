@@ -389,16 +389,18 @@ def test_workload1_tiny_fp32():
 
 @pytest.mark.parametrize("alpha", synth.WORKLOADS[2].alphas)
 def test_workload2_single_layer(alpha):
+    """Every one of the 256 decode steps checked against the oracle."""
     wl = synth.WORKLOADS[2]
     case(f"{wl.name} alpha={alpha}")
-    _run_layer(wl, 0, [wl.L], [alpha], wl.T, _steps(wl.T))
+    _run_layer(wl, 0, [wl.L], [alpha], wl.T, range(wl.T))
 
 
 def test_workload4_ragged():
+    """16 ragged sequences, every one of the 256 decode steps checked."""
     wl = synth.WORKLOADS[4]
     L, alphas = synth.lengths_and_alphas(wl)
     case(f"{wl.name} L={L}")
-    _run_layer(wl, 0, L, alphas, wl.T, _steps(wl.T, 64))
+    _run_layer(wl, 0, L, alphas, wl.T, range(wl.T))
 
 
 @pytest.mark.parametrize("seed", range(12))
@@ -423,23 +425,31 @@ def test_full_chain_random_shapes(seed):
     _run_layer(wl, 0, L, alphas, T, range(T))
 
 
-def test_workload3_layers_and_sweep():
+W3_DECODE_LAYERS = (0, 13, 27)
+
+
+@pytest.mark.parametrize("layer", range(synth.WORKLOADS[3].layers))
+def test_workload3_layer(layer):
+    """One layer of the 28-layer stack at all 20 ratios k/20: eviction
+    (scores, selection, compaction) checked at every ratio; decode checked at
+    the first, second, last and every 16th step on layers 0, 13 and 27, and
+    at the first and last step on the others."""
     wl = synth.WORKLOADS[3]
-    case(f"{wl.name}: eviction on every layer at 5 ratios, decode checked on 3 layers")
-    for layer in range(wl.layers):
-        pr = synth.make_prompt(wl, layer)
-        dc = synth.make_decode(wl, layer)
-        alphas = wl.alphas[::4] if layer not in (0, 13, 27) else wl.alphas[::2]
-        for a in alphas:
-            steps = [0, wl.T - 1] if layer in (0, 13, 27) else []
-            _run_layer(wl, layer, [wl.L], [a], wl.T, steps, prompt=pr, dec=dc)
+    steps = _steps(wl.T) if layer in W3_DECODE_LAYERS else [0, wl.T - 1]
+    case(f"{wl.name} layer={layer}: eviction at {len(wl.alphas)} ratios, decode steps {steps}")
+    pr = synth.make_prompt(wl, layer)
+    dc = synth.make_decode(wl, layer)
+    for a in wl.alphas:
+        _run_layer(wl, layer, [wl.L], [a], wl.T, steps, prompt=pr, dec=dc)
 
 
 @pytest.mark.parametrize("alpha", synth.WORKLOADS[5].alphas)
 def test_workload5_long_context(alpha):
+    """L = 131072: decode checked at the first, second, last and every 16th
+    of the 512 steps."""
     wl = synth.WORKLOADS[5]
     case(f"{wl.name} alpha={alpha}")
-    _run_layer(wl, 0, [wl.L], [alpha], wl.T, [0, 255, wl.T - 1])
+    _run_layer(wl, 0, [wl.L], [alpha], wl.T, _steps(wl.T))
 
 
 # ------------------------------------------------------------------ properties
