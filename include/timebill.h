@@ -202,7 +202,11 @@ tb_status tb_compact_kv(const void* k, const void* v, const int32_t* keep_idx,
  * bf16 uses the matrix cores (P rounded to bf16 for the PV product); fp32
  * keeps fp32 products.  Requires cap % 32 == 0.
  * The library cannot see kv_len: the caller must keep kv_len[b] + 1 <= cap
- * when appending (an append that would overflow is dropped on the device).
+ * when appending.  A device length outside [0, cap] is clamped into it; if
+ * kv_len[b] is cap when a row is to be appended, the append is dropped on the
+ * device: k_new/v_new are not stored, out[b] is the attention over the cap
+ * cached rows (without the new token), kv_len[b] stays cap, and the call
+ * still returns TB_OK (the status is decided on the host before any launch).
  * Two kernels are enqueued (chunk partials, then their merge).
  * ws: tb_workspace_bytes(TB_OP_DECODE, B, 0, Hq, Hkv, d, 0, cap) bytes (no
  * initialisation needed).  Calls sharing a workspace must not overlap. */
@@ -211,6 +215,24 @@ tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new,
                          int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
                          int32_t cap, tb_dtype dt, void* out, void* ws,
                          size_t ws_bytes, hipStream_t stream);
+
+/* tb_decode_attn without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the chunk partials go to a scratch array
+ * of TB_DECODE_SCRATCH_BYTES that the library holds in each GPU's memory from
+ * load to process exit.  Same arguments, kernels, launch plan and results as
+ * tb_decode_attn.  Calls whose workspace need,
+ * tb_workspace_bytes(TB_OP_DECODE, B, 0, Hq, Hkv, d, 0, cap), exceeds the
+ * scratch return TB_EWORKSPACE before any launch.  Every call on a GPU uses
+ * that GPU's one scratch array: calls that overlap on one GPU (different
+ * streams, or graphs replayed concurrently) race and give wrong results;
+ * stream-ordered calls are safe.  No memory is allocated or freed (the
+ * scratch address is looked up once per device, on the first call there). */
+#define TB_DECODE_SCRATCH_BYTES ((size_t)16 << 20)
+tb_status tb_decode_attn_noalloc(const void* q, const void* k_new, const void* v_new,
+                                 void* k_cache, void* v_cache, int32_t* kv_len,
+                                 int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
+                                 int32_t cap, tb_dtype dt, void* out, hipStream_t stream);
 
 /* ---- paged caches (serving) --------------------------------------------
  * The same compaction and decode over caches kept in pages of 32 rows, one

@@ -23,7 +23,7 @@ V_TILE = 32          # the compact V cache is stored as transposed tiles of 32 r
 
 EXPORTED = ("tb_keep_count", "tb_last_error", "tb_workspace_bytes", "tb_score_window",
             "tb_score_window_avgpool", "tb_score_knorm", "tb_score_h2o", "tb_prefill_attn",
-            "tb_select_topk", "tb_compact_kv_paged", "tb_decode_attn_paged", "tb_compact_kv", "tb_decode_attn", "tb_ete_fit", "tb_wcet",
+            "tb_select_topk", "tb_compact_kv_paged", "tb_decode_attn_paged", "tb_compact_kv", "tb_decode_attn", "tb_decode_attn_noalloc", "tb_ete_fit", "tb_wcet",
             "tb_alpha_star", "tb_response_length", "tb_predictor_length")
 
 _lib = None
@@ -78,6 +78,9 @@ def load() -> ctypes.CDLL:
     lib.tb_decode_attn.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp,
                                    sz, vp]
     lib.tb_decode_attn.restype = i32
+    lib.tb_decode_attn_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
+                                           vp, vp]
+    lib.tb_decode_attn_noalloc.restype = i32
     lib.tb_ete_fit.argtypes = [p_dbl, p_dbl, i32, i32, p_dbl]
     lib.tb_ete_fit.restype = i32
     lib.tb_wcet.argtypes = [p_dbl, p_dbl, dbl, dbl, i32]
@@ -313,6 +316,27 @@ def tb_decode_attn(q: torch.Tensor, k_new: Optional[torch.Tensor], v_new: Option
         _dev(v_cache, "v_cache"), _dev(kv_len, "kv_len", torch.int32), B, Hq, Hkv, d, cap,
         _dtype_code(q), _dev(out, "out"), _dev(ws, "ws"), ws.numel() * ws.element_size(),
         _stream(stream)))
+
+
+def tb_decode_attn_noalloc(q: torch.Tensor, k_new: Optional[torch.Tensor],
+                           v_new: Optional[torch.Tensor], k_cache: torch.Tensor,
+                           v_cache: torch.Tensor, kv_len: torch.Tensor, out: torch.Tensor,
+                           stream=None) -> None:
+    """tb_decode_attn with the library's scratch in place of a workspace."""
+    B, Hq, d = q.shape
+    Hkv = k_cache.shape[1]
+    cap = _check_caches(k_cache, v_cache, B, Hkv, d)
+    if out.shape != q.shape:
+        raise ValueError("out must match q")
+    for t, name in ((k_new, "k_new"), (v_new, "v_new")):
+        if t is not None and tuple(t.shape) != (B, Hkv, d):
+            raise ValueError(f"{name} must be [B, Hkv, d]")
+    if any(t is not None and t.dtype != q.dtype for t in (k_new, v_new, k_cache, v_cache, out)):
+        raise TypeError("decode tensors must share a dtype")
+    _check(load().tb_decode_attn_noalloc(
+        _dev(q, "q"), _dev(k_new, "k_new"), _dev(v_new, "v_new"), _dev(k_cache, "k_cache"),
+        _dev(v_cache, "v_cache"), _dev(kv_len, "kv_len", torch.int32), B, Hq, Hkv, d, cap,
+        _dtype_code(q), _dev(out, "out"), _stream(stream)))
 
 
 class KVCache:

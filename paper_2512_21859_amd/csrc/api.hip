@@ -412,12 +412,16 @@ tb_status compact_impl(const char* name, const void* k, const void* v, const int
   }
 }
 
+// use_scratch: the partials go to the library-held scratch array (ws and
+// ws_bytes are ignored); the need is checked against its size before any HIP
+// call.
 tb_status decode_impl(const char* name, const void* q, const void* k_new, const void* v_new,
                       void* k_cache, void* v_cache, int32_t* kv_len, int32_t B, int32_t Hq,
                       int32_t Hkv, int32_t d, int32_t cap, const Paging* pg, tb_dtype dt,
-                      void* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+                      void* out, void* ws, size_t ws_bytes, hipStream_t stream,
+                      bool use_scratch = false) {
   try {
-    if (!q || !k_cache || !v_cache || !kv_len || !out || !ws)
+    if (!q || !k_cache || !v_cache || !kv_len || !out || (!ws && !use_scratch))
       return fail(TB_EINVAL, "%s: null pointer", name);
     if ((k_new == nullptr) != (v_new == nullptr))
       return fail(TB_EINVAL, "%s: k_new and v_new must both be given or both NULL", name);
@@ -430,6 +434,16 @@ tb_status decode_impl(const char* name, const void* q, const void* k_new, const 
       return fail(TB_EINVAL, "cap must be a multiple of %d (got %d)", tb::kVTile, cap);
     const bool bf16 = dt == TB_BF16;
     const size_t need = decode_ws(B, Hkv, G, d, cap, bf16);
+    if (use_scratch) {
+      if (need > TB_DECODE_SCRATCH_BYTES)
+        return fail(TB_EWORKSPACE,
+                    "%s: this call needs %zu bytes of workspace; the library's scratch holds "
+                    "%zu (use tb_decode_attn with a workspace)",
+                    name, need, static_cast<size_t>(TB_DECODE_SCRATCH_BYTES));
+      const hipError_t e = tb::decode_scratch(&ws);
+      if (e != hipSuccess) return hip_status(e, "decode scratch lookup");
+      ws_bytes = TB_DECODE_SCRATCH_BYTES;
+    }
     if (ws_bytes < need)
       return fail(TB_EWORKSPACE, "%s: workspace %zu < %zu bytes", name, ws_bytes, need);
     tb::DecodeArgs a{};
@@ -494,6 +508,14 @@ tb_status tb_decode_attn(const void* q, const void* k_new, const void* v_new, vo
                          size_t ws_bytes, hipStream_t stream) {
   return decode_impl("tb_decode_attn", q, k_new, v_new, k_cache, v_cache, kv_len, B, Hq, Hkv, d,
                      cap, nullptr, dt, out, ws, ws_bytes, stream);
+}
+
+tb_status tb_decode_attn_noalloc(const void* q, const void* k_new, const void* v_new,
+                                 void* k_cache, void* v_cache, int32_t* kv_len, int32_t B,
+                                 int32_t Hq, int32_t Hkv, int32_t d, int32_t cap, tb_dtype dt,
+                                 void* out, hipStream_t stream) {
+  return decode_impl("tb_decode_attn_noalloc", q, k_new, v_new, k_cache, v_cache, kv_len, B, Hq,
+                     Hkv, d, cap, nullptr, dt, out, nullptr, 0, stream, /*use_scratch=*/true);
 }
 
 tb_status tb_decode_attn_paged(const void* q, const void* k_new, const void* v_new,

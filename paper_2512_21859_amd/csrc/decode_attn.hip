@@ -38,6 +38,9 @@
 // launch.  Lengths are read on the device only.  No atomics; every reduction
 // has a fixed order, so results are bit-reproducible.
 
+#include <mutex>
+
+#include "../../include/timebill.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -686,6 +689,34 @@ hipError_t launch_g(const DecodeArgs& a, int G, hipStream_t st) {
 
 int decode_chunk_unit(int waves, bool bf16) { return bf16 ? waves * kVT : kValuWaves * kRowsPerIter; }
 int decode_max_chunks() { return 4096; }
+
+// Workspace of tb_decode_attn_noalloc: one array per GPU, held from load to
+// process exit.  Host code never passes the array's name to a kernel (on the
+// host it is a stand-in, not a device address): decode_scratch() looks up the
+// current device's address once and hands that out.
+namespace {
+static __device__ __align__(256) unsigned char scratch[TB_DECODE_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices];
+}  // namespace
+
+hipError_t decode_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_addr[dev] = p;
+  }
+  *ptr = g_scratch_addr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_decode(const DecodeArgs& a, int G, int d, bool bf16, hipStream_t st) {
   if (bf16) return d == 128 ? launch_g<bf16_t, 128>(a, G, st) : launch_g<bf16_t, 64>(a, G, st);

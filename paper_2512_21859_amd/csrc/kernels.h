@@ -146,5 +146,8 @@ DecodePlan decode_plan(int B, int Hkv, int cap, bool bf16);
 int decode_chunk_unit(int waves, bool bf16);
 int decode_max_chunks();
 hipError_t launch_decode(const DecodeArgs& a, int G, int d, bool bf16, hipStream_t st);
+// The current device's address of the library-held decode scratch array
+// (TB_DECODE_SCRATCH_BYTES); looked up once per device.
+hipError_t decode_scratch(void** ptr);
 
 }  // namespace tb

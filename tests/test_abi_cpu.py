@@ -258,6 +258,26 @@ def test_decode_validation(lib):
     assert call(ws=None) == E.TB_EINVAL
 
 
+def test_decode_noalloc_validation(lib):
+    """The entry point without a workspace validates like tb_decode_attn and
+    refuses, before any HIP call, a call whose workspace need exceeds the
+    library's 16 MiB scratch."""
+    E = _lib
+
+    def call(B=1, Hq=28, Hkv=4, d=128, cap=128, kn=FAKE, vn=FAKE, q=FAKE):
+        return lib.tb_decode_attn_noalloc(q, kn, vn, FAKE, FAKE, FAKE, B, Hq, Hkv, d, cap,
+                                          _lib.TB_BF16, FAKE, None)
+
+    assert call(q=None) == E.TB_EINVAL
+    assert call(kn=None) == E.TB_EINVAL
+    assert call(Hq=36, Hkv=4) == E.TB_EUNSUPPORTED
+    assert call(cap=100) == E.TB_EINVAL
+    big = dict(B=64, Hq=64, Hkv=8, d=128, cap=65536)
+    assert _lib.tb_workspace_bytes(_lib.TB_OP_DECODE, 64, 0, 64, 8, 128, 0, 65536) > 16 << 20
+    assert call(**big) == E.TB_EWORKSPACE
+    assert b"scratch" in lib.tb_last_error()
+
+
 def test_compact_paged_validation(lib):
     E = _lib
 
