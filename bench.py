@@ -1,28 +1,41 @@
 """Benchmark of the eviction + decode hot path on one MI355X.
 
-Workload: one bf16 layer with a prompt of L = 8192 tokens, 28 query / 4 KV
-heads of dimension 128, observation window 32, max-pool 7, swept over the
-eviction ratios alpha in {0, 0.25, 0.5, 0.75, 0.95} (no eviction plus the
-paper's fixed-ratio arms), 256 decode steps per ratio.  Inputs are seeded
-synthetic tensors already resident in HBM when timing starts.
+Headline workload: a 28-layer stack with the Qwen2.5-7B attention shape
+(28 query / 4 KV heads of dimension 128, bf16), a prompt of L = 32768 tokens
+(the paper's context), independent random K/V per layer, observation window
+32, max-pool 7, swept over the eviction ratios alpha = k/20, k = 0..19, with
+128 decode tokens per ratio.  Inputs are seeded synthetic tensors already
+resident in HBM when timing starts.
 
-One step = for every alpha: score the window, select, compact (one eviction,
-as after a prefill), then 256 decode steps (append + attention), replayed
-from a HIP graph captured once.  The metric is decode tokens per second over
-the whole step (eviction time included); per-alpha rows give the decode time
-per token and the achieved bandwidth.
+One step = for every alpha: evict every layer (score the window, select,
+compact: once per request, as after a prefill), then 128 decode tokens, one
+token being the decode step (append + attention) of all 28 layers in order,
+replayed from a HIP graph captured once per ratio.  The metric is decode
+tokens per second over the whole step (eviction included); per-ratio rows
+give the eviction time, the time per token and the achieved bandwidth, and
+the per-token time is fitted with the execution-time model's decode-step form
+t = p N_kv + q.
 
-The roofline entry is for the decode-attention kernel, the dominant one:
-algorithmic bytes per launch (K and V rows of the cache plus q, the new K/V
-row and the output) divided by its average launch duration, measured with
-HIP events recorded on the stream the graphs replay on.  The CPU baseline is
-the float64 oracle on this host, on a bounded sample of the same workload.
+The roofline entry is for the decode call (tb_decode_attn: the split-K partial
+kernel decode_mfma_kernel and its merge kernel), the dominant work:
+algorithmic bytes per call (K and V rows of the cache plus q, the new K/V row
+and the output) divided by the average call duration, measured with HIP
+events recorded on the stream the graphs replay on (the gaps between the two
+kernels included).  The CPU baseline is the float64 oracle on this host, on a
+bounded sample of the same workload.
 """
-from __future__ import annotations
+import os
+
+# The CPU baseline's BLAS threads: the host's CPUs available to this process,
+# capped by a thread count the environment already sets; fixed before numpy
+# (imported by torch) loads its thread pools.
+_HOST_CPUS = len(os.sched_getaffinity(0))
+_BLAS_THREADS = min(_HOST_CPUS, int(os.environ.get("OMP_NUM_THREADS", _HOST_CPUS) or _HOST_CPUS))
+for _v in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
+    os.environ[_v] = str(_BLAS_THREADS)
 
 import argparse
 import json
-import os
 import sys
 import time
 
@@ -36,17 +49,15 @@ HBM_PEAK_GBS = 8000.0
 def _parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="minimum CPU time of the oracle baseline sample")
+    ap.add_argument("--no-single", action="store_true",
+                    help="skip the single-layer L=8192 ratio sweep (and its cold-cache run)")
     ap.add_argument("--no-long-context", action="store_true",
                     help="skip the supplementary long-context decode measurement")
-    ap.add_argument("--no-cold", action="store_true",
-                    help="skip the cold-cache decode measurement (caches rotated over 1 GiB)")
-    ap.add_argument("--no-layer-sweep", action="store_true",
-                    help="skip the supplementary 28-layer L=32768 ratio sweep")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the 2 GiB read / copy bandwidth ceilings")
     ap.add_argument("--no-prefill", action="store_true",
@@ -55,10 +66,15 @@ def _parse():
                     help="skip the scorer-variant timings")
     ap.add_argument("--no-paged", action="store_true",
                     help="skip the paged-cache batch and serving-stream measurements")
-    ap.add_argument("--only", choices=("cold", "long", "layers", "ceiling", "scorers", "prefill",
-                                       "paged"),
-                    help="run one supplementary measurement alone and print its JSON "
-                         "(for profiling that workload by itself)")
+    ap.add_argument("--only", choices=("headline", "single", "long", "ceiling", "scorers",
+                                       "prefill", "paged"),
+                    help="run one measurement alone and print its JSON (for profiling that "
+                         "workload by itself; 'headline' is the timed sweep without the "
+                         "CPU baseline)")
+    ap.add_argument("--tokens", type=int, default=None,
+                    help="decode tokens per ratio in the headline sweep (default: the "
+                         "workload's 128; fewer only for counter runs, which record per-call "
+                         "figures)")
     ap.add_argument("--pmc-calibration", action="store_true",
                     help="first copy 512 MiB device-to-device twice (a kernel of known "
                          "traffic for scaling hardware byte counters)")
@@ -78,9 +94,10 @@ def _evict_bytes(Hq, Hkv, d, L, w, n_keep, esz=2):
 
 
 def measured_traffic():
-    """HBM bytes per decode launch from the committed counter runs, or None when
-    the decode kernels or their launch plan have changed since the counters were
-    taken (the record holds the sha256 of each source it depends on)."""
+    """HBM bytes per decode call of the headline sweep from the committed counter
+    runs, or None when the decode kernels or their launch plan have changed
+    since the counters were taken (the record holds the sha256 of each source
+    it depends on)."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "decode_traffic.json")
     try:
@@ -92,63 +109,78 @@ def measured_traffic():
                     return None
     except (OSError, KeyError, ValueError, AttributeError):
         return None
-    return rec["traffic_bytes_per_launch"]
+    return rec["traffic_bytes_per_call"]
 
 
-def cpu_baseline(wl, pr, dc, min_seconds):
-    """The float64 oracle on this host: whole passes of the step (eviction and
-    every decode step at each ratio), repeated until min_seconds have passed,
-    with the time of each stage (scores, selection, compaction, decode)."""
+def cpu_baseline(min_seconds):
+    """The float64 oracle on this host, on a bounded sample of the headline
+    workload: whole evictions (window scores, pooling, selection, compaction)
+    of layers 0, 1, ... and decode steps 0, 16, ..., 112, 127 of those layers at
+    ratios spread over the sweep, until min_seconds have passed.  Scaled to the
+    whole sweep: every ratio's eviction of all 28 layers costs the sampled mean
+    eviction, and a decode step is fitted linearly in the retained length from
+    the sampled steps; tokens/s = 20 * 128 tokens / that total."""
     import numpy as np
     from oracle import timebill_oracle as O
+    from paper_2512_21859_amd import synth
     try:
         from threadpoolctl import threadpool_info
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:       # pragma: no cover - reporting only
-        threads = len(os.sched_getaffinity(0))
-    q64 = pr["q_win"][0].double().numpy()
-    k64 = pr["k"][0].double().numpy()
-    v64 = pr["v"][0].double().numpy()
-    qs = dc["q"][:, 0].double().numpy()
-    kn = dc["k_new"][:, 0].double().numpy()
-    vn = dc["v_new"][:, 0].double().numpy()
-    L, w, pool = wl.L, wl.w, wl.pool
-    stage = {"score": 0.0, "select": 0.0, "compact": 0.0, "decode": 0.0}
-    tokens, passes = 0, 0
+        threads = _BLAS_THREADS
+    wl = synth.WORKLOADS[3]
+    L, w, pool, T, nl = wl.L, wl.w, wl.pool, wl.T, wl.layers
+    check = sorted(set(range(0, T, 16)) | {T - 1})
+    sample_alphas = [wl.alphas[i] for i in (0, 10, 19, 5, 15, 2, 17)]
+    evict_s, steps = [], []          # eviction seconds; (retained rows, seconds) per step
     t0 = time.perf_counter()
-    while True:
-        for a in wl.alphas:
+    layers_done, alphas_done = 0, []
+    for layer in range(nl):
+        pr = synth.make_prompt(wl, layer)
+        dc = synth.make_decode(wl, layer)
+        q64, k64, v64 = (pr[x][0].double().numpy() for x in ("q_win", "k", "v"))
+        qs, kn, vn = (dc[x][:, 0].double().numpy() for x in ("q", "k_new", "v_new"))
+        for a in sample_alphas:
             c0 = time.perf_counter()
             pooled = O.max_pool(O.window_scores(q64, k64, L, w), pool)
-            c1 = time.perf_counter()
             nk = O.keep_count(L, a, w)
             keep = [O.select_keep(pooled[g], L, w, nk) for g in range(k64.shape[0])]
-            c2 = time.perf_counter()
             kc = np.stack([O.compact(k64[g], v64[g], keep[g])[0] for g in range(len(keep))])
             vc = np.stack([O.compact(k64[g], v64[g], keep[g])[1] for g in range(len(keep))])
-            c3 = time.perf_counter()
-            O.decode_sequence(qs, kn, vn, kc, vc)
-            c4 = time.perf_counter()
-            stage["score"] += c1 - c0
-            stage["select"] += c2 - c1
-            stage["compact"] += c3 - c2
-            stage["decode"] += c4 - c3
-            tokens += wl.T
-        passes += 1
-        wall = time.perf_counter() - t0
-        if wall >= min_seconds:
+            evict_s.append(time.perf_counter() - c0)
+            alphas_done.append(a)
+            for t in check:
+                c1 = time.perf_counter()
+                O.decode_sequence(qs, kn, vn, kc, vc, steps=[t])
+                steps.append((nk + t + 1, time.perf_counter() - c1))
+            if time.perf_counter() - t0 >= min_seconds:
+                break
+        layers_done = layer + 1
+        if time.perf_counter() - t0 >= min_seconds:
             break
-    n = passes * len(wl.alphas)
-    return {"value": tokens / wall, "unit": "tokens/s", "cores": int(threads),
-            "kind": "oracle",
-            "stage_ms": {"score_per_eviction": round(stage["score"] / n * 1e3, 2),
-                         "select_per_eviction": round(stage["select"] / n * 1e3, 2),
-                         "compact_per_eviction": round(stage["compact"] / n * 1e3, 2),
-                         "decode_per_step": round(stage["decode"] / (n * wl.T) * 1e3, 3)},
-            "sample": (f"float64 numpy oracle on the host: {passes} whole pass(es) of the step "
-                       f"(eviction plus all {wl.T} decode steps at each of the "
-                       f"{len(wl.alphas)} ratios), {wall:.1f} s of CPU work; stage times "
-                       f"averaged over the {n} evictions")}
+    wall = time.perf_counter() - t0
+    x = np.array([n for n, _ in steps], dtype=np.float64)
+    y = np.array([s for _, s in steps], dtype=np.float64)
+    slope, icpt = np.polyfit(x, y, 1) if np.ptp(x) > 0 else (0.0, float(y.mean()))
+    ev_mean = float(np.mean(evict_s))
+    total = 0.0
+    for a in wl.alphas:
+        nk = O.keep_count(L, a, w)
+        total += nl * ev_mean + nl * sum(slope * (nk + t + 1) + icpt for t in range(T))
+    tokens = len(wl.alphas) * T
+    return {"value": tokens / total, "unit": "tokens/s", "cores": int(threads),
+            "host_cpus": _HOST_CPUS, "blas_threads": _BLAS_THREADS, "kind": "oracle",
+            "stage_ms": {"eviction_per_layer": round(ev_mean * 1e3, 1),
+                         "decode_step_per_layer_at_32768_rows": round(
+                             (slope * 32768 + icpt) * 1e3, 2)},
+            "sample": (f"float64 numpy oracle on the host, {wall:.1f} s of CPU work: "
+                       f"{len(evict_s)} whole evictions of one layer (window scores, "
+                       f"pooling, selection, compaction) over {layers_done} layer(s) at "
+                       f"ratios {sorted(set(alphas_done))}, and "
+                       f"{len(steps)} single decode steps (steps {check} of each); scaled to "
+                       f"the whole sweep (20 ratios x 28 layers x 128 tokens) with the mean "
+                       f"eviction and a least-squares line of step time against retained "
+                       f"length")}
 
 
 def long_context(torch, _lib, synth, Evictor, dev, steps=64, alpha=0.5):
@@ -406,16 +438,20 @@ def prefill_sweep(torch, _lib, synth, dev, lengths=(1024, 2048, 4096, 8192, 1638
             "timing": "best of 3 replays of a graph of repeated calls (2..20 by length)"}
 
 
-def layer_sweep(torch, _lib, synth, Evictor, dev, T=None):
-    """Supplementary: the 28-layer model shape at L = 32768 (28 q / 4 kv heads,
-    d = 128, w = 32, pool 7) over the ratios k/20, k = 0..19.  Per ratio: evict
-    every layer, then decode T tokens, one token being the decode step of all
-    28 layers in order, replayed from a graph.  The per-token time is fitted
-    against the retained length with the execution-time model's decode-step
-    form t = p N_kv + q (least squares, computed by tb_ete_fit)."""
+def _pct(xs, q):
+    xs = sorted(xs)
+    return xs[min(len(xs) - 1, int(q * (len(xs) - 1) + 0.5))]
+
+
+LLC_BYTES = 256 << 20      # MI355X last-level (Infinity) cache
+
+
+def headline(torch, _lib, synth, Evictor, dev, steps, warmup, tokens=None):
+    """The 28-layer L = 32768 sweep (module docstring).  Returns the headline
+    fields of the JSON line."""
     wl = synth.WORKLOADS[3]
-    T = wl.T if T is None else T
-    B, Hq, Hkv, d, w, L, nl = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L, wl.layers
+    T, nl = (wl.T if tokens is None else tokens), wl.layers
+    B, Hq, Hkv, d, w, L = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L
     lay = []
     for layer in range(nl):
         pr = synth.make_prompt(wl, layer)
@@ -425,81 +461,235 @@ def layer_sweep(torch, _lib, synth, Evictor, dev, T=None):
         del pr, dc
     ev = Evictor(B, L, Hq, Hkv, d, w, wl.pool, device=dev)
     stream = torch.cuda.current_stream()
-    cs = torch.cuda.Stream()
-    rows = []
-    for a in wl.alphas:
-        nk = _lib.tb_keep_count(L, a, w)
-        caches = [_lib.KVCache(B, Hq, Hkv, nk + T, d, wl.dtype, device=dev) for _ in range(nl)]
-        out = torch.empty((T, nl, B, Hq, d), dtype=wl.dtype, device=dev)
+    alphas = list(wl.alphas)
+    n_keep = {a: _lib.tb_keep_count(L, a, w) for a in alphas}
+    caches = {a: [_lib.KVCache(B, Hq, Hkv, n_keep[a] + T, d, wl.dtype, device=dev)
+                  for _ in range(nl)] for a in alphas}
+    out = torch.empty((T, nl, B, Hq, d), dtype=wl.dtype, device=dev)
 
-        def evict_all():
-            for layer in range(nl):
-                x = lay[layer]
-                ev.evict(x["q_win"], x["k"], x["v"], [L], [a], caches[layer], stream)
+    def evict_all(a):
+        for layer in range(nl):
+            x = lay[layer]
+            ev.evict(x["q_win"], x["k"], x["v"], [L], [a], caches[a][layer], stream)
 
-        evict_all()
+    # one graph per ratio: T tokens x 28 layers of decode calls (lengths live on
+    # the device, so every replay after an eviction starts from n_keep)
+    graphs = {}
+    cap_stream = torch.cuda.Stream()
+    for a in alphas:
+        evict_all(a)
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=cs):
+        with torch.cuda.graph(g, stream=cap_stream):
             for t in range(T):
                 for layer in range(nl):
-                    x, c = lay[layer], caches[layer]
+                    x, c = lay[layer], caches[a][layer]
                     _lib.tb_decode_attn(x["q"][t], x["k_new"][t], x["v_new"][t], c.k, c.v,
-                                        c.kv_len, out[t, layer], c.ws, stream=cs)
-        torch.cuda.synchronize()
-        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
-        ev_best, de_best = float("inf"), float("inf")
-        for _ in range(2):
-            e0.record(stream)
-            evict_all()
-            e1.record(stream)
-            g.replay()
-            e2.record(stream)
-            torch.cuda.synchronize()
-            ev_best = min(ev_best, e0.elapsed_time(e1))
-            de_best = min(de_best, e1.elapsed_time(e2))
-        tok_us = de_best * 1e3 / T
-        dbytes = nl * sum(_decode_bytes(Hq, Hkv, d, nk + t + 1) for t in range(T)) / T
-        rows.append({"alpha": a, "n_keep": nk,
-                     "us_per_token": round(tok_us, 2),
-                     "tokens_per_s": round(1e6 / tok_us, 1),
-                     "decode_GBps": round(dbytes / (tok_us * 1e-6) / 1e9, 1),
-                     "evict_all_layers_us": round(ev_best * 1e3, 1)})
-        del g, caches, out
-        torch.cuda.empty_cache()
+                                        c.kv_len, out[t, layer], c.ws, stream=cap_stream)
+        graphs[a] = g
+    torch.cuda.synchronize()
+
+    def step(evs=None):
+        for i, a in enumerate(alphas):
+            if evs is not None:
+                evs[3 * i].record(stream)
+            evict_all(a)
+            if evs is not None:
+                evs[3 * i + 1].record(stream)
+            graphs[a].replay()
+            if evs is not None:
+                evs[3 * i + 2].record(stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    n_al = len(alphas)
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3 * n_al)]
+              for _ in range(steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for s_ in range(steps):
+        step(events[s_])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_end)
+
+    rows = []
+    hbm_bytes = hbm_ms = hbm_calls = 0.0
+    all_bytes = all_ms = 0.0
+    for i, a in enumerate(alphas):
+        ev_ms = [events[k][3 * i].elapsed_time(events[k][3 * i + 1]) for k in range(steps)]
+        de_ms = [events[k][3 * i + 1].elapsed_time(events[k][3 * i + 2]) for k in range(steps)]
+        e_med, d_med = _pct(ev_ms, 0.5), _pct(de_ms, 0.5)
+        nk = n_keep[a]
+        tok_bytes = nl * sum(_decode_bytes(Hq, Hkv, d, nk + t + 1) for t in range(T)) / T
+        tok_us = d_med * 1e3 / T
+        streams_hbm = tok_bytes > LLC_BYTES
+        rows.append({
+            "alpha": a, "n_keep": nk,
+            "evict_all_layers_us": round(e_med * 1e3, 1),
+            "us_per_token": round(tok_us, 2),
+            "us_per_token_p10_p90": [round(_pct(de_ms, 0.1) * 1e3 / T, 2),
+                                     round(_pct(de_ms, 0.9) * 1e3 / T, 2)],
+            "tokens_per_s": round(T / ((d_med + e_med) * 1e-3), 1),
+            "decode_tokens_per_s": round(1e6 / tok_us, 1),
+            "decode_bytes_per_token": round(tok_bytes),
+            "decode_GBps": round(tok_bytes / (tok_us * 1e-6) / 1e9, 1),
+            "decode_frac_of_8TBps": round(tok_bytes / (tok_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "working_set": "hbm" if streams_hbm else "fits the 256 MB last-level cache (warm)",
+        })
+        all_bytes += tok_bytes * T * steps
+        all_ms += sum(de_ms)
+        if streams_hbm:
+            hbm_bytes += tok_bytes * T * steps
+            hbm_ms += sum(de_ms)
+            hbm_calls += T * nl * steps
     # eviction stages of one layer at ratio 0.5 (scores do not depend on the ratio)
     a = 0.5
-    nk = _lib.tb_keep_count(L, a, w)
-    cache = _lib.KVCache(B, Hq, Hkv, nk, d, wl.dtype, device=dev)
-    x = lay[0]
+    nk = n_keep[a]
+    x, c = lay[0], caches[a][0]
     sc_t = _best_ms(torch, lambda: ev.score(x["q_win"], x["k"], [L], stream))
     se_t = _best_ms(torch, lambda: ev.select([L], [a], stream))
-    co_t = _best_ms(torch, lambda: cache.compact_from(x["k"], x["v"], ev.keep_idx, [nk], stream))
+    co_t = _best_ms(torch, lambda: c.compact_from(x["k"], x["v"], ev.keep_idx, [nk], stream))
     cbytes = 2 * 2 * Hkv * nk * d * 2
     stages = {"alpha": a, "score_us": round(sc_t * 1e3, 1), "select_us": round(se_t * 1e3, 1),
               "compact_us": round(co_t * 1e3, 1),
+              "compaction_bytes": cbytes,
               "compact_GBps": round(cbytes / (co_t * 1e-3) / 1e9, 1),
+              "compact_frac_of_8TBps": round(cbytes / (co_t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
               "score_window_flops": 2 * Hq * w * L * d,
-              "score_fp64_TFLOPs": round(2 * Hq * w * L * d / (sc_t * 1e-3) / 1e12, 2)}
-    del cache
+              "score_fp64_TFLOPs": round(2 * Hq * w * L * d / (sc_t * 1e-3) / 1e12, 2),
+              "timing": "best of 3, HIP events around one call"}
     xs = [r["n_keep"] + (T + 1) / 2 for r in rows]
     ys = [r["us_per_token"] for r in rows]
     p, q = _lib.tb_ete_fit(xs, ys, 1)
-    pred = [p * x + q for x in xs]
+    pred = [p * xx + q for xx in xs]
     my = sum(ys) / len(ys)
     ss_res = sum((y - f) ** 2 for y, f in zip(ys, pred))
     ss_tot = sum((y - my) ** 2 for y in ys)
-    del lay, ev
+    tokens = n_al * T * steps
+    calls = hbm_calls
+    achieved = hbm_bytes / (hbm_ms * 1e-3) / 1e9
+    del graphs, caches, lay, ev, out
     torch.cuda.empty_cache()
-    return {"workload": f"bf16, B=1, {nl} layers, L={L}, 28 q / 4 kv heads, d=128, w=32, "
-                        f"pool 7, ratios k/20 (k = 0..19), {T} decode tokens per ratio",
-            "per_alpha": rows,
-            "evict_one_layer": stages,
-            "token_time_fit": {"p_us_per_kv_row": p, "q_us": q,
-                               "r2": 1 - ss_res / ss_tot if ss_tot > 0 else 1.0,
-                               "mape_pct": 100.0 * sum(abs(f - y) / y for y, f in zip(ys, pred)) / len(ys)},
-            "timing": "best of 2: HIP events around the 28 evictions and around a graph of "
-                      f"{T} x {nl} decode launches"}
+    return {
+        "value": round(tokens / (total_ms * 1e-3), 1),
+        "ms_per_step": round(total_ms / steps, 3),
+        "wall_s": round(wall, 3),
+        "config": {
+            "workload": f"{nl}-layer stack bf16 (28 q / 4 kv heads, d=128), B=1, prompt "
+                        f"L={L}, w={w}, pool {wl.pool}, ratios alpha=k/20 (k=0..19), {T} "
+                        f"decode tokens per ratio; one step = every ratio's eviction of all "
+                        f"{nl} layers plus its {T} tokens",
+            "B": B, "L": L, "layers": nl, "Hq": Hq, "Hkv": Hkv, "d": d, "w": w,
+            "pool": wl.pool, "alphas": alphas, "decode_tokens_per_alpha": T,
+            "parallelism": "none (1 GPU)",
+        },
+        "roofline": {
+            "kernel": "tb_decode_attn: decode_mfma_kernel (split-K partials) + "
+                      "decode_merge_kernel / decode_merge_wave_kernel, one call per layer "
+                      "and token",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": measured_traffic(),
+            "traffic_note": "HBM bytes per decode call (FETCH_SIZE and WRITE_SIZE scaled by a "
+                            "512 MiB copy, profiles/pmc_decode_28layer_L32768.md); null if the "
+                            "decode kernels or their launch plan changed since",
+            "avg_call_us": round(hbm_ms * 1e3 / calls, 3),
+            "bytes_per_call": round(hbm_bytes / calls),
+            "ratios": "alpha <= 0.85 (per-token working set above the 256 MB last-level "
+                      "cache, streamed from HBM)",
+            "all_ratios_GBps": round(all_bytes / (all_ms * 1e-3) / 1e9, 1),
+            "timing": "HIP events on the replay stream around each ratio's graph of "
+                      f"{T} x {nl} decode calls, divided by the call count (the gap between "
+                      "the two kernels of a call included)",
+        },
+        "per_alpha": rows,
+        "per_alpha_timing": "median over the timed steps (p10, p90 beside it) of HIP events "
+                            "around each ratio's 28 evictions and its graph of decode calls",
+        "evict_one_layer": stages,
+        "token_time_fit": {"p_us_per_kv_row": p, "q_us": q,
+                           "r2": 1 - ss_res / ss_tot if ss_tot > 0 else 1.0,
+                           "mape_pct": 100.0 * sum(abs(f - y) / y for y, f in zip(ys, pred)) / len(ys),
+                           "note": "least squares of the per-token time (28 layer calls) against "
+                                   "the mean retained length over the 20 ratios (tb_ete_fit): "
+                                   "the decode-step form t = p N_kv + q of the execution-time "
+                                   "model"},
+    }
+
+
+def single_layer(torch, _lib, synth, Evictor, dev, reps=10, cold=True):
+    """Supplementary: one bf16 layer with a prompt of L = 8192 tokens (28 q / 4
+    kv heads, d = 128, w = 32, pool 7) at the ratios 0 (no eviction) and the
+    paper's fixed-ratio arms 0.25 / 0.5 / 0.75 / 0.95, 256 decode steps each;
+    reps passes of (eviction + a graph of the 256 steps) per ratio, medians.
+    Its 17 MB cache sits in the last-level cache; the cold run rotates the
+    ratio-0 step over >= 1 GiB of caches."""
+    wl = synth.WORKLOADS[2]
+    B, Hq, Hkv, d, w, L, T = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L, wl.T
+    pr = synth.make_prompt(wl)
+    dc = synth.make_decode(wl)
+    q_win, k, v = (pr[x].to(dev) for x in ("q_win", "k", "v"))
+    qd, knd, vnd = (dc[x].to(dev) for x in ("q", "k_new", "v_new"))
+    del pr, dc
+    ev = Evictor(B, L, Hq, Hkv, d, w, wl.pool, device=dev)
+    stream = torch.cuda.current_stream()
+    rows = []
+    cap_stream = torch.cuda.Stream()
+    for a in wl.alphas:
+        nk = _lib.tb_keep_count(L, a, w)
+        cache = _lib.KVCache(B, Hq, Hkv, nk + T, d, wl.dtype, device=dev)
+        out = torch.empty((T, B, Hq, d), dtype=wl.dtype, device=dev)
+        ev.evict(q_win, k, v, [L], [a], cache, stream)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cap_stream):
+            for t in range(T):
+                _lib.tb_decode_attn(qd[t], knd[t], vnd[t], cache.k, cache.v, cache.kv_len,
+                                    out[t], cache.ws, stream=cap_stream)
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev_ms, de_ms = [], []
+        for r in range(reps + 1):
+            e[0].record(stream)
+            ev.evict(q_win, k, v, [L], [a], cache, stream)
+            e[1].record(stream)
+            g.replay()
+            e[2].record(stream)
+            torch.cuda.synchronize()
+            if r:
+                ev_ms.append(e[0].elapsed_time(e[1]))
+                de_ms.append(e[1].elapsed_time(e[2]))
+        e_med, d_med = _pct(ev_ms, 0.5), _pct(de_ms, 0.5)
+        dbytes = sum(_decode_bytes(Hq, Hkv, d, nk + t + 1) for t in range(T))
+        rows.append({"alpha": a, "n_keep": nk, "evict_us": round(e_med * 1e3, 2),
+                     "decode_us_per_step": round(d_med * 1e3 / T, 3),
+                     "decode_us_per_step_p10_p90": [round(_pct(de_ms, 0.1) * 1e3 / T, 3),
+                                                    round(_pct(de_ms, 0.9) * 1e3 / T, 3)],
+                     "decode_GBps": round(dbytes / (d_med * 1e-3) / 1e9, 1),
+                     "tokens_per_s": round(T / ((d_med + e_med) * 1e-3), 1)})
+        del g, cache, out
+    xs = [r["n_keep"] + (T + 1) / 2 for r in rows]
+    ys = [r["decode_us_per_step"] for r in rows]
+    slope, icpt = _lib.tb_ete_fit(xs, ys, 1)
+    res = {"workload": f"bf16, B=1, L={L}, 28 q / 4 kv heads, d=128, w=32, pool 7, ratios "
+                       f"{list(wl.alphas)}, {T} decode steps each (cache in the last-level cache)",
+           "per_alpha": rows,
+           "decode_time_fit": {"p_us_per_kv_row": slope, "q_us": icpt},
+           "timing": f"median of {reps} passes: HIP events around the eviction and around a "
+                     f"graph of the {T} decode steps"}
+    if cold:
+        res["cold_decode"] = cold_decode(torch, _lib, Evictor, dev, wl, q_win, k, v, qd, knd, vnd)
+    del q_win, k, v, qd, knd, vnd, ev
+    torch.cuda.empty_cache()
+    return res
 
 
 def paged_serving(torch, _lib, synth, Evictor, dev, T=64, n_req=64, max_seqs=16,
@@ -757,190 +947,52 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    if args.only in ("long", "layers", "ceiling", "scorers", "prefill", "paged"):
-        fn = {"long": lambda: long_context(torch, _lib, synth, Evictor, dev),
-              "layers": lambda: layer_sweep(torch, _lib, synth, Evictor, dev),
-              "ceiling": lambda: hbm_ceiling(torch, dev),
-              "scorers": lambda: scorer_variants(torch, _lib, synth, Evictor, dev),
-              "prefill": lambda: prefill_sweep(torch, _lib, synth, dev),
-              "paged": lambda: paged_serving(torch, _lib, synth, Evictor, dev)}[args.only]
-        print(json.dumps({"section": args.only, **fn()}), flush=True)
+    sections = {
+        "single": lambda: single_layer(torch, _lib, synth, Evictor, dev),
+        "long": lambda: long_context(torch, _lib, synth, Evictor, dev),
+        "ceiling": lambda: hbm_ceiling(torch, dev),
+        "scorers": lambda: scorer_variants(torch, _lib, synth, Evictor, dev),
+        "prefill": lambda: prefill_sweep(torch, _lib, synth, dev),
+        "paged": lambda: paged_serving(torch, _lib, synth, Evictor, dev),
+    }
+    if args.only and args.only != "headline":
+        print(json.dumps({"section": args.only, **sections[args.only]()}), flush=True)
         return
-    wl = synth.WORKLOADS[2]
-    B, Hq, Hkv, d, w, L, T = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L, wl.T
-    pr = synth.make_prompt(wl)
-    dc = synth.make_decode(wl)
-    q_win, k, v = (pr[x].to(dev) for x in ("q_win", "k", "v"))
-    qd, knd, vnd = (dc[x].to(dev) for x in ("q", "k_new", "v_new"))
 
-    if args.only == "cold":
-        print(json.dumps({"section": "cold", **cold_decode(torch, _lib, Evictor, dev, wl, q_win,
-                                                            k, v, qd, knd, vnd)}), flush=True)
-        return
-    ev = Evictor(B, L, Hq, Hkv, d, w, wl.pool, device=dev)
-    stream = torch.cuda.current_stream()
-    n_keep = {a: _lib.tb_keep_count(L, a, w) for a in wl.alphas}
-    caches = {a: _lib.KVCache(B, Hq, Hkv, n_keep[a] + T, d, wl.dtype, device=dev)
-              for a in wl.alphas}
-    outs = {a: torch.empty((T, B, Hq, d), dtype=wl.dtype, device=dev) for a in wl.alphas}
-
-    def evict(a):
-        ev.evict(q_win, k, v, [L], [a], caches[a], stream)
-
-    # One graph per ratio with the T decode launches (lengths live on the device).
-    graphs = {}
-    cap_stream = torch.cuda.Stream()
-    for a in wl.alphas:
-        evict(a)
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        c = caches[a]
-        with torch.cuda.graph(g, stream=cap_stream):
-            for t in range(T):
-                _lib.tb_decode_attn(qd[t], knd[t], vnd[t], c.k, c.v, c.kv_len, outs[a][t],
-                                    c.ws, stream=cap_stream)
-        graphs[a] = g
-    torch.cuda.synchronize()
-
-    n_al = len(wl.alphas)
-
-    def step(evs=None):
-        for i, a in enumerate(wl.alphas):
-            if evs is not None:
-                evs[3 * i].record(stream)
-            evict(a)
-            if evs is not None:
-                evs[3 * i + 1].record(stream)
-            graphs[a].replay()
-            if evs is not None:
-                evs[3 * i + 2].record(stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3 * n_al)]
-              for _ in range(args.steps)]
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    t_start.record(stream)
-    for s in range(args.steps):
-        step(events[s])
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    total_ms = t_start.elapsed_time(t_end)
-
-    per_alpha = []
-    dec_bytes_total, dec_ms_total, launches = 0.0, 0.0, 0
-    for i, a in enumerate(wl.alphas):
-        ev_ms = [events[s][3 * i].elapsed_time(events[s][3 * i + 1]) for s in range(args.steps)]
-        de_ms = [events[s][3 * i + 1].elapsed_time(events[s][3 * i + 2]) for s in range(args.steps)]
-        ev_ms.sort()
-        de_ms.sort()
-        e_med, d_med = ev_ms[len(ev_ms) // 2], de_ms[len(de_ms) // 2]
-
-        def pct(xs, q):
-            return xs[min(len(xs) - 1, int(q * (len(xs) - 1) + 0.5))]
-        nk = n_keep[a]
-        dbytes = sum(_decode_bytes(Hq, Hkv, d, nk + t + 1) for t in range(T))
-        ebytes = _evict_bytes(Hq, Hkv, d, L, w, nk)
-        dec_bytes_total += dbytes * args.steps
-        dec_ms_total += sum(de_ms)
-        launches += T * args.steps
-        per_alpha.append({
-            "alpha": a, "n_keep": nk,
-            "evict_us": round(e_med * 1e3, 2),
-            "evict_us_p10_p90": [round(pct(ev_ms, 0.1) * 1e3, 2), round(pct(ev_ms, 0.9) * 1e3, 2)],
-            "decode_us_per_token": round(d_med * 1e3 / T, 3),
-            "decode_us_per_token_p10_p90": [round(pct(de_ms, 0.1) * 1e3 / T, 3),
-                                            round(pct(de_ms, 0.9) * 1e3 / T, 3)],
-            "decode_GBps": round(dbytes / (d_med * 1e-3) / 1e9, 1),
-            "evict_plus_decode_GBps": round((dbytes + ebytes) / ((d_med + e_med) * 1e-3) / 1e9, 1),
-            "tokens_per_s": round(T / ((d_med + e_med) * 1e-3), 1),
-        })
-    # decode time per step against retained length: least-squares line t = p N_kv + q
-    # (the execution-time model's decode-step form), fitted by the library
-    xs = [p["n_keep"] + (T + 1) / 2 for p in per_alpha]
-    ys = [p["decode_us_per_token"] for p in per_alpha]
-    slope, icpt = _lib.tb_ete_fit(xs, ys, 1)
-    pred = [slope * x + icpt for x in xs]
-    my = sum(ys) / len(ys)
-    ss_res = sum((y - f) ** 2 for y, f in zip(ys, pred))
-    ss_tot = sum((y - my) ** 2 for y in ys)
-    mape = 100.0 * sum(abs(f - y) / y for y, f in zip(ys, pred)) / len(ys)
-
-    tokens = n_al * T * args.steps
-    value = tokens / (total_ms * 1e-3)
-    avg_launch_us = dec_ms_total * 1e3 / launches
-    achieved = dec_bytes_total / (dec_ms_total * 1e-3) / 1e9
+    head = headline(torch, _lib, synth, Evictor, dev, args.steps, args.warmup, args.tokens)
     result = {
         "metric": "decode tokens/s and HBM GB/s (evict+decode attn) vs eviction ratio α, 1 GPU",
-        "value": round(value, 1),
+        "value": head.pop("value"),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(total_ms / args.steps, 4),
+        "ms_per_step": head.pop("ms_per_step"),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic",
-        "config": {
-            "workload": "single layer bf16, B=1, L=8192, 28 q / 4 kv heads, d=128, w=32, "
-                        "pool 7, alpha sweep 0/0.25/0.5/0.75/0.95, 256 decode steps each",
-            "B": B, "L": L, "Hq": Hq, "Hkv": Hkv, "d": d, "w": w, "pool": wl.pool,
-            "alphas": list(wl.alphas), "decode_steps": T,
-            "parallelism": "none (1 GPU)",
-        },
-        "roofline": {
-            "kernel": "decode_kernel (split-K GQA decode attention with append)",
-            "bound": "hbm",
-            "achieved": round(achieved, 1),
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic(),
-            "traffic_note": "HBM bytes per decode launch (FETCH_SIZE x2 + WRITE_SIZE, scaled "
-                            "by a 512 MiB copy; profiles/pmc_bf16_L8192_sweep.md); null if "
-                            "the decode kernels or their launch plan changed since",
-            "avg_launch_us": round(avg_launch_us, 3),
-            "bytes_per_launch": round(dec_bytes_total / launches),
-            "timing": "HIP events around each ratio's graph of decode launches, "
-                      "divided by the launch count (inter-kernel gaps included)",
-        },
-        "per_alpha": per_alpha,
-        "per_alpha_timing": "median over the timed steps (p10, p90 beside it) of HIP events "
-                            "around each ratio's eviction and its graph of decode launches",
-        "decode_time_fit": {"p_us_per_kv_row": slope, "q_us": icpt,
-                            "r2": 1 - ss_res / ss_tot if ss_tot > 0 else 1.0,
-                            "mape_pct": mape,
-                            "note": "least squares of per-step decode time vs mean retained "
-                                    "length over the ratio sweep (tb_ete_fit)"},
-        "wall_s": round(wall, 3),
+        "data": "synthetic (seeded N(0,1) K/V/queries with planted heavy-hitter keys; "
+                "random-init stand-in for LongBench on Qwen2.5-7B)",
+        **head,
     }
-    if not args.no_cold:
-        result["cold_decode"] = cold_decode(torch, _lib, Evictor, dev, wl, q_win, k, v,
-                                            qd, knd, vnd)
-    del caches, graphs, outs
-    torch.cuda.empty_cache()
+    if args.only == "headline":
+        print(json.dumps(result), flush=True)
+        return
+    if not args.no_single:
+        result["single_layer"] = sections["single"]()
     if not args.no_long_context:
-        result["long_context"] = long_context(torch, _lib, synth, Evictor, dev)
+        result["long_context"] = sections["long"]()
     if not args.no_prefill:
-        result["prefill"] = prefill_sweep(torch, _lib, synth, dev)
+        result["prefill"] = sections["prefill"]()
     if not args.no_paged:
-        result["paged"] = paged_serving(torch, _lib, synth, Evictor, dev)
+        result["paged"] = sections["paged"]()
     if not args.no_scorers:
-        result["scorers"] = scorer_variants(torch, _lib, synth, Evictor, dev)
-    if not args.no_layer_sweep:
-        result["layer_sweep"] = layer_sweep(torch, _lib, synth, Evictor, dev)
+        result["scorers"] = sections["scorers"]()
     if not args.no_ceiling:
-        result["hbm_ceiling"] = hbm_ceiling(torch, dev)
+        result["hbm_ceiling"] = sections["ceiling"]()
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, pr, dc, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(result), flush=True)
 
 
