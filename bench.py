@@ -67,7 +67,7 @@ def _parse():
     ap.add_argument("--no-paged", action="store_true",
                     help="skip the paged-cache batch and serving-stream measurements")
     ap.add_argument("--only", choices=("headline", "single", "long", "ceiling", "scorers",
-                                       "prefill", "paged"),
+                                       "prefill", "paged", "counters"),
                     help="run one measurement alone and print its JSON (for profiling that "
                          "workload by itself; 'headline' is the timed sweep without the "
                          "CPU baseline)")
@@ -600,7 +600,7 @@ def headline(torch, _lib, synth, Evictor, dev, steps, warmup, tokens=None):
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": measured_traffic(),
             "traffic_note": "HBM bytes per decode call (FETCH_SIZE and WRITE_SIZE scaled by a "
-                            "512 MiB copy, profiles/pmc_decode_28layer_L32768.md); null if the "
+                            "512 MiB copy, profiles/pmc_decode_compact_28layer_L32768.md); null if the "
                             "decode kernels or their launch plan changed since",
             "avg_call_us": round(hbm_ms * 1e3 / calls, 3),
             "bytes_per_call": round(hbm_bytes / calls),
@@ -623,6 +623,52 @@ def headline(torch, _lib, synth, Evictor, dev, steps, warmup, tokens=None):
                                    "the decode-step form t = p N_kv + q of the execution-time "
                                    "model"},
     }
+
+
+def counter_sweep(torch, _lib, synth, dev, tokens=8):
+    """For HBM counter runs: the headline's compaction and decode calls at the
+    ratios whose working set streams from HBM (alpha <= 0.85, the roofline's
+    ratios) and at the headline's shapes and launch plans, launched one by one
+    (no graph, no scoring).  Per ratio: every layer's cache is compacted from a
+    fixed kept set (the first n_keep - w prefix positions and the window), then
+    `tokens` decode tokens of all 28 layers.  Kernel traffic does not depend on
+    which rows are kept.  Returns the dispatch order for attributing counters."""
+    wl = synth.WORKLOADS[3]
+    nl, B, Hq, Hkv, d, w, L = wl.layers, wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L
+    alphas = [a for a in wl.alphas
+              if nl * _decode_bytes(Hq, Hkv, d, _lib.tb_keep_count(L, a, w) + 1) > LLC_BYTES]
+    lay = []
+    for layer in range(nl):
+        pr = synth.make_prompt(wl, layer)
+        dc = synth.make_decode(wl, layer, T=tokens)
+        lay.append({x: pr[x].to(dev) for x in ("k", "v")})
+        lay[-1].update({x: dc[x].to(dev) for x in ("q", "k_new", "v_new")})
+        del pr, dc
+    stream = torch.cuda.current_stream()
+    order = []
+    for a in alphas:
+        nk = _lib.tb_keep_count(L, a, w)
+        keep = torch.cat([torch.arange(nk - w), torch.arange(L - w, L)]).to(torch.int32)
+        keep_idx = torch.zeros((B, Hkv, L), dtype=torch.int32)
+        keep_idx[:, :, :nk] = keep
+        keep_idx = keep_idx.to(dev)
+        caches = [_lib.KVCache(B, Hq, Hkv, nk + wl.T, d, wl.dtype, device=dev) for _ in range(nl)]
+        for layer in range(nl):
+            caches[layer].compact_from(lay[layer]["k"], lay[layer]["v"], keep_idx, [nk], stream)
+        out = torch.empty((B, Hq, d), dtype=wl.dtype, device=dev)
+        for t in range(tokens):
+            for layer in range(nl):
+                x, c = lay[layer], caches[layer]
+                _lib.tb_decode_attn(x["q"][t], x["k_new"][t], x["v_new"][t], c.k, c.v,
+                                    c.kv_len, out, c.ws, stream=stream)
+        torch.cuda.synchronize()
+        order.append({"alpha": a, "n_keep": nk, "compactions": nl, "decode_calls": tokens * nl})
+        del caches, keep_idx, out
+    del lay
+    torch.cuda.empty_cache()
+    return {"workload": f"{nl}-layer L={L} shapes, ratios {alphas}: per ratio {nl} "
+                        f"compactions then {tokens} x {nl} decode calls, eager",
+            "tokens": tokens, "order": order}
 
 
 def single_layer(torch, _lib, synth, Evictor, dev, reps=10, cold=True):
@@ -954,6 +1000,7 @@ def main():
         "scorers": lambda: scorer_variants(torch, _lib, synth, Evictor, dev),
         "prefill": lambda: prefill_sweep(torch, _lib, synth, dev),
         "paged": lambda: paged_serving(torch, _lib, synth, Evictor, dev),
+        "counters": lambda: counter_sweep(torch, _lib, synth, dev),
     }
     if args.only and args.only != "headline":
         print(json.dumps({"section": args.only, **sections[args.only]()}), flush=True)
