@@ -297,6 +297,49 @@ def hbm_ceiling(torch, dev, nbytes=2 << 30):
                    "torch copy_ (read + write) over 2 GiB buffers, HIP events, best of 5"}
 
 
+FP64_PEAK_TFLOPS = 78.6
+
+
+def mfma_ceiling(torch, dev):
+    """Practical matrix-core rates, best of 5 over grids of 1-8 blocks of 4
+    waves per CU: the benchmark's probe kernel (libtbbench.so) runs eight
+    independent accumulation chains per wave on register operands for the
+    float64 16x16x4 shape (the window scorer's products) and the bf16
+    16x16x32 shape (the prefill's and decode's products)."""
+    import ctypes
+    probe = ctypes.CDLL(os.path.join(ROOT, "paper_2512_21859_amd", "libtbbench.so"))
+    probe.tbb_mfma_peak.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                    ctypes.c_void_p]
+    probe.tbb_mfma_peak.restype = ctypes.c_int
+    stream = torch.cuda.current_stream()
+    out = {}
+    # (kind, flops per instruction, iterations: about 1-2 ms at the datasheet peak
+    # on the largest grid)
+    for name, kind, flops, iters, peak in (("fp64_16x16x4", 0, 16 * 16 * 4 * 2, 1200,
+                                            FP64_PEAK_TFLOPS),
+                                           ("bf16_16x16x32", 1, 16 * 16 * 32 * 2, 4000,
+                                            BF16_PEAK_TFLOPS)):
+        best_rate, best_blocks = 0.0, 0
+        for per_cu in (1, 2, 4, 8):
+            blocks = 256 * per_cu
+            sink = torch.empty((blocks * 256,), dtype=torch.float64, device=dev)
+
+            def run():
+                if probe.tbb_mfma_peak(kind, blocks, iters, sink.data_ptr(), stream.cuda_stream) != 0:
+                    raise RuntimeError("matrix-core probe failed")
+            run()
+            t = _best_ms(torch, run, reps=5)
+            rate = blocks * 4 * iters * 8 * flops / (t * 1e-3) / 1e12
+            if rate > best_rate:
+                best_rate, best_blocks = rate, blocks
+            del sink
+        out[name] = {"TFLOPs": round(best_rate, 1), "blocks": best_blocks,
+                     "frac_of_datasheet": round(best_rate / peak, 4)}
+    out["how"] = ("probe kernel: 8 independent accumulation chains per wave on register "
+                  "operands, 256 threads per block, best grid and best of 5 (HIP events)")
+    return out
+
+
 def cold_decode(torch, _lib, Evictor, dev, wl, q_win, k, v, qd, knd, vnd,
                 target_bytes=1 << 30):
     """Decode at ratio 0 for the L = 8192 workload with the step's cache
@@ -479,6 +522,8 @@ def headline(torch, _lib, synth, Evictor, dev, steps, warmup, tokens=None):
     out = torch.empty((T, nl, B, Hq, d), dtype=wl.dtype, device=dev)
 
     def evict_all(a):
+        # one stream for everything: spreading the layers' evictions over side
+        # streams measured slower (every later decode dispatch slowed down)
         for layer in range(nl):
             x = lay[layer]
             ev.evict(x["q_win"], x["k"], x["v"], [L], [a], caches[a][layer], stream)
@@ -1007,7 +1052,7 @@ def main():
     sections = {
         "single": lambda: single_layer(torch, _lib, synth, Evictor, dev),
         "long": lambda: long_context(torch, _lib, synth, Evictor, dev),
-        "ceiling": lambda: hbm_ceiling(torch, dev),
+        "ceiling": lambda: {"hbm": hbm_ceiling(torch, dev), "mfma": mfma_ceiling(torch, dev)},
         "scorers": lambda: scorer_variants(torch, _lib, synth, Evictor, dev),
         "prefill": lambda: prefill_sweep(torch, _lib, synth, dev),
         "paged": lambda: paged_serving(torch, _lib, synth, Evictor, dev),
@@ -1048,7 +1093,9 @@ def main():
     if not args.no_scorers:
         result["scorers"] = sections["scorers"]()
     if not args.no_ceiling:
-        result["hbm_ceiling"] = sections["ceiling"]()
+        ceil = sections["ceiling"]()
+        result["hbm_ceiling"] = ceil["hbm"]
+        result["mfma_ceiling"] = ceil["mfma"]
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(result), flush=True)

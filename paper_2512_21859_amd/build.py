@@ -53,12 +53,14 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}")
-    # the benchmark's bandwidth probe: a separate library, not part of the ABI
-    bsrc = os.path.join(HERE, "bench_csrc", "stream_read.hip")
-    bobj = os.path.join(BUILD, "stream_read.o")
-    _run([HIPCC, *COMMON_FLAGS, "-c", bsrc, "-o", bobj])
+    # the benchmark's ceiling probes (HBM read, matrix cores): a separate
+    # library, not part of the ABI
+    bsrcs = sorted(glob.glob(os.path.join(HERE, "bench_csrc", "*.hip")))
+    bobjs = [os.path.join(BUILD, "bench_" + os.path.basename(s)[:-4] + ".o") for s in bsrcs]
+    for s, o in zip(bsrcs, bobjs):
+        _run([HIPCC, *COMMON_FLAGS, "-c", s, "-o", o])
     tmp = BENCH_LIB + ".tmp"
-    _run([HIPCC, "-shared", f"--offload-arch={ARCH}", "-o", tmp, bobj])
+    _run([HIPCC, "-shared", f"--offload-arch={ARCH}", "-o", tmp, *bobjs])
     os.replace(tmp, BENCH_LIB)
     if verbose:
         print(f"built {BENCH_LIB}")
