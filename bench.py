@@ -287,6 +287,7 @@ def hbm_ceiling(torch, dev, nbytes=2 << 30):
         t = _best_ms(torch, run, reps=5)
         if t < rd_best:
             rd_best, rd_blocks = t, blocks
+    by_size = read_floor_by_size(torch, probe, x, sink)
     del x, sink
     torch.cuda.empty_cache()
     return {"read_GBps": round(nbytes / (rd_best * 1e-3) / 1e9, 1),
@@ -294,7 +295,44 @@ def hbm_ceiling(torch, dev, nbytes=2 << 30):
             "copy_GBps": round(2 * nbytes / (cp * 1e-3) / 1e9, 1),
             "bytes": nbytes,
             "how": "streaming-read probe kernel (16-byte nontemporal loads, best grid) and "
-                   "torch copy_ (read + write) over 2 GiB buffers, HIP events, best of 5"}
+                   "torch copy_ (read + write) over 2 GiB buffers, HIP events, best of 5",
+            "read_by_size": by_size}
+
+
+def read_floor_by_size(torch, probe, x, sink, sizes_mib=(4, 8, 16, 32, 64, 128, 256)):
+    """The streaming-read probe at the sizes one decode or compaction call
+    moves (64 MiB ~ one layer's K and V at L = 32768), launched back to back
+    from a graph over disjoint windows of the 2 GiB buffer (at least 1 GiB per
+    replay, so the 256 MB last-level cache holds none of it): the time per
+    launch is what a single launch that only streams its bytes costs,
+    dispatch and ramp included.  Best grid of 256 / 512 / 1024 blocks, best
+    of 5 replays."""
+    total = x.numel() * x.element_size()
+    rows = []
+    for mib in sizes_mib:
+        size = mib << 20
+        n = max(16, -(-(1 << 30) // size))
+        if n * size > total:
+            n = total // size
+        best = (float("inf"), 0)
+        for blocks in (256, 512, 1024):
+            cs = torch.cuda.Stream()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=cs):
+                for i in range(n):
+                    if probe.tbb_stream_read(x.data_ptr() + i * size, size, sink.data_ptr(), blocks,
+                                             cs.cuda_stream) != 0:
+                        raise RuntimeError("stream-read probe failed")
+            g.replay()
+            torch.cuda.synchronize()
+            t = _best_ms(torch, g.replay, reps=5) / n
+            if t < best[0]:
+                best = (t, blocks)
+            del g
+        rows.append({"MiB": mib, "us_per_launch": round(best[0] * 1e3, 2), "blocks": best[1],
+                     "GBps": round(size / (best[0] * 1e-3) / 1e9, 1),
+                     "frac_of_8TBps": round(size / (best[0] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)})
+    return rows
 
 
 FP64_PEAK_TFLOPS = 78.6
