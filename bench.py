@@ -876,7 +876,7 @@ def paged_serving(torch, _lib, synth, Evictor, dev, T=64, n_req=64, max_seqs=16,
         table[b] = torch.tensor(pg + [pg[-1]] * (max_pages - need[b]), dtype=torch.int32)
     table = table.to(dev)
     k_pool = torch.zeros((sum(need), Hkv, PAGE, d), dtype=wl.dtype, device=dev)
-    v_pool = torch.zeros((sum(need), Hkv, d, PAGE), dtype=wl.dtype, device=dev)
+    v_pool = torch.zeros((sum(need), Hkv, PAGE, d), dtype=wl.dtype, device=dev)
     len_p = torch.zeros((B,), dtype=torch.int32, device=dev)
     ws_p = torch.zeros_like(cache.ws)
     out_c = torch.empty((T, B, Hq, d), dtype=wl.dtype, device=dev)

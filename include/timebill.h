@@ -35,9 +35,9 @@
  *     scores     [B][Hkv][Lmax]    fp32; entries j >= L[b] - w are left untouched
  *     keep_idx   [B][Hkv][Lmax]    int32; the first n_keep[b] entries are valid
  *     k_cache    [B][Hkv][cap][d]  compact K cache, row-major
- *     v_cache    [B][Hkv][cap/32][d][32]  compact V cache, transposed per tile
- *                of 32 rows (element (j, e) at tile j/32, column e, slot j%32);
- *                cap must be a multiple of 32
+ *     v_cache    [B][Hkv][cap][d]  compact V cache, row-major
+ *                (the kernels walk both in 32-row tiles: cap must be a
+ *                multiple of 32)
  *     kv_len     [B]               int32 current cache length per sequence (device)
  *     q, out     [B][Hq][d];  k_new, v_new [B][Hkv][d]
  *   Query head h uses KV head h / (Hq / Hkv).  The logit scale is 1/sqrt(d).
@@ -180,8 +180,7 @@ tb_status tb_select_topk(const float* scores, int32_t B, const int32_t* L,
 /* Compaction: k_cache[b][g][i] = k[b][g][keep_idx[b][g][i]] (same for v) for
  * i < n_keep[b]; the retained caches are what decoding uses (Sec. 5.2).
  * Sets kv_len[b] = n_keep[b] on the device (stream-ordered).
- * V rows are written transposed into 32-row tiles; the slots of the last
- * tile past n_keep[b] are zero-filled.
+ * Rows i >= n_keep[b] of the caches are not written.
  * Requires 1 <= n_keep[b] <= min(Lmax, cap), cap % 32 == 0.  Indices should lie in
  * [0, Lmax); the device clamps any other index into that range rather than
  * reading outside the prompt.  Caches must not alias k or v.
@@ -238,7 +237,7 @@ tb_status tb_decode_attn_noalloc(const void* q, const void* k_new, const void* v
  * The same compaction and decode over caches kept in pages of 32 rows, one
  * page holding a sequence's 32-row tile for every KV head:
  *   k_pool [n_pages][Hkv][32][d]   K rows, row-major
- *   v_pool [n_pages][Hkv][d][32]   the tile's V^T
+ *   v_pool [n_pages][Hkv][32][d]   V rows, row-major
  *   block_table [B][max_pages]     int32 (device): row t/32 of sequence b is
  *                                  in page block_table[b][t / 32]
  * A sequence holds up to max_pages * 32 rows (1 <= max_pages <= 2^25, else

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libtimebill.so")
 TB_OK, TB_EINVAL, TB_EUNSUPPORTED, TB_EWORKSPACE, TB_EHIP, TB_EINTERNAL = range(6)
 TB_F32, TB_BF16 = 0, 1
 TB_OP_SCORE, TB_OP_SELECT, TB_OP_COMPACT, TB_OP_DECODE, TB_OP_H2O = range(5)
-V_TILE = 32          # the compact V cache is stored as transposed tiles of 32 rows
+V_TILE = 32          # rows per tile (and per page) of the compact caches; cap is a multiple
 
 EXPORTED = ("tb_keep_count", "tb_last_error", "tb_workspace_bytes", "tb_score_window",
             "tb_score_window_avgpool", "tb_score_knorm", "tb_score_h2o", "tb_prefill_attn",
@@ -258,32 +258,20 @@ def tb_response_length(n_hat: int, bucket: int, k: int, n_max: int):
     return int(nh.value), int(nw)
 
 
-def v_rows_to_tiles(v_rows: torch.Tensor) -> torch.Tensor:
-    """Layout helper: V rows [..., cap, d] -> V^T tiles [..., cap/32, d, 32]."""
-    *lead, cap, d = v_rows.shape
-    return v_rows.reshape(*lead, cap // V_TILE, V_TILE, d).transpose(-1, -2).contiguous()
-
-
-def v_tiles_to_rows(v_tiles: torch.Tensor) -> torch.Tensor:
-    """Layout helper: V^T tiles [..., cap/32, d, 32] -> V rows [..., cap, d]."""
-    *lead, nt, d, t = v_tiles.shape
-    return v_tiles.transpose(-1, -2).reshape(*lead, nt * t, d)
-
-
 def _check_caches(k_cache, v_cache, B, Hkv, d):
     cap = k_cache.shape[2]
     if tuple(k_cache.shape) != (B, Hkv, cap, d):
         raise ValueError("k_cache must be [B, Hkv, cap, d]")
-    if cap % V_TILE or tuple(v_cache.shape) != (B, Hkv, cap // V_TILE, d, V_TILE):
-        raise ValueError("v_cache must be [B, Hkv, cap/32, d, 32] with cap a multiple of 32")
+    if cap % V_TILE or tuple(v_cache.shape) != (B, Hkv, cap, d):
+        raise ValueError("v_cache must be [B, Hkv, cap, d] with cap a multiple of 32")
     return cap
 
 
 def tb_compact_kv(k: torch.Tensor, v: torch.Tensor, keep_idx: torch.Tensor,
                   n_keep: Sequence[int], k_cache: torch.Tensor, v_cache: torch.Tensor,
                   kv_len: torch.Tensor, stream=None) -> None:
-    """k, v [B,Hkv,Lmax,d] -> k_cache [B,Hkv,cap,d], v_cache [B,Hkv,cap/32,d,32];
-    kv_len [B] int32 set to n_keep."""
+    """k, v [B,Hkv,Lmax,d] -> k_cache, v_cache [B,Hkv,cap,d]; kv_len [B] int32
+    set to n_keep."""
     B, Hkv, Lmax, d = k.shape
     if v.shape != k.shape:
         raise ValueError("k and v shapes disagree")
@@ -343,16 +331,16 @@ class KVCache:
     """Compact caches of one layer plus the host-side lengths the library cannot see.
 
     Allocation happens here (torch device memory); every computation is a
-    call into the library.  ``cap`` is rounded up to whole 32-row V^T tiles;
-    ``v`` holds V transposed per tile.  ``decode`` refuses an append past ``cap``.
+    call into the library.  ``cap`` is rounded up to whole 32-row tiles; ``k``
+    and ``v`` are row-major.  ``decode`` refuses an append past ``cap``.
     """
 
     def __init__(self, B: int, Hq: int, Hkv: int, cap: int, d: int, dtype: torch.dtype,
                  device="cuda"):
-        cap = -(-cap // V_TILE) * V_TILE          # whole V^T tiles
+        cap = -(-cap // V_TILE) * V_TILE          # whole 32-row tiles
         self.B, self.Hq, self.Hkv, self.cap, self.d = B, Hq, Hkv, cap, d
         self.k = torch.empty((B, Hkv, cap, d), dtype=dtype, device=device)
-        self.v = torch.empty((B, Hkv, cap // V_TILE, d, V_TILE), dtype=dtype, device=device)
+        self.v = torch.empty((B, Hkv, cap, d), dtype=dtype, device=device)
         self.kv_len = torch.zeros((B,), dtype=torch.int32, device=device)
         nbytes = tb_workspace_bytes(TB_OP_DECODE, B, 0, Hq, Hkv, d, 0, cap)
         self.ws = torch.zeros((max(nbytes, 1),), dtype=torch.uint8, device=device)
@@ -387,8 +375,8 @@ def tb_predictor_length(prefill_abc: Sequence[float], predict_abc: Sequence[floa
 
 def _check_pools(k_pool, v_pool, block_table, dtype):
     n_pages, Hkv, t, d = k_pool.shape
-    if t != V_TILE or tuple(v_pool.shape) != (n_pages, Hkv, d, V_TILE):
-        raise ValueError("pools must be k_pool [P, Hkv, 32, d] and v_pool [P, Hkv, d, 32]")
+    if t != V_TILE or tuple(v_pool.shape) != (n_pages, Hkv, V_TILE, d):
+        raise ValueError("pools must be k_pool and v_pool [P, Hkv, 32, d]")
     if k_pool.dtype != dtype or v_pool.dtype != dtype:
         raise TypeError("pools must share the inputs' dtype")
     if block_table.dim() != 2:

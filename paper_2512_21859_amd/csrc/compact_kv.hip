@@ -2,17 +2,15 @@
 //
 // grid = (ceil(max n_keep / 32), Hkv, B), block = 256 threads; block t fills
 // destination rows [32t, 32t + 32) of one (sequence, KV head), i.e. one
-// 32-row tile of the contiguous cache or one page of a paged cache:
-//   K rows are copied row-major: each row is split into 16-byte pieces, one
-//     per lane, so a wave instruction moves whole contiguous rows;
-//   V rows are gathered into LDS, then written as one transposed 32-row tile
-//     [d][32] (contiguous 16-byte stores of 8 (bf16) or 4 (fp32) keys of one
-//     column); slots past n_keep are zero-filled.
-// All loads of a thread are issued before its stores.  HBM traffic is one read
-// and one write of each kept row of K and V.  The cache writes are streaming
-// (non-temporal) stores: measured at L = 131072, 8 KV heads, half the rows
-// kept, 80 us against 104 us with ordinary stores (6.7 against 5.2 TB/s);
-// non-temporal loads of the gathered rows did not help.
+// 32-row tile of the contiguous cache or one page of a paged cache.  K and V
+// rows are both copied row-major: each row is split into 16-byte pieces, one
+// per lane, so a wave instruction moves whole contiguous rows.  Rows past
+// n_keep are not written.  All loads of a thread are issued before its
+// stores.  HBM traffic is one read and one write of each kept row of K and V.
+// The cache writes are streaming (non-temporal) stores: measured at
+// L = 131072, 8 KV heads, half the rows kept, 80 us against 104 us with
+// ordinary stores (6.7 against 5.2 TB/s); non-temporal loads of the gathered
+// rows did not help.
 
 #include "common.h"
 #include "kernels.h"
@@ -29,9 +27,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   constexpr int LPR = ROW_BYTES / 16;                 // lanes per row
   constexpr int ROWS_PER_PASS = kThreads / LPR;
   constexpr int PASSES = kVT / ROWS_PER_PASS;
-  constexpr int EPV = 16 / sizeof(T);                 // elements per 16 bytes
-  constexpr int TILE_VECS = D * kVT / EPV;            // 16-byte pieces per V^T tile
-  static_assert(PASSES >= 1 && TILE_VECS % kThreads == 0, "tile shape");
+  static_assert(PASSES >= 1 && kVT % ROWS_PER_PASS == 0, "tile shape");
   const int tile = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int n = a.n_keep[b];
   const int i0 = tile * kVT;
@@ -44,16 +40,12 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   const char* vs = static_cast<const char*>(a.v) + bg * a.Lmax * ROW_BYTES + part * 16;
   const size_t off = cache_tile_off<PAGED>(a, b, g, tile, D);   // element offset of the tile
   char* kd = static_cast<char*>(a.k_cache) + off * sizeof(T) + part * 16;   // tile row 0
-  T* vtile = static_cast<T*>(a.v_cache) + off;
-
-  __shared__ T s_v[kVT][D + EPV];                     // padded rows
+  char* vd = static_cast<char*>(a.v_cache) + off * sizeof(T) + part * 16;
 
   uint4 kr[PASSES], vr[PASSES];
 #pragma unroll
   for (int p = 0; p < PASSES; ++p) {
     const int i = i0 + r0 + p * ROWS_PER_PASS;
-    kr[p] = make_uint4(0u, 0u, 0u, 0u);
-    vr[p] = make_uint4(0u, 0u, 0u, 0u);
     if (i < n) {
       // indices are clamped into the prompt so a bad index cannot fault
       const int j = min(max(keep[i], 0), a.Lmax - 1);
@@ -65,18 +57,10 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
 #pragma unroll
   for (int p = 0; p < PASSES; ++p) {
     const int rr = r0 + p * ROWS_PER_PASS;
-    if (i0 + rr < n) stg16_stream(kd + static_cast<size_t>(rr) * ROW_BYTES, kr[p]);
-    *reinterpret_cast<uint4*>(&s_v[rr][part * EPV]) = vr[p];   // zero past n_keep
-  }
-  __syncthreads();
-  // V^T tile: piece v covers column d = v / (32/EPV), keys (v % (32/EPV))*EPV ..
-#pragma unroll
-  for (int v = threadIdx.x; v < TILE_VECS; v += kThreads) {
-    const int d = v / (kVT / EPV), k0 = (v % (kVT / EPV)) * EPV;
-    T vals[EPV];
-#pragma unroll
-    for (int e = 0; e < EPV; ++e) vals[e] = s_v[k0 + e][d];
-    stg16_stream(vtile + static_cast<size_t>(d) * kVT + k0, *reinterpret_cast<const uint4*>(vals));
+    if (i0 + rr < n) {
+      stg16_stream(kd + static_cast<size_t>(rr) * ROW_BYTES, kr[p]);
+      stg16_stream(vd + static_cast<size_t>(rr) * ROW_BYTES, vr[p]);
+    }
   }
 }
 

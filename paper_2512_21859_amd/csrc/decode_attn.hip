@@ -1,12 +1,17 @@
 // Single-token grouped-query decode attention over the compact KV cache,
 // with the new token's K/V appended in the same step.
 //
-// Cache layout: K rows are row-major [B][Hkv][cap][d]; V is stored
-// transposed in tiles of 32 rows, [B][Hkv][cap/32][d][32], so that the
-// matrix-core operand "8 consecutive keys of one V column" is one contiguous
-// 16-byte load.  Paged caches (a block table per sequence) keep the same
-// 32-row tiles in pools [pages][Hkv][32][d] / [pages][Hkv][d][32]; a wave's
-// 32-row step then starts with one table lookup.
+// Cache layout: K and V rows are row-major, [B][Hkv][cap][d].  The kernels
+// walk the cache in tiles of 32 rows; paged caches (a block table per
+// sequence) keep those tiles as pages of pools [pages][Hkv][32][d], and a
+// wave's 32-row step starts with one table lookup.  The matrix-core PV
+// product wants "8 consecutive keys of one V column" per lane: each wave
+// copies a tile's V rows into its own LDS buffer (16-byte chunks swizzled by
+// row) and reads the operand back with the gfx950 transpose read.  Measured
+// against a cache stored as transposed 32-row tiles (one 16-byte global load
+// per operand, no LDS): bit-identical, 0-3.5% faster for caches of 8k-33k
+// rows, 4-7% slower below 4k rows (one wave per block, where the LDS round
+// trip is not hidden).
 //
 // Two launches per decode step and layer (both capturable in a HIP graph):
 //   partial kernel, grid = (n_chunks, Hkv, B): block (c, g, b) covers a
@@ -57,6 +62,25 @@ __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
+
+// transpose read of 4 bf16: within each 16-lane group, lane i receives
+// element i % 4 of the 8-byte chunks read by lanes 4j + i / 4, j = 0..3
+__device__ __forceinline__ u32x2 lds_read_tr16(const void* p) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4s*)p));
+}
+
+// Chunk c of V row R of a wave's buffer sits at c ^ vswz(R): a half-wave's
+// transpose reads (rows 8 g + 0..3 and 8 (g + 1) + 0..3, 32 bytes each)
+// then cover all banks.  Rows R and R + 4 (and R + 32 k) share the swizzle.
+template <int D>
+__device__ __forceinline__ int vswz(int R) {
+  if constexpr (D == 128) return 2 * ((R & 3) | (((R >> 3) & 1) << 2));   // 16 chunks per row
+  else return 2 * (((R >> 1) & 1) | (((R >> 3) & 1) << 1));               // 8 chunks per row
+}
+
 // --------------------------------------------------------------------------
 // bf16: matrix-core partial kernel.
 // --------------------------------------------------------------------------
@@ -73,12 +97,18 @@ void decode_mfma_kernel(DecodeArgs a) {
   const int q4 = lane >> 4, r16 = lane & 15;
   const int Hkv = a.Hkv, Hq = Hkv * G;
 
-  __shared__ float4 s_o[WAVES][G][D / 4 + 1];     // +1: spreads heads over banks
+  // Each wave's V rows of its current tile (32 rows x 16 chunks of 16 bytes,
+  // chunk c of row R at c ^ vswz(R)); after the tile loop the same bytes hold
+  // the wave's (o) for the block's combine: [G][D / 4 + 1] float4 per wave,
+  // +1 spreading the heads over banks (3.7 KB of the 8 KB at G = 7, d = 128).
+  constexpr int CH = D / 8;                       // 16-byte chunks per row
+  static_assert(G * (D / 4 + 1) * 16 <= kVT * CH * 16, "combine buffer fits the V buffer");
+  __shared__ u32x4 s_v[WAVES][kVT * CH];
   __shared__ float s_ml[WAVES][16][2];
 
   const size_t bg = static_cast<size_t>(b) * Hkv + g;
   const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
-  const uint16_t* vt = static_cast<const uint16_t*>(a.v_cache);
+  const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
   const uint16_t* kn = static_cast<const uint16_t*>(a.k_new) + bg * D;
   const uint16_t* vn = static_cast<const uint16_t*>(a.v_new) + bg * D;
   const int cap = a.cap;
@@ -92,7 +122,9 @@ void decode_mfma_kernel(DecodeArgs a) {
   // Everything below up to the length check is issued without waiting for
   // kv_len: the first block's K/V loads only need rows < cap, so the length
   // load and the data loads are in flight together.
-  u32x4 kr[2][KC], vr[NC];
+  // V rows: the tile's 32 x CH chunks, chunk p = 64 u + lane (row p / CH)
+  constexpr int VPL = kVT * CH / 64;              // V chunks per lane (8 at d = 128)
+  u32x4 kr[2][KC], vr[VPL];
   auto load_block = [&](int base) {            // base: a multiple of 32 below cap
     const size_t off = cache_tile_off<PAGED>(a, b, g, base / kVT, D);
 #pragma unroll
@@ -101,10 +133,11 @@ void decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
       for (int k = 0; k < KC; ++k) kr[t][k] = ld16(src + 32 * k + 8 * q4);
     }
-    const uint16_t* vtile = vt + off;
+    const uint16_t* vtile = vc + off;
 #pragma unroll
-    for (int n = 0; n < NC; ++n) vr[n] = ld16(vtile + (16 * n + r16) * kVT + 8 * q4);
+    for (int u = 0; u < VPL; ++u) vr[u] = ld16(vtile + static_cast<size_t>(64 * u + lane) * 8);
   };
+  u32x4* sv = s_v[wave];
   int n0 = a.kv_len[b];
   if (t_first < t_hi) load_block(kVT * t_first);
 
@@ -145,9 +178,9 @@ void decode_mfma_kernel(DecodeArgs a) {
       for (int k = 0; k < KC; ++k) *reinterpret_cast<u32x4*>(kd + 32 * k + 8 * q4) = knew[k];
     }
     if (q4 == 0) {
-      uint16_t* vd = static_cast<uint16_t*>(a.v_cache) + off + (n0 % kVT);
+      uint16_t* vd = static_cast<uint16_t*>(a.v_cache) + off + static_cast<size_t>(n0 % kVT) * D;
 #pragma unroll
-      for (int n = 0; n < NC; ++n) vd[(16 * n + r16) * kVT] = vnew[n];
+      for (int n = 0; n < NC; ++n) vd[16 * n + r16] = vnew[n];
     }
   }
 
@@ -164,8 +197,13 @@ void decode_mfma_kernel(DecodeArgs a) {
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int k = 0; k < KC; ++k) ck[t][k] = kr[t][k];
+    // this tile's V rows into the wave's buffer (the wave's earlier reads of
+    // it are done: LDS accesses of one wave complete in order)
 #pragma unroll
-    for (int n = 0; n < NC; ++n) cv[n] = vr[n];
+    for (int u = 0; u < VPL; ++u) {
+      const int cidx = 64 * u + lane, R = cidx / CH;
+      sv[R * CH + ((cidx % CH) ^ vswz<D>(R))] = vr[u];
+    }
     if (t + WAVES < t_end) load_block(kVT * (t + WAVES));   // prefetch the next tile
 
     // wave-uniform: does this tile hold the appended row, or run past the end?
@@ -216,8 +254,19 @@ void decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) pB[j] = static_cast<__bf16>(p[j]);
 
-    // ---- V^T operand: zero keys past the end, patch the appended row
-    // (branch-free word masks over this lane's 8 keys)
+    // ---- V^T operand by transpose reads: lane (q4, r16) reads 8 bytes (d =
+    // 16 n + 4 (r16 & 3) .. +3) of rows 8 q4 + r16 / 4 and + 4, and receives
+    // d = 16 n + r16 of keys 8 q4 .. 8 q4 + 7; rows +4 share the swizzle
+#pragma unroll
+    for (int n = 0; n < NC; ++n) {
+      const int R1 = 8 * q4 + (r16 >> 2);
+      const int ch = 2 * n + ((r16 & 3) >> 1);
+      const uint16_t* p1 = reinterpret_cast<const uint16_t*>(sv + R1 * CH + (ch ^ vswz<D>(R1))) + (r16 & 1) * 4;
+      const u32x2 lo = lds_read_tr16(p1), hi = lds_read_tr16(p1 + 4 * D);
+      cv[n] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+    }
+    // zero keys past the end, patch the appended row (branch-free word masks
+    // over this lane's 8 keys)
     if (tail || has_new) {
       const int kq = base + 8 * q4;               // first key of this lane's 8
       const int cnt = min(max(N - kq, 0), 8);     // valid keys among the 8
@@ -261,10 +310,14 @@ void decode_mfma_kernel(DecodeArgs a) {
     if (c == 0 && g == 0 && tid == 0) a.seq_len[b] = N;
     return;
   }
+  // the wave's (o) goes into its own V buffer (its last reads of it are done)
+  auto s_o = [&](int wv, int h, int e4) -> float4& {
+    return reinterpret_cast<float4*>(s_v[wv])[h * (D / 4 + 1) + e4];
+  };
   if (r16 < G) {
 #pragma unroll
     for (int n = 0; n < NC; ++n)
-      s_o[wave][r16][4 * n + q4] = make_float4(accO[n][0], accO[n][1], accO[n][2], accO[n][3]);
+      s_o(wave, r16, 4 * n + q4) = make_float4(accO[n][0], accO[n][1], accO[n][2], accO[n][3]);
   }
   if (q4 == 0) { s_ml[wave][r16][0] = m_run; s_ml[wave][r16][1] = l_tot; }
   __syncthreads();
@@ -280,7 +333,7 @@ void decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
       for (int wv = 0; wv < WAVES; ++wv) {
         const float sc = exp2f(s_ml[wv][h][0] - M);
-        const float4 x = s_o[wv][h][e4];
+        const float4 x = s_o(wv, h, e4);
         L += s_ml[wv][h][1] * sc;
         O.x += x.x * sc; O.y += x.y * sc; O.z += x.z * sc; O.w += x.w * sc;
       }
@@ -319,14 +372,14 @@ __global__ __launch_bounds__(kValuThreads) void decode_valu_kernel(DecodeArgs a)
 
   const size_t bg = static_cast<size_t>(b) * Hkv + g;
   const float* kc = static_cast<const float*>(a.k_cache);
-  const float* vt = static_cast<const float*>(a.v_cache);
+  const float* vc = static_cast<const float*>(a.v_cache);
   const float* kn = static_cast<const float*>(a.k_new) + bg * D;
   const float* vn = static_cast<const float*>(a.v_new) + bg * D;
 
   if (app && n0 >= lo && n0 < hi && wave == 0) {
     const size_t off = cache_tile_off<PAGED>(a, b, g, n0 / kVT, D);
     float* kd = static_cast<float*>(a.k_cache) + off + static_cast<size_t>(n0 % kVT) * D;
-    float* vd = static_cast<float*>(a.v_cache) + off + (n0 % kVT);
+    float* vd = static_cast<float*>(a.v_cache) + off + static_cast<size_t>(n0 % kVT) * D;
     constexpr int PER = (D + 63) / 64;
     float kx[PER], vx[PER];
 #pragma unroll
@@ -338,7 +391,7 @@ __global__ __launch_bounds__(kValuThreads) void decode_valu_kernel(DecodeArgs a)
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int e = lane + 64 * i;
-      if (e < D) { kd[e] = kx[i]; vd[e * kVT] = vx[i]; }
+      if (e < D) { kd[e] = kx[i]; vd[e] = vx[i]; }
     }
   }
 
@@ -372,12 +425,12 @@ __global__ __launch_bounds__(kValuThreads) void decode_valu_kernel(DecodeArgs a)
       const int rr = valid[u] ? row : wlo;                      // a row inside the cache
       const size_t off = cache_tile_off<PAGED>(a, b, g, rr / kVT, D);
       const float* krow = kc + off + static_cast<size_t>(rr % kVT) * D;
-      const float* vcol = vt + off + (rr % kVT);
+      const float* vrow = vc + off + static_cast<size_t>(rr % kVT) * D;
 #pragma unroll
       for (int e = 0; e < DPL; ++e) {
         const int d = sub * DPL + e;
         kf[u][e] = valid[u] ? (is_new ? kn[d] : krow[d]) : 0.f;
-        vf[u][e] = valid[u] ? (is_new ? vn[d] : vcol[d * kVT]) : 0.f;
+        vf[u][e] = valid[u] ? (is_new ? vn[d] : vrow[d]) : 0.f;
       }
     }
     float s[kUnroll][G];

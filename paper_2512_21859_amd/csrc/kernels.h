@@ -10,7 +10,7 @@ namespace tb {
 constexpr int kMaxB = 64;        // per-sequence values travel in kernel arguments
 constexpr int kScoreTile = 64;   // keys per scoring tile
 constexpr int kScoreRows = 256;  // window rows per scoring block
-constexpr int kVTile = 32;       // rows per V^T tile of the compact V cache
+constexpr int kVTile = 32;       // rows per tile of the compact caches (and per page)
 
 // ---------------------------------------------------------------- scoring
 struct ScoreArgs {
@@ -93,11 +93,11 @@ struct CompactArgs {
   const void* v;
   const int32_t* keep_idx;  // [B][Hkv][Lmax]
   void* k_cache;          // [B][Hkv][cap][d]
-  void* v_cache;          // [B][Hkv][cap/32][d][32]
+  void* v_cache;          // [B][Hkv][cap][d]
   int32_t* kv_len;        // [B]
   int32_t B, Lmax, Hkv, cap;
   // paged caches (table != nullptr): tile t of sequence b lives in page
-  // table[b * max_pages + t] of pools [n_pages][Hkv][32][d] (K) / [d][32] (V^T)
+  // table[b * max_pages + t] of pools [n_pages][Hkv][32][d] (K and V)
   const int32_t* table;
   int32_t max_pages, n_pages;
   int32_t n_keep[kMaxB];
@@ -107,9 +107,9 @@ hipError_t launch_compact(const CompactArgs& a, int d, int elem_bytes, int max_k
 
 // ---------------------------------------------------------------- decode
 // Element offset of the 32-row tile t of (sequence b, KV head g) in the K
-// cache and in the V^T cache (the same offset for both: a tile holds 32 K rows
-// or one 32-key V^T tile).  Contiguous caches: [B][Hkv][cap][d]; paged: pools
-// [n_pages][Hkv][32][d], page from the block table, clamped into the pool.
+// cache and in the V cache (the same offset for both).  Contiguous caches:
+// [B][Hkv][cap][d]; paged: pools [n_pages][Hkv][32][d], page from the block
+// table, clamped into the pool.
 template <bool PAGED, typename Args>
 __device__ __forceinline__ size_t cache_tile_off(const Args& a, int b, int g, int t, int d) {
   if constexpr (PAGED) {
@@ -126,7 +126,7 @@ struct DecodeArgs {
   const void* k_new;      // [B][Hkv][d] (unused when append == 0)
   const void* v_new;
   void* k_cache;          // [B][Hkv][cap][d]
-  void* v_cache;          // [B][Hkv][cap/32][d][32]
+  void* v_cache;          // [B][Hkv][cap][d]
   int32_t* kv_len;        // [B]
   void* out;              // [B][Hq][d]
   float* part;            // ws: [B][Hkv][n_chunks][G][d+4] chunk partials (o, m, l)

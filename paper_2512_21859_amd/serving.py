@@ -7,8 +7,8 @@ response length).  Requests are admitted in batches: one batched eviction
 which they join the running batch, where every decode step serves all active
 requests in one launch per layer.
 
-Layout: every layer has its own page pools (k_pool [P, Hkv, 32, d], v_pool
-[P, Hkv, d, 32]); one block table [max_seqs, max_pages] serves all layers, so
+Layout: every layer has its own page pools (k_pool and v_pool
+[P, Hkv, 32, d]); one block table [max_seqs, max_pages] serves all layers, so
 a request owns the same page numbers in every layer.  Each layer keeps its own
 kv_len [max_seqs] because every decode call appends to it.  The active
 requests occupy slots 0..n-1 of the table; a retiring request's slot is
@@ -228,7 +228,7 @@ class Server:
         self.w, self.pool, self.max_admit, self.max_prompt = w, pool, max_admit, max_prompt
         self.slots = SlotTable(n_pages, max_seqs, max_pages)
         self.k_pool = torch.zeros((n_layers, n_pages, Hkv, PAGE, d), dtype=dtype, device=device)
-        self.v_pool = torch.zeros((n_layers, n_pages, Hkv, d, PAGE), dtype=dtype, device=device)
+        self.v_pool = torch.zeros((n_layers, n_pages, Hkv, PAGE, d), dtype=dtype, device=device)
         self.table = torch.zeros((max_seqs, max_pages), dtype=torch.int32, device=device)
         self.kv_len = torch.zeros((n_layers, max_seqs), dtype=torch.int32, device=device)
         # covers every batch size up to max_seqs

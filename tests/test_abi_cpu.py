@@ -234,7 +234,7 @@ def test_compact_validation(lib):
                                  FAKE, None, 0, None)
 
     assert call(n=65) == E.TB_EINVAL          # beyond cap
-    assert call(cap=60) == E.TB_EINVAL        # cap not a whole number of V^T tiles
+    assert call(cap=60) == E.TB_EINVAL        # cap not a whole number of 32-row tiles
     assert call(n=0) == E.TB_EINVAL
     assert call(n=101, cap=200) == E.TB_EINVAL  # beyond Lmax
     assert call(d=32) == E.TB_EUNSUPPORTED
@@ -253,7 +253,7 @@ def test_decode_validation(lib):
     assert call(Hq=30) == E.TB_EINVAL
     assert call(d=256) == E.TB_EUNSUPPORTED
     assert call(cap=0) == E.TB_EINVAL
-    assert call(cap=100) == E.TB_EINVAL       # cap not a whole number of V^T tiles
+    assert call(cap=100) == E.TB_EINVAL       # cap not a whole number of 32-row tiles
     assert call(wsb=8) == E.TB_EWORKSPACE
     assert call(ws=None) == E.TB_EINVAL
 

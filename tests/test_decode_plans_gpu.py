@@ -49,7 +49,7 @@ def test_single_sequence_plans(cap, d):
     vn = torch.randn((T, B, Hkv, d), generator=gen).to(torch.bfloat16)
     cache = _lib.KVCache(B, Hq, Hkv, cap, d, torch.bfloat16)
     cache.k.copy_(kc)
-    cache.v.copy_(_lib.v_rows_to_tiles(vc))
+    cache.v.copy_(vc)
     cache.kv_len.fill_(n0)
     cache.host_len = [n0]
     out = torch.empty((T, B, Hq, d), dtype=torch.bfloat16, device=DEV)

@@ -54,7 +54,7 @@ def test_smallest_prefix_and_wide_pool(pool):
 def _cache_with(B, Hq, Hkv, d, cap, dtype, kc, vc, lens):
     cache = _lib.KVCache(B, Hq, Hkv, cap, d, dtype)
     cache.k.copy_(kc)
-    cache.v.copy_(_lib.v_rows_to_tiles(vc))
+    cache.v.copy_(vc)
     cache.kv_len.copy_(torch.tensor(lens, dtype=torch.int32))
     cache.host_len = list(lens)
     return cache
@@ -150,12 +150,12 @@ def test_compact_clamps_out_of_range_indices(dtype):
     keep[:, :, : len(idx)] = torch.tensor(idx, dtype=torch.int32)
     n_keep = [len(idx), 3]
     kc = torch.zeros((B, Hkv, cap, d), dtype=dtype, device=DEV)
-    vc = torch.zeros((B, Hkv, cap // 32, d, 32), dtype=dtype, device=DEV)
+    vc = torch.zeros((B, Hkv, cap, d), dtype=dtype, device=DEV)
     kv_len = torch.zeros((B,), dtype=torch.int32, device=DEV)
     _lib.tb_compact_kv(k.to(DEV), v.to(DEV), keep.to(DEV), n_keep, kc, vc, kv_len)
     torch.cuda.synchronize()
     clamped = [min(max(i, 0), Lmax - 1) for i in idx]
-    v_rows = vc.cpu().transpose(-1, -2).reshape(B, Hkv, cap, d)
+    v_rows = vc.cpu()
     for b in range(B):
         rows = clamped[: n_keep[b]]
         assert torch.equal(kc[b, :, : n_keep[b]].cpu(), k[b][:, rows])
@@ -179,7 +179,7 @@ def test_decode_full_cache_drops_the_append(dtype):
     vn = torch.randn((B, Hkv, d), generator=gen).to(dtype)
     cache = _lib.KVCache(B, Hq, Hkv, cap, d, dtype)
     cache.k.copy_(kc)
-    cache.v.copy_(_lib.v_rows_to_tiles(vc))
+    cache.v.copy_(vc)
     cache.kv_len.fill_(cap)
     k_before, v_before = cache.k.clone(), cache.v.clone()
     out = torch.empty((B, Hq, d), dtype=dtype, device=DEV)

@@ -36,8 +36,8 @@ def case(msg):
     print(f"\n[case] {msg}", flush=True)
 
 
-def _gather_k(k_pool, pages, g, n):
-    return torch.cat([k_pool[p, g] for p in pages], dim=0)[:n]
+def _gather_rows(pool, pages, g, n):
+    return torch.cat([pool[p, g] for p in pages], dim=0)[:n]
 
 
 @pytest.mark.parametrize("dtype,d,G", [(torch.bfloat16, 128, 7), (torch.bfloat16, 128, 8),
@@ -75,10 +75,10 @@ def test_paged_equals_contiguous(dtype, d, G):
         junk = [-7, 10 ** 6, n_pages][b]
         table[b] = torch.tensor(pages[b] + [junk] * (max_pages - need[b]), dtype=torch.int32)
     k_pool = torch.full((n_pages, Hkv, PAGE, d), FILL, dtype=dtype, device=DEV)
-    v_pool = torch.full((n_pages, Hkv, d, PAGE), FILL, dtype=dtype, device=DEV)
+    v_pool = torch.full((n_pages, Hkv, PAGE, d), FILL, dtype=dtype, device=DEV)
     cap = max_pages * PAGE
     kc = torch.full((B, Hkv, cap, d), FILL, dtype=dtype, device=DEV)
-    vc = torch.full((B, Hkv, cap // PAGE, d, PAGE), FILL, dtype=dtype, device=DEV)
+    vc = torch.full((B, Hkv, cap, d), FILL, dtype=dtype, device=DEV)
     len_p = torch.zeros((B,), dtype=torch.int32, device=DEV)
     len_c = torch.zeros((B,), dtype=torch.int32, device=DEV)
     kd, vd, keepd, tabd = k.to(DEV), v.to(DEV), keep.to(DEV), table.to(DEV)
@@ -102,9 +102,10 @@ def test_paged_equals_contiguous(dtype, d, G):
     for b in range(B):
         n = n_keep[b] + T
         for g in range(Hkv):
-            assert torch.equal(_gather_k(k_pool, pages[b], g, n), kc[b, g, :n])
+            assert torch.equal(_gather_rows(k_pool, pages[b], g, n), kc[b, g, :n])
             for t, p in enumerate(pages[b]):
-                assert torch.equal(v_pool[p, g], vc[b, g, t]), f"b={b} g={g} tile {t}"
+                assert torch.equal(v_pool[p, g], vc[b, g, PAGE * t:PAGE * (t + 1)]), \
+                    f"b={b} g={g} tile {t}"
     for p in unused:
         assert bool((k_pool[p] == FILL).all()) and bool((v_pool[p] == FILL).all()), \
             f"page {p} owned by nobody was written"
@@ -368,9 +369,8 @@ def _rows(srv, r, layers):
         out = []
         for layer in range(layers):
             for g in range(srv.Hkv):
-                out.append(_gather_k(srv.k_pool[layer], e.pages, g, e.length).clone())
-                out.append(torch.cat([srv.v_pool[layer][p, g] for p in e.pages], dim=1)
-                           [:, : e.length].clone())
+                out.append(_gather_rows(srv.k_pool[layer], e.pages, g, e.length).clone())
+                out.append(_gather_rows(srv.v_pool[layer], e.pages, g, e.length).clone())
         return out
 
 
@@ -570,7 +570,7 @@ def test_paged_decode_clamps_table_entries():
     Hq = Hkv * G
     gen = torch.Generator().manual_seed(31)
     k_pool = torch.randn((n_pages, Hkv, PAGE, d), generator=gen).to(torch.bfloat16)
-    v_pool = torch.randn((n_pages, Hkv, d, PAGE), generator=gen).to(torch.bfloat16)
+    v_pool = torch.randn((n_pages, Hkv, PAGE, d), generator=gen).to(torch.bfloat16)
     q = torch.randn((1, Hq, d), generator=gen).to(torch.bfloat16)
     kn = torch.randn((1, Hkv, d), generator=gen).to(torch.bfloat16)
     vn = torch.randn((1, Hkv, d), generator=gen).to(torch.bfloat16)
@@ -589,7 +589,7 @@ def test_paged_decode_clamps_table_entries():
     got = f64(out[0])
     for g in range(Hkv):
         k_rows = torch.cat([k_pool[p, g] for p in used])[:n0]
-        v_rows = torch.cat([v_pool[p, g].transpose(0, 1) for p in used])[:n0]
+        v_rows = torch.cat([v_pool[p, g] for p in used])[:n0]
         rk = np.concatenate([f64(k_rows), f64(kn[0, g])[None]])
         rv = np.concatenate([f64(v_rows), f64(vn[0, g])[None]])
         ref = O.decode_step(f64(q[0, g * G:(g + 1) * G]), rk, rv)

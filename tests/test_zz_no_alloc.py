@@ -29,7 +29,7 @@ def _pair(seed, B, Hq, Hkv, d, cap, lens, dtype):
     for _ in range(2):
         c = _lib.KVCache(B, Hq, Hkv, cap, d, dtype)
         c.k.copy_(kc)
-        c.v.copy_(_lib.v_rows_to_tiles(vc))
+        c.v.copy_(vc)
         c.kv_len.copy_(torch.tensor(lens, dtype=torch.int32))
         c.host_len = list(lens)
         caches.append(c)
