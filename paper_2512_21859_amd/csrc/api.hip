@@ -85,11 +85,15 @@ namespace tb {
 //   and its cap/32 tiles are split between them as evenly as whole tiles
 //   allow (blocks of a fixed row count left up to 48 CUs idle; a second
 //   round of blocks past 256 doubles the step time).
-// * A block's tiles are shared by the most waves (1, 2, 4 or 8) that still
-//   give every wave a tile: with two waves per SIMD (the register budget)
-//   more waves keep more tiles in flight per CU.  At 28 layers, 32768 rows:
-//   18.4-18.7 us per layer-step with 8 waves against 19.3 (4) and 20.5 (2);
-//   16384 rows: 13.4 against 13.8 (4); 8192 rows: 10.9 (4) against 11.2 (2).
+// * A block's tiles are shared by 1, 2, 4 or 8 waves: with two waves per
+//   SIMD (the register budget) more waves keep more tiles in flight per CU,
+//   but each wave also stages its tile's V rows through LDS, and a wave with
+//   a single tile cannot hide that.  Measured with the row-major V cache at
+//   28 layers (us per layer-step, 2-16 tiles per block): 2 tiles, one wave
+//   9.51 against 9.62 (two); 3 tiles, two waves 10.26 against 10.64 (one);
+//   4-7 tiles, four waves 11.37-13.08 against 11.59-13.42 (two); 8 tiles,
+//   four waves 13.31 against 13.52 (eight); 9-16 tiles, eight waves 14.56-
+//   19.13 against 14.68-19.22 (four).
 // * Small caches (<= 2560 rows) keep at most 32 partials per KV head, which
 //   one wave per query head merges in a single round of loads.
 // * Batches (B > 1) are usually ragged, and the plan sees only the capacity:
@@ -121,8 +125,7 @@ DecodePlan decode_plan(int B, int Hkv, int cap, bool bf16) {
   C = std::max<long long>(1, std::min<long long>({C, tiles, decode_max_chunks()}));
   const long long per_block = tiles / C;       // every block holds per_block or per_block + 1
   int waves = 1;
-  if (!batch)
-    while (waves < 8 && 2 * waves <= per_block) waves *= 2;
+  if (!batch) waves = per_block >= 9 ? 8 : per_block >= 4 ? 4 : per_block >= 3 ? 2 : 1;
   p.waves = waves;
   p.n_chunks = static_cast<int32_t>(C);
   p.chunk = static_cast<int32_t>((tiles + C - 1) / C * kVTile);   // rows of the largest block
