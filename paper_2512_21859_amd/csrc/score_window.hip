@@ -11,7 +11,8 @@
 // Four kernels, all with fixed-order reductions (no atomics):
 //   K1 score_tiles: block = (64-key tile, <=256 window rows) of one KV head,
 //      512 threads; wave w owns 32 rows x the 64 keys (waves whose rows are all
-//      padding skip the products).  Window queries and keys are staged in LDS
+//      padding skip the products).  Window queries (as fp32) and keys (as
+//      float64, converted once since every wave reads them) are staged in LDS
 //      in 32-wide d chunks, the next chunk's global loads in flight while the
 //      current one is multiplied; the float64 dot products run on the matrix
 //      cores (v_mfma_f64_16x16x4_f64, 2 x 4 tiles of 16 x 16 per wave).  Each
@@ -115,7 +116,7 @@ __global__ __launch_bounds__(kTilesThreads, 2) void score_tiles_kernel(ScoreArgs
   const bool active = row0 + kWaveRows * wave < R;    // wave-uniform: not all padding
 
   __shared__ float qs[kRows][kDC + 1];             // +1: conflict-free column reads
-  __shared__ float ks[kT][kDC + 1];
+  __shared__ double ks[kT][kDC + 1];             // keys staged as float64: every wave reads them
   __shared__ int s_lim[kRows];                     // last key a row sees (-1: padding)
   if (tid < kRows) {
     const int r = row0 + tid;
@@ -156,7 +157,7 @@ __global__ __launch_bounds__(kTilesThreads, 2) void score_tiles_kernel(ScoreArgs
     for (int e = 0; e < 16; ++e) qs[qrow][qoff + e] = qv[e];
     if (tid < 256) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ks[kk][kdp + e] = kv[e];
+      for (int e = 0; e < 8; ++e) ks[kk][kdp + e] = static_cast<double>(kv[e]);
     }
   };
 
@@ -182,7 +183,7 @@ __global__ __launch_bounds__(kTilesThreads, 2) void score_tiles_kernel(ScoreArgs
         for (int rt = 0; rt < 2; ++rt)
           av[rt] = static_cast<double>(qs[kWaveRows * wave + 16 * rt + r16][dd]);
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) bv[kt] = static_cast<double>(ks[16 * kt + r16][dd]);
+        for (int kt = 0; kt < 4; ++kt) bv[kt] = ks[16 * kt + r16][dd];
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
