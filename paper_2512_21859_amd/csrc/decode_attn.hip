@@ -56,7 +56,7 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
-constexpr int kVT = kVTile;           // rows per V^T tile (32)
+constexpr int kVT = kVTile;           // rows per cache tile (32)
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 
@@ -97,7 +97,7 @@ void decode_mfma_kernel(DecodeArgs a) {
   const int q4 = lane >> 4, r16 = lane & 15;
   const int Hkv = a.Hkv, Hq = Hkv * G;
 
-  // Each wave's V rows of its current tile (32 rows x 16 chunks of 16 bytes,
+  // Each wave's V rows of its current tile (32 rows x CH chunks of 16 bytes,
   // chunk c of row R at c ^ vswz(R)); after the tile loop the same bytes hold
   // the wave's (o) for the block's combine: [G][D / 4 + 1] float4 per wave,
   // +1 spreading the heads over banks (3.7 KB of the 8 KB at G = 7, d = 128).
