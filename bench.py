@@ -93,19 +93,28 @@ def _evict_bytes(Hq, Hkv, d, L, w, n_keep, esz=2):
     return score + select + compact
 
 
+def code_sha256(text):
+    """sha256 of a C++ source with its comments and whitespace removed, so
+    that edits to comments alone do not count as a change of the code."""
+    import hashlib
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return hashlib.sha256("".join(text.split()).encode()).hexdigest()
+
+
 def measured_traffic():
     """HBM bytes per decode call of the headline sweep from the committed counter
     runs, or None when the decode kernels or their launch plan have changed
-    since the counters were taken (the record holds the sha256 of each source
+    since the counters were taken (the record holds code_sha256 of each source
     it depends on)."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", "decode_traffic.json")
     try:
         with open(path) as f:
             rec = json.load(f)
-        for src, sha in rec["sources_sha256"].items():
-            with open(os.path.join(ROOT, src), "rb") as f:
-                if hashlib.sha256(f.read()).hexdigest() != sha:
+        for src, sha in rec["sources_code_sha256"].items():
+            with open(os.path.join(ROOT, src)) as f:
+                if code_sha256(f.read()) != sha:
                     return None
     except (OSError, KeyError, ValueError, AttributeError):
         return None
