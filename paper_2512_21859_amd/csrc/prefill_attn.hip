@@ -21,10 +21,11 @@
 // key 8(r/4) + 4t + r%4) so that lane group q of the S^T result holds keys
 // 8q .. 8q+7 of the step, exactly the P^T operand: the online softmax, the
 // bf16 packing of P and the rescale of O^T stay in the lane.  Softmax runs in
-// the base-2 domain with fp32 statistics (the running max on the raw dot
-// products, the scale folded into each exponent's FMA); P is rounded to bf16
-// for the PV product.  O^T is rescaled only in steps where some row's max
-// moved.  Each step runs its two column tiles phase by phase (both QK
+// the base-2 domain with fp32 statistics (an exponent reference on the raw
+// dot products, the scale folded into each exponent's FMA); P is rounded to
+// bf16 for the PV product.  The reference moves only when a row's maximum
+// exceeds it by more than 2^8, so O^T is rescaled (and a correction
+// exponential computed) only in the few steps where that happens.  Each step runs its two column tiles phase by phase (both QK
 // products, one mask branch, both softmaxes, one statistics branch, one
 // rescale test, both PV products), so one tile's products overlap the
 // other's exponentials: +4% at N = 16384-32768 over one tile at a time,
@@ -42,6 +43,7 @@ typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 constexpr int kWaves = 4;
 constexpr int kStage = 64;                    // keys per LDS stage
+constexpr float kLazy = 8.f;                  // reference slack, scaled log2 units
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -149,17 +151,28 @@ void prefill_attn_kernel(PrefillArgs a) {
   // the sum (of the same bf16-rounded P the numerator uses) lands in row 0 of
   // accL: item 0 of the lanes of group 0
   f32x4 accL[CQ];
-  float m_run[CQ];                            // running max of the raw dot products
-  // the window rows' normaliser is reported exact to fp32 (unrounded P), so
-  // the waves holding window rows also keep a vector-ALU sum
-  float l_part[CQ];
+  // The exponent reference of each row, on the raw dot products (the scale
+  // is positive): it moves only when a step's maximum exceeds it by more
+  // than kLazy in scaled log2 units, so P <= 2^kLazy (bf16 and the fp32
+  // accumulators keep the same relative precision at that size) and most
+  // steps need no correction exponential and no rescale of O^T.
+  float m_ref[CQ];
+  float m_thr[CQ];                            // m_ref + kLazy / scale: a step past it moves m_ref
+  float m_sc[CQ];                             // m_ref * scale (the exponents' offset)
+  // the window rows' statistics are reported exact to fp32 (unrounded P,
+  // true maximum), so the waves holding window rows also keep a vector-ALU
+  // sum and the true running maximum
+  float l_part[CQ], m_max[CQ];
 #pragma unroll
   for (int cq = 0; cq < CQ; ++cq) {
 #pragma unroll
     for (int n = 0; n < NC; ++n) accO[cq][n] = f32x4{0.f, 0.f, 0.f, 0.f};
     accL[cq] = f32x4{0.f, 0.f, 0.f, 0.f};
-    m_run[cq] = -INFINITY;
+    m_ref[cq] = -INFINITY;
+    m_thr[cq] = -INFINITY;
+    m_sc[cq] = -INFINITY;
     l_part[cq] = 0.f;
+    m_max[cq] = -INFINITY;
   }
   const uint32_t one2 = r16 == 0 ? 0x3F803F80u : 0u;          // two bf16 ones
   const u32x4 onesA = {one2, one2, one2, one2};
@@ -243,28 +256,47 @@ void prefill_attn_kernel(PrefillArgs a) {
             if (base + 8 * q4 + j > qi) S[cq][j >> 2][j & 3] = -INFINITY;
         }
       }
-      float corr[CQ];
+      // Each lane first compares the maximum of its own 8 keys with the
+      // reference; only when some lane exceeds it by more than kLazy (always
+      // on a row's first step: m_ref = -inf there, and every wave's first
+      // step holds key 0, which no query masks) does the wave take the row
+      // maxima over the 4 lane groups and move those rows' references.
+      float xm[CQ];
+      bool grow = false;
+#pragma unroll
+      for (int cq = 0; cq < CQ; ++cq) {
+        const f32x4 s0 = S[cq][0], s1 = S[cq][1];
+        xm[cq] = fmax2(fmax2(fmax2(s0[0], s0[1]), fmax2(s0[2], s0[3])),
+                       fmax2(fmax2(s1[0], s1[1]), fmax2(s1[2], s1[3])));
+        grow = grow || xm[cq] > m_thr[cq];
+      }
+      if (__builtin_amdgcn_ballot_w64(grow)) {                 // rare
+#pragma unroll
+        for (int cq = 0; cq < CQ; ++cq) {
+          const float mt = group_max(xm[cq]);
+          const float m_new = (mt - m_ref[cq]) * a.scale_log2 > kLazy ? mt : m_ref[cq];
+          // 2^((old - new) scale): exactly 1 where the reference stays, 0 on
+          // the first step
+          const float corr = __builtin_amdgcn_exp2f((m_ref[cq] - m_new) * a.scale_log2);
+#pragma unroll
+          for (int n = 0; n < NC; ++n)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) accO[cq][n][i] *= corr;
+          accL[cq][0] *= corr;
+          l_part[cq] *= corr;
+          m_ref[cq] = m_new;
+          m_sc[cq] = m_new * a.scale_log2;
+          m_thr[cq] = m_new + kLazy / a.scale_log2;
+        }
+      }
       float p[CQ][8];
 #pragma unroll
       for (int cq = 0; cq < CQ; ++cq) {
-        float s[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) s[j] = S[cq][j >> 2][j & 3];
-        float mt = fmax2(fmax2(fmax2(s[0], s[1]), fmax2(s[2], s[3])),
-                         fmax2(fmax2(s[4], s[5]), fmax2(s[6], s[7])));
-        mt = group_max(mt);
-        // the running max is kept on the raw dot products (the scale is
-        // positive) and the scale enters each exponent through one FMA;
-        // finite: every wave's first step holds key 0, which no query masks
-        const float m_new = fmax2(m_run[cq], mt);
-        const float mc = m_new * a.scale_log2;
-        // 1 when the max did not move; 0 on the first step (m_run = -inf)
-        corr[cq] = __builtin_amdgcn_exp2f((m_run[cq] - m_new) * a.scale_log2);
-        m_run[cq] = m_new;
+        const float mc = m_sc[cq];
         // hardware exp2: results below 2^-126 flush to zero, far below a
-        // softmax term that can matter next to the row max's term of 1
+        // softmax term that can matter next to the reference's term
 #pragma unroll
-        for (int j = 0; j < 8; ++j) p[cq][j] = __builtin_amdgcn_exp2f(fmaf(s[j], a.scale_log2, -mc));
+        for (int j = 0; j < 8; ++j) p[cq][j] = __builtin_amdgcn_exp2f(fmaf(S[cq][j >> 2][j & 3], a.scale_log2, -mc));
       }
       if (stats_wave) {                                       // wave-uniform
 #pragma unroll
@@ -272,7 +304,8 @@ void prefill_attn_kernel(PrefillArgs a) {
           float psum = 0.f;
 #pragma unroll
           for (int j = 0; j < 8; ++j) psum += p[cq][j];
-          l_part[cq] = l_part[cq] * corr[cq] + psum;
+          l_part[cq] += psum;
+          m_max[cq] = fmax2(m_max[cq], group_max(xm[cq]));
         }
       }
       bf16x8 pB[CQ];
@@ -280,21 +313,6 @@ void prefill_attn_kernel(PrefillArgs a) {
       for (int cq = 0; cq < CQ; ++cq)
 #pragma unroll
         for (int j = 0; j < 8; ++j) pB[cq][j] = static_cast<__bf16>(p[cq][j]);
-      // rescaling by exactly 1 changes nothing: skip it unless some lane's max
-      // moved in some tile (the tiles whose max stayed are multiplied by 1)
-      bool moved = false;
-#pragma unroll
-      for (int cq = 0; cq < CQ; ++cq) moved = moved || corr[cq] != 1.f;
-      if (__builtin_amdgcn_ballot_w64(moved)) {
-#pragma unroll
-        for (int cq = 0; cq < CQ; ++cq) {
-#pragma unroll
-          for (int n = 0; n < NC; ++n)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) accO[cq][n][i] *= corr[cq];
-          accL[cq][0] *= corr[cq];
-        }
-      }
 #pragma unroll
       for (int cq = 0; cq < CQ; ++cq) {
         accL[cq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(onesA), pB[cq], accL[cq], 0, 0, 0);
@@ -334,6 +352,7 @@ void prefill_attn_kernel(PrefillArgs a) {
     if (stats_wave) {
       z = l_part[cq] + __shfl_xor(l_part[cq], 16);
       z += __shfl_xor(z, 32);
+      z *= __builtin_amdgcn_exp2f((m_ref[cq] - m_max[cq]) * a.scale_log2);   // to the true maximum
     }
     const int qi = row0 + 16 * cq + r16;
     if (qi < L) {
@@ -348,7 +367,7 @@ void prefill_attn_kernel(PrefillArgs a) {
       // window rows: row max (natural-log units) and normaliser of the softmax
       if (stats_wave && q4 == 0 && qi >= L - a.w) {
         float* ws = a.window_stats + ((static_cast<size_t>(b) * a.Hq + h) * a.w + (qi - (L - a.w))) * 2;
-        ws[0] = m_run[cq] * a.scale_log2 * 0.69314718055994531f;   // raw max -> natural units
+        ws[0] = m_max[cq] * a.scale_log2 * 0.69314718055994531f;   // raw max -> natural units
         ws[1] = z;
       }
     }
