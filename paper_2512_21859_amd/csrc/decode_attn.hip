@@ -57,6 +57,7 @@ typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 constexpr int kVT = kVTile;           // rows per cache tile (32)
+constexpr float kLazy = 8.f;          // slack of the bf16 kernel's exponent reference (log2 units)
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 
@@ -187,7 +188,14 @@ void decode_mfma_kernel(DecodeArgs a) {
   f32x4 accO[NC];
 #pragma unroll
   for (int n = 0; n < NC; ++n) accO[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY;   // running max of head r16 (same in the 4 lane groups)
+  // Exponent reference of head r16 (same in the 4 lane groups), kept on the
+  // raw dot products (the scale is positive and enters each exponent through
+  // one FMA): it moves only when a tile's maximum passes it by more than
+  // kLazy scaled log2 units, so p <= 2^kLazy and most tiles need no rescale
+  // of O^T.
+  float m_run = -INFINITY;
+  float m_thr = -INFINITY;   // m_run + kLazy / scale
+  float m_sc = -INFINITY;    // m_run * scale, the partial's reference (log2 units)
   float l_part = 0.f;        // this lane's share of the running sum of head r16
 
   for (int t = t_first; t < t_end; t += WAVES) {
@@ -230,26 +238,40 @@ void decode_mfma_kernel(DecodeArgs a) {
     }
     float s[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) s[j] = S[j >> 2][j & 3] * a.scale_log2;
+    for (int j = 0; j < 8; ++j) s[j] = S[j >> 2][j & 3];
     if (tail) {
 #pragma unroll
       for (int j = 0; j < 8; ++j)
         if (base + 8 * q4 + j >= N) s[j] = -INFINITY;
     }
-    float mt = s[0];
+    float xm = s[0];
 #pragma unroll
-    for (int j = 1; j < 8; ++j) mt = fmaxf(mt, s[j]);
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    // m_new is finite: every tile visited has at least one valid key (base < N)
-    const float corr = exp2f(m_run - m_new);
-    m_run = m_new;
+    for (int j = 1; j < 8; ++j) xm = fmaxf(xm, s[j]);
+    // rare (always on a head's first tile): some lane's keys pass the
+    // threshold; the head's maximum over the 4 lane groups becomes the
+    // reference and O^T and the sum are rescaled by 2^(old - new)
+    if (__builtin_amdgcn_ballot_w64(xm > m_thr)) {
+      float mt = fmaxf(xm, __shfl_xor(xm, 16));
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      // finite: every tile visited has at least one valid key (base < N)
+      const float m_new = mt > m_thr ? mt : m_run;
+      const float sc_new = m_new * a.scale_log2;
+      const float corr = __builtin_amdgcn_exp2f(m_sc - sc_new);
+      l_part *= corr;
+#pragma unroll
+      for (int n = 0; n < NC; ++n)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) accO[n][i] *= corr;
+      m_run = m_new;
+      m_sc = sc_new;
+      m_thr = m_new + kLazy / a.scale_log2;
+    }
+    // hardware exp2 (results below 2^-126 of the reference flush to zero)
     float p[8];
     float psum = 0.f;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) { p[j] = exp2f(s[j] - m_new); psum += p[j]; }
-    l_part = l_part * corr + psum;
+    for (int j = 0; j < 8; ++j) { p[j] = __builtin_amdgcn_exp2f(fmaf(s[j], a.scale_log2, -m_sc)); psum += p[j]; }
+    l_part += psum;
     bf16x8 pB;
 #pragma unroll
     for (int j = 0; j < 8; ++j) pB[j] = static_cast<__bf16>(p[j]);
@@ -286,11 +308,8 @@ void decode_mfma_kernel(DecodeArgs a) {
       }
     }
 #pragma unroll
-    for (int n = 0; n < NC; ++n) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) accO[n][i] *= corr;
+    for (int n = 0; n < NC; ++n)
       accO[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(cv[n]), pB, accO[n], 0, 0, 0);
-    }
   }
 
   // ---- merge the lane groups' sums, then the waves, into this block's partial
@@ -305,7 +324,7 @@ void decode_mfma_kernel(DecodeArgs a) {
       for (int n = 0; n < NC; ++n)
         *reinterpret_cast<float4*>(part + r16 * (D + 4) + 16 * n + 4 * q4) =
             make_float4(accO[n][0], accO[n][1], accO[n][2], accO[n][3]);
-      if (q4 == 0) *reinterpret_cast<float2*>(part + r16 * (D + 4) + D) = make_float2(m_run, l_tot);
+      if (q4 == 0) *reinterpret_cast<float2*>(part + r16 * (D + 4) + D) = make_float2(m_sc, l_tot);
     }
     if (c == 0 && g == 0 && tid == 0) a.seq_len[b] = N;
     return;
@@ -319,7 +338,7 @@ void decode_mfma_kernel(DecodeArgs a) {
     for (int n = 0; n < NC; ++n)
       s_o(wave, r16, 4 * n + q4) = make_float4(accO[n][0], accO[n][1], accO[n][2], accO[n][3]);
   }
-  if (q4 == 0) { s_ml[wave][r16][0] = m_run; s_ml[wave][r16][1] = l_tot; }
+  if (q4 == 0) { s_ml[wave][r16][0] = m_sc; s_ml[wave][r16][1] = l_tot; }
   __syncthreads();
 
   for (int idx = tid; idx < G * (D / 4); idx += 64 * WAVES) {
