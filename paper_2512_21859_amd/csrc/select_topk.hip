@@ -113,6 +113,12 @@ __device__ __forceinline__ void for_each_key(int n, Load load, F f) {
   }
 }
 
+// LDS slot of prefix key j (of the cached prefix or of an emit tile): the low
+// 4 bits are XORed with bits 6..9, so the emit's reads (thread t takes keys
+// 16 t .. 16 t + 15) hit 64 different banks across a wave, while the
+// counting passes' reads (64 consecutive keys per wave) stay conflict-free.
+__device__ __forceinline__ int kslot(int j) { return j ^ ((j >> 6) & 15); }
+
 template <bool CACHED>
 __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
   const int g = blockIdx.x, b = blockIdx.y;
@@ -140,10 +146,10 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
 
   // 0. key range (and the LDS copy of the prefix)
   const auto from_hbm = [&](int j) { return key_of(sc[j]); };
-  const auto from_lds = [&](int j) { return s_keys[j]; };
+  const auto from_lds = [&](int j) { return s_keys[kslot(j)]; };
   uint32_t kmax = 0u, kmin = 0xffffffffu;
   for_each_key(pref, from_hbm, [&](int j, uint32_t k) {
-    if (CACHED) s_keys[j] = k;
+    if (CACHED) s_keys[kslot(j)] = k;
     kmax = max(kmax, k);
     kmin = min(kmin, k);
   });
@@ -198,7 +204,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
     const uint32_t* tk = s_keys + (CACHED ? base : 0);
     if (!CACHED) {
       for_each_key(min(kTileN, pref - base), [&](int i) { return key_of(sc[base + i]); },
-                   [&](int i, uint32_t k) { s_keys[i] = k; });
+                   [&](int i, uint32_t k) { s_keys[kslot(i)] = k; });
       __syncthreads();
     }
     const int j0 = base + tid * kPer;
@@ -207,7 +213,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
     for (int q = 0; q < kPer; ++q) {
       const int j = j0 + q;
       const bool in = j < pref;
-      kk[q] = in ? tk[tid * kPer + q] : 0u;
+      kk[q] = in ? tk[kslot(tid * kPer + q)] : 0u;
       gt += (in && kk[q] > tau) ? 1u : 0u;
       eq += (in && kk[q] == tau) ? 1u : 0u;
     }
