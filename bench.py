@@ -7,8 +7,10 @@ Headline workload: a 28-layer stack with the Qwen2.5-7B attention shape
 128 decode tokens per ratio.  Inputs are seeded synthetic tensors already
 resident in HBM when timing starts.
 
-One step = for every alpha: evict every layer (score the window, select,
-compact: once per request, as after a prefill), then 128 decode tokens, one
+One step = for every alpha: evict every layer (score each layer's window,
+then select and compact all 28 layers in one call each, the layers stacked
+on the batch axis: once per request, as after a prefill), then 128 decode
+tokens, one
 token being the decode step (append + attention) of all 28 layers in order,
 replayed from a HIP graph captured once per ratio.  The metric is decode
 tokens per second over the whole step (eviction included); per-ratio rows
@@ -550,30 +552,40 @@ LLC_BYTES = 256 << 20      # MI355X last-level (Infinity) cache
 def headline(torch, _lib, synth, Evictor, dev, steps, warmup, tokens=None):
     """The 28-layer L = 32768 sweep (module docstring).  Returns the headline
     fields of the JSON line."""
+    from paper_2512_21859_amd.pipeline import StackEvictor
     wl = synth.WORKLOADS[3]
     T, nl = (wl.T if tokens is None else tokens), wl.layers
     B, Hq, Hkv, d, w, L = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L
-    lay = []
+    # the layers' prompt tensors and caches are stacked layer-major on the
+    # batch axis ([nl * B, ...]); each layer's entries are views of its rows
+    stack = {}
+    lay = [dict() for _ in range(nl)]
     for layer in range(nl):
         pr = synth.make_prompt(wl, layer)
         dc = synth.make_decode(wl, layer, T=T)
-        lay.append({x: pr[x].to(dev) for x in ("q_win", "k", "v")})
-        lay[-1].update({x: dc[x].to(dev) for x in ("q", "k_new", "v_new")})
+        for x in ("q_win", "k", "v"):
+            if x not in stack:
+                stack[x] = torch.empty((nl * B,) + tuple(pr[x].shape[1:]), dtype=pr[x].dtype,
+                                       device=dev)
+            stack[x][layer * B:(layer + 1) * B].copy_(pr[x])
+            lay[layer][x] = stack[x][layer * B:(layer + 1) * B]
+        lay[layer].update({x: dc[x].to(dev) for x in ("q", "k_new", "v_new")})
         del pr, dc
     ev = Evictor(B, L, Hq, Hkv, d, w, wl.pool, device=dev)
+    sev = StackEvictor(nl, B, L, Hq, Hkv, d, w, wl.pool, device=dev)
     stream = torch.cuda.current_stream()
     alphas = list(wl.alphas)
     n_keep = {a: _lib.tb_keep_count(L, a, w) for a in alphas}
-    caches = {a: [_lib.KVCache(B, Hq, Hkv, n_keep[a] + T, d, wl.dtype, device=dev)
-                  for _ in range(nl)] for a in alphas}
+    caches = {a: _lib.KVCache(nl * B, Hq, Hkv, n_keep[a] + T, d, wl.dtype, device=dev)
+              for a in alphas}
     out = torch.empty((T, nl, B, Hq, d), dtype=wl.dtype, device=dev)
 
     def evict_all(a):
-        # one stream for everything: spreading the layers' evictions over side
+        # every layer scored on its own, then one selection and one compaction
+        # for the stack (a layer's selection alone keeps Hkv CUs busy); one
+        # stream for everything: spreading the layers' evictions over side
         # streams measured slower (every later decode dispatch slowed down)
-        for layer in range(nl):
-            x = lay[layer]
-            ev.evict(x["q_win"], x["k"], x["v"], [L], [a], caches[a][layer], stream)
+        sev.evict(stack["q_win"], stack["k"], stack["v"], [L] * B, [a] * B, caches[a], stream)
 
     # one graph per ratio: T tokens x 28 layers of decode calls (lengths live on
     # the device, so every replay after an eviction starts from n_keep)
@@ -584,11 +596,12 @@ def headline(torch, _lib, synth, Evictor, dev, steps, warmup, tokens=None):
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=cap_stream):
+            c = caches[a]
             for t in range(T):
                 for layer in range(nl):
-                    x, c = lay[layer], caches[a][layer]
-                    _lib.tb_decode_attn(x["q"][t], x["k_new"][t], x["v_new"][t], c.k, c.v,
-                                        c.kv_len, out[t, layer], c.ws, stream=cap_stream)
+                    x, r = lay[layer], slice(layer * B, (layer + 1) * B)
+                    _lib.tb_decode_attn(x["q"][t], x["k_new"][t], x["v_new"][t], c.k[r], c.v[r],
+                                        c.kv_len[r], out[t, layer], c.ws, stream=cap_stream)
         graphs[a] = g
     torch.cuda.synchronize()
 
@@ -654,7 +667,9 @@ def headline(torch, _lib, synth, Evictor, dev, steps, warmup, tokens=None):
     # eviction stages of one layer at ratio 0.5 (scores do not depend on the ratio)
     a = 0.5
     nk = n_keep[a]
-    x, c = lay[0], caches[a][0]
+    x = lay[0]
+    c = _lib.KVCache(B, Hq, Hkv, nk + T, d, wl.dtype, device=dev)
+    ev.evict(x["q_win"], x["k"], x["v"], [L], [a], c, stream)
     sc_t = _best_ms(torch, lambda: ev.score(x["q_win"], x["k"], [L], stream))
     se_t = _best_ms(torch, lambda: ev.select([L], [a], stream))
     co_t = _best_ms(torch, lambda: c.compact_from(x["k"], x["v"], ev.keep_idx, [nk], stream))
@@ -677,7 +692,7 @@ def headline(torch, _lib, synth, Evictor, dev, steps, warmup, tokens=None):
     tokens = n_al * T * steps
     calls = hbm_calls
     achieved = hbm_bytes / (hbm_ms * 1e-3) / 1e9
-    del graphs, caches, lay, ev, out
+    del graphs, caches, lay, stack, ev, sev, c, out
     torch.cuda.empty_cache()
     return {
         "value": round(tokens / (total_ms * 1e-3), 1),

@@ -17,6 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtimebill.so")
 
 TB_OK, TB_EINVAL, TB_EUNSUPPORTED, TB_EWORKSPACE, TB_EHIP, TB_EINTERNAL = range(6)
+MAX_B = 64          # sequences per call (include/timebill.h: B <= 64)
 TB_F32, TB_BF16 = 0, 1
 TB_OP_SCORE, TB_OP_SELECT, TB_OP_COMPACT, TB_OP_DECODE, TB_OP_H2O = range(5)
 V_TILE = 32          # rows per tile (and per page) of the compact caches; cap is a multiple

@@ -50,12 +50,16 @@ class Evictor:
         self.sel_ws = torch.empty((sel,), dtype=torch.uint8, device=device) if sel else None
 
     def score(self, q_win: torch.Tensor, k: torch.Tensor, L: Sequence[int], stream=None) -> None:
+        self.score_into(q_win, k, L, self.scores, self.raw, stream)
+
+    def score_into(self, q_win, k, L, scores, raw=None, stream=None) -> None:
+        """score() into caller-given [B, Hkv, Lmax] scores (and raw scores)."""
         if self.scorer == "knorm":
-            _lib.tb_score_knorm(k, L, self.w, self.scores, stream)
+            _lib.tb_score_knorm(k, L, self.w, scores, stream)
         elif self.scorer == "h2o":
-            _lib.tb_score_h2o(q_win, k, L, self.scores, self.ws, stream)
+            _lib.tb_score_h2o(q_win, k, L, scores, self.ws, stream)
         else:
-            _lib.tb_score_window(q_win, k, L, self.w, self.pool, self.scores, self.raw, self.ws,
+            _lib.tb_score_window(q_win, k, L, self.w, self.pool, scores, raw, self.ws,
                                  stream, avgpool=self.scorer == "snapkv_avg")
 
     def select(self, L: Sequence[int], alphas: Sequence[float], stream=None):
@@ -66,6 +70,49 @@ class Evictor:
         """Score, select and compact into ``cache``; returns n_keep per sequence."""
         self.score(q_win, k, L, stream)
         n_keep = self.select(L, alphas, stream)
+        cache.compact_from(k, v, self.keep_idx, n_keep, stream)
+        return n_keep
+
+
+class StackEvictor:
+    """Eviction of a stack of layers of one shape, laid out layer-major on the
+    batch axis: sequence b of layer l is row l * B + b of every [layers * B,
+    ...] tensor.  Each layer is scored on its own (one layer's scoring
+    workspace, whose exponentials stay in the last-level cache), then one
+    selection and one compaction cover the whole stack: at B = 1 and 4 KV
+    heads a selection of one layer keeps 4 CUs busy, the stack's keeps
+    4 * layers.  Layer by layer the results equal those of an Evictor.
+    layers * B may not exceed the library's batch limit (64)."""
+
+    def __init__(self, layers: int, B: int, Lmax: int, Hq: int, Hkv: int, d: int, w: int,
+                 pool: int, device="cuda", scorer: str = "snapkv"):
+        if layers < 1 or layers * B > _lib.MAX_B:
+            raise ValueError(f"need 1 <= layers and layers * B <= {_lib.MAX_B}")
+        self.layers, self.B = layers, B
+        self.layer = Evictor(B, Lmax, Hq, Hkv, d, w, pool, device=device, scorer=scorer)
+        NB = layers * B
+        self.scores = torch.empty((NB, Hkv, Lmax), dtype=torch.float32, device=device)
+        self.keep_idx = torch.empty((NB, Hkv, Lmax), dtype=torch.int32, device=device)
+        sel = _lib.tb_workspace_bytes(_lib.TB_OP_SELECT, NB, Lmax, Hq, Hkv, d, w, 0)
+        self.sel_ws = torch.empty((sel,), dtype=torch.uint8, device=device) if sel else None
+
+    def evict(self, q_win, k, v, L: Sequence[int], alphas: Sequence[float],
+              cache: "_lib.KVCache", stream=None) -> List[int]:
+        """q_win [layers*B, Hq, w, d] (or the prefill's queries for h2o), k, v
+        [layers*B, Hkv, Lmax, d]; L and alphas per sequence (B values, the
+        same for every layer); cache has batch layers*B.  Returns n_keep per
+        row of the stack."""
+        B, NB = self.B, self.layers * self.B
+        if k.shape[0] != NB or v.shape[0] != NB or q_win.shape[0] != NB:
+            raise ValueError("q_win, k and v must hold layers * B sequences")
+        if len(L) != B or len(alphas) != B:
+            raise ValueError("L and alphas take one value per sequence of a layer")
+        for l in range(self.layers):
+            s = slice(l * B, (l + 1) * B)
+            self.layer.score_into(q_win[s], k[s], L, self.scores[s], None, stream)
+        Ls, als = list(L) * self.layers, list(alphas) * self.layers
+        n_keep = _lib.tb_select_topk(self.scores, Ls, self.layer.w, als, self.keep_idx,
+                                     self.sel_ws, stream)
         cache.compact_from(k, v, self.keep_idx, n_keep, stream)
         return n_keep
 
