@@ -257,11 +257,24 @@ __global__ __launch_bounds__(kThreads) void row_stats_kernel(ScoreArgs a) {
   const int nt = (a.L[b] + kT - 1) / kT;
   const size_t rowo = (static_cast<size_t>(bg) * a.R + r) * a.n_tiles;
   double M = -INFINITY, Z = 0.0;
-  for (int t = lane; t < nt; t += 64) {
-    const double m = a.tile_m[rowo + t], z = a.tile_z[rowo + t];
-    if (m == -INFINITY) continue;
-    if (m > M) { Z = Z * exp(M - m) + z; M = m; }
-    else       { Z += z * exp(m - M); }
+  // the lane's tiles t = lane, lane + 64, ... in that order, their loads
+  // issued 8 at a time ahead of the merge (one memory round trip per 8)
+  constexpr int kAhead = 8;
+  for (int t0 = lane; t0 < nt; t0 += 64 * kAhead) {
+    double mv[kAhead], zv[kAhead];
+#pragma unroll
+    for (int k = 0; k < kAhead; ++k) {
+      const int t = min(t0 + 64 * k, nt - 1);
+      mv[k] = a.tile_m[rowo + t];
+      zv[k] = a.tile_z[rowo + t];
+    }
+#pragma unroll
+    for (int k = 0; k < kAhead; ++k) {
+      const double m = mv[k], z = zv[k];
+      if (t0 + 64 * k >= nt || m == -INFINITY) continue;
+      if (m > M) { Z = Z * exp(M - m) + z; M = m; }
+      else       { Z += z * exp(m - M); }
+    }
   }
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
