@@ -674,6 +674,16 @@ def headline(torch, _lib, synth, Evictor, dev, steps, warmup, tokens=None):
     se_t = _best_ms(torch, lambda: ev.select([L], [a], stream))
     co_t = _best_ms(torch, lambda: c.compact_from(x["k"], x["v"], ev.keep_idx, [nk], stream))
     cbytes = 2 * 2 * Hkv * nk * d * 2
+    # the stack's compaction (all layers in one call, as evict_all runs it)
+    evict_all(a)
+    cs_t = _best_ms(torch, lambda: caches[a].compact_from(stack["k"], stack["v"], sev.keep_idx,
+                                                          [nk] * (nl * B), stream))
+    stack_compaction = {"alpha": a, "layers": nl, "us": round(cs_t * 1e3, 1),
+                        "bytes": cbytes * nl,
+                        "GBps": round(cbytes * nl / (cs_t * 1e-3) / 1e9, 1),
+                        "frac_of_8TBps": round(cbytes * nl / (cs_t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                        "timing": "best of 3, HIP events around one tb_compact_kv call over the "
+                                  f"{nl}-layer stack"}
     stages = {"alpha": a, "score_us": round(sc_t * 1e3, 1), "select_us": round(se_t * 1e3, 1),
               "compact_us": round(co_t * 1e3, 1),
               "compaction_bytes": cbytes,
@@ -733,6 +743,7 @@ def headline(torch, _lib, synth, Evictor, dev, steps, warmup, tokens=None):
         "per_alpha_timing": "median over the timed steps (p10, p90 beside it) of HIP events "
                             "around each ratio's 28 evictions and its graph of decode calls",
         "evict_one_layer": stages,
+        "stack_compaction": stack_compaction,
         "token_time_fit": {"p_us_per_kv_row": p, "q_us": q,
                            "r2": 1 - ss_res / ss_tot if ss_tot > 0 else 1.0,
                            "mape_pct": 100.0 * sum(abs(f - y) / y for y, f in zip(ys, pred)) / len(ys),
