@@ -41,6 +41,11 @@ def _run(wl, L, w=0):
     (64, 8, 2, [1, 64, 200], 1),
     (128, 7, 1, [1000], 64),
     (64, 16, 2, [777, 2049], 32),      # d = 64 over many blocks, ragged tails
+    # KV-head counts that do not divide the 8 XCDs of the block order, and
+    # (tile, batch, KV head) unit counts that are not whole XCD rounds
+    (128, 9, 3, [700, 1500, 33], 32),
+    (64, 10, 5, [1200, 513], 16),
+    (128, 16, 8, [1025], 32),
 ])
 def test_prefill_matches_oracle(d, Hq, Hkv, L, w):
     case(f"prefill d={d} Hq={Hq} Hkv={Hkv} L={L} w={w}")
