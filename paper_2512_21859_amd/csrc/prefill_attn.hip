@@ -391,15 +391,9 @@ void prefill_attn_kernel(PrefillArgs a) {
 
 }  // namespace
 
-hipError_t launch_prefill(const PrefillArgs& a, int d, hipStream_t st) {
-  // two column tiles per wave (244 VGPRs, two waves per SIMD; 64 KB of LDS
-  // per block at d = 128, so two blocks per CU); three or four tiles cut the
-  // LDS operand reads per product but need one wave per SIMD, and measured
-  // slower (530 and 462 against 900 TFLOP/s at N = 32768)
-  constexpr int CQ = 2;
+template <int CQ>
+hipError_t launch_prefill_cq(const PrefillArgs& a, int d, int lmax, hipStream_t st) {
   constexpr int rows = kWaves * 16 * CQ;
-  int lmax = 0;
-  for (int b = 0; b < a.B; ++b) lmax = max(lmax, a.L[b]);
   // units of (query tile rank, batch, KV head), padded to whole rounds of
   // the 8 XCDs, times the G query heads of each
   const int units = ((lmax + rows - 1) / rows) * a.B * a.Hkv;
@@ -407,6 +401,22 @@ hipError_t launch_prefill(const PrefillArgs& a, int d, hipStream_t st) {
   if (d == 128) prefill_attn_kernel<128, CQ><<<grid, 64 * kWaves, 0, st>>>(a);
   else          prefill_attn_kernel<64, CQ><<<grid, 64 * kWaves, 0, st>>>(a);
   return hipGetLastError();
+}
+
+hipError_t launch_prefill(const PrefillArgs& a, int d, hipStream_t st) {
+  // two column tiles per wave (244 VGPRs, two waves per SIMD; 64 KB of LDS
+  // per block at d = 128, so two blocks per CU); three or four tiles cut the
+  // LDS operand reads per product but need one wave per SIMD, and measured
+  // slower (530 and 462 against 900 TFLOP/s at N = 32768)
+  // Prompts of up to 1024 tokens take one column tile per wave (64-row
+  // blocks): twice the blocks, half the serial work of the heaviest query
+  // tile, for a launch that does not fill the CUs (224 blocks of 128 rows at
+  // N = 1024, 28 query heads): 49 -> 58 TFLOP/s at N = 256, 124 -> 144 at
+  // 512, 284 -> 301 at 1024; at 2048 it lost 7%, at 4096 27%.
+  int lmax = 0;
+  for (int b = 0; b < a.B; ++b) lmax = max(lmax, a.L[b]);
+  if (lmax <= 1024) return launch_prefill_cq<1>(a, d, lmax, st);
+  return launch_prefill_cq<2>(a, d, lmax, st);
 }
 
 }  // namespace tb
