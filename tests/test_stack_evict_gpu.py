@@ -2,7 +2,7 @@
 one by one, then selected and compacted in one call each.  Every layer must
 get exactly what the per-layer Evictor gives it: the same keep counts, kept
 positions, compacted cache rows and lengths, for ragged batches, per-sequence
-ratios and the window, averaged-window and key-norm scorers; a decode step
+ratios and every scorer (window, averaged window, key norm, H2O); a decode step
 over a layer's rows of the stacked cache must equal the decode over that
 layer's own cache, bit for bit."""
 import pytest
@@ -81,3 +81,34 @@ def test_stack_rejects_bad_shapes():
     cache = _lib.KVCache(2, 4, 2, 256, 64, torch.bfloat16)
     with pytest.raises(ValueError):
         sev.evict(q, k, k, [256], [0.5], cache)
+
+
+def test_stack_equals_per_layer_h2o():
+    """H2O takes every prompt query (q [layers*B, Hq, Lmax, d]) in place of
+    the window queries; the stacked eviction must still equal the per-layer
+    one, layer by layer."""
+    layers, L, alphas = 3, [900, 640], [0.5, 0.25]
+    B, Hq, Hkv, d, w, pool, T = len(L), 8, 2, 128, 32, 1, 2
+    case(f"{layers} layers, L={L}, alphas={alphas}, scorer=h2o")
+    wl = synth.custom(2400, torch.bfloat16, B, L, Hq, Hkv, d, w, pool, T)
+    Lmax = max(L)
+    prompts = [synth.make_prompt(wl, layer, L) for layer in range(layers)]
+    q = torch.cat([synth.make_queries(wl, layer, L) for layer in range(layers)]).to(DEV)
+    k = torch.cat([p["k"] for p in prompts]).to(DEV)
+    v = torch.cat([p["v"] for p in prompts]).to(DEV)
+    n_keep = [_lib.tb_keep_count(L[b], alphas[b], w) for b in range(B)]
+    cap = max(n_keep) + T
+    sev = StackEvictor(layers, B, Lmax, Hq, Hkv, d, w, pool, scorer="h2o")
+    cs = _lib.KVCache(layers * B, Hq, Hkv, cap, d, wl.dtype)
+    assert sev.evict(q, k, v, L, alphas, cs) == n_keep * layers
+    ev = Evictor(B, Lmax, Hq, Hkv, d, w, pool, scorer="h2o")
+    for layer in range(layers):
+        r = slice(layer * B, (layer + 1) * B)
+        cl = _lib.KVCache(B, Hq, Hkv, cap, d, wl.dtype)
+        assert ev.evict(q[r], k[r], v[r], L, alphas, cl) == n_keep
+        torch.cuda.synchronize()
+        for b in range(B):
+            n = n_keep[b]
+            assert torch.equal(sev.keep_idx[layer * B + b, :, :n - w], ev.keep_idx[b, :, :n - w])
+            assert torch.equal(cs.k[layer * B + b, :, :n], cl.k[b, :, :n])
+            assert torch.equal(cs.v[layer * B + b, :, :n], cl.v[b, :, :n])
