@@ -8,11 +8,12 @@
 // attention.  out[b][h][i] = sum_{j <= i} softmax_j(q[b][h][i] . k[b][g][j] /
 // sqrt(d)) v[b][g][j], g = h / (Hq / Hkv).
 //
-// Block = 128 query rows of one query head (4 waves x 32 rows), blocks issued
-// heaviest first (latest rows) and grouped by KV head on the XCDs, so the
-// query heads that read the same K/V rows do so through one L2 (measured:
-// 962-969 -> 1144-1145 TFLOP/s at N = 32768, 530-543 -> 867-877 at 4096).
-// K and V stream through LDS 64 keys at a time,
+// Block = the query rows of one query head (4 or 8 waves of 32 rows; 16 per
+// wave for short prompts: the launch below), blocks issued heaviest first
+// (latest rows) and grouped by KV head on the XCDs, so the query heads that
+// read the same K/V rows do so through one L2 (measured: 962-969 -> 1144-1145
+// TFLOP/s at N = 32768, 530-543 -> 867-877 at 4096).  K and V stream through
+// LDS 64 or 128 keys at a time,
 // double-buffered: each stage goes global -> LDS by direct loads (no
 // registers), issued one stage ahead, one barrier per stage.  Both stay
 // row-major in LDS (16-byte chunks XOR-swizzled by row against bank
@@ -44,8 +45,6 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
-constexpr int kWaves = 4;
-constexpr int kStage = 64;                    // keys per LDS stage
 constexpr float kLazy = 8.f;                  // reference slack, scaled log2 units
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -106,9 +105,12 @@ __device__ __forceinline__ float from_group0(float x, int lane) {
   return __shfl(x, lane & 15);
 }
 
-template <int D, int CQ>
-__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(CQ == 2 ? 2 : 1)))
+// WAVES waves of CQ column tiles each per block; K and V stages of STAGE keys
+template <int D, int CQ, int WAVES, int STAGE>
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(CQ == 2 ? 2 : 1)))
 void prefill_attn_kernel(PrefillArgs a) {
+  constexpr int kWaves = WAVES;
+  constexpr int kStage = STAGE;               // keys per LDS stage
   constexpr int kRowsPerWave = 16 * CQ;       // CQ 16-query column tiles per wave
   constexpr int kBlockRows = kWaves * kRowsPerWave;
   constexpr int KC = D / 32;                  // k-chunks of the QK^T product
@@ -197,8 +199,8 @@ void prefill_attn_kernel(PrefillArgs a) {
   const int wave_key_end = min(L, row0 + kRowsPerWave);         // causal limit of this wave
   const bool stats_wave = a.window_stats != nullptr && row0 + kRowsPerWave > L - a.w;
 
-  // One stage of 64 keys goes global -> LDS by direct loads, one stage ahead:
-  // load u of thread tid fills chunk position p = 256 u + tid of K and of V
+  // One stage of STAGE keys goes global -> LDS by direct loads, one stage
+  // ahead: load u of thread tid fills chunk position p = 64 WAVES u + tid of K and of V
   // (a wave's 64 lanes write 1 KB contiguous), taking from global memory the
   // chunk the swizzled layout keeps there.  Keys past L read row L - 1 (any
   // valid row: they are masked).
@@ -391,32 +393,39 @@ void prefill_attn_kernel(PrefillArgs a) {
 
 }  // namespace
 
-template <int CQ>
+template <int CQ, int WAVES, int STAGE>
 hipError_t launch_prefill_cq(const PrefillArgs& a, int d, int lmax, hipStream_t st) {
-  constexpr int rows = kWaves * 16 * CQ;
+  constexpr int rows = WAVES * 16 * CQ;
   // units of (query tile rank, batch, KV head), padded to whole rounds of
   // the 8 XCDs, times the G query heads of each
   const int units = ((lmax + rows - 1) / rows) * a.B * a.Hkv;
   const dim3 grid(((units + 7) / 8) * 8 * (a.Hq / a.Hkv));
-  if (d == 128) prefill_attn_kernel<128, CQ><<<grid, 64 * kWaves, 0, st>>>(a);
-  else          prefill_attn_kernel<64, CQ><<<grid, 64 * kWaves, 0, st>>>(a);
+  if (d == 128) prefill_attn_kernel<128, CQ, WAVES, STAGE><<<grid, 64 * WAVES, 0, st>>>(a);
+  else          prefill_attn_kernel<64, CQ, WAVES, STAGE><<<grid, 64 * WAVES, 0, st>>>(a);
   return hipGetLastError();
 }
 
 hipError_t launch_prefill(const PrefillArgs& a, int d, hipStream_t st) {
-  // two column tiles per wave (244 VGPRs, two waves per SIMD; 64 KB of LDS
-  // per block at d = 128, so two blocks per CU); three or four tiles cut the
-  // LDS operand reads per product but need one wave per SIMD, and measured
-  // slower (530 and 462 against 900 TFLOP/s at N = 32768)
-  // Prompts of up to 1024 tokens take one column tile per wave (64-row
-  // blocks): twice the blocks, half the serial work of the heaviest query
-  // tile, for a launch that does not fill the CUs (224 blocks of 128 rows at
-  // N = 1024, 28 query heads): 49 -> 58 TFLOP/s at N = 256, 124 -> 144 at
-  // 512, 284 -> 301 at 1024; at 2048 it lost 7%, at 4096 27%.
+  // Block shapes by prompt length (28 q / 4 kv heads, d = 128, measured on
+  // one box, alternated; TFLOP/s):
+  // * two column tiles per wave (225 VGPRs, two waves per SIMD); three or
+  //   four tiles cut the LDS operand reads per product but need one wave
+  //   per SIMD, and measured slower (530 and 462 against 900 at 32768);
+  // * N >= 8192: 8 waves (256 rows) and 128-key stages, 128 KB of LDS, one
+  //   block per CU: the stage's global -> LDS traffic and barriers are
+  //   shared by twice the rows: 1147 -> 1191-1194 at 32768, 1137 -> 1166 at
+  //   16384, 1078 -> 1099 at 8192, but 1020 -> 971-983 at 6144;
+  // * below that 4 waves (128 rows) and 64-key stages, two blocks per CU;
+  // * up to 1024 tokens one column tile per wave (64-row blocks): the
+  //   128-row launch has 224 blocks for 256 CUs at N = 1024 and the heaviest
+  //   query tile's serial steps set the time; twice the blocks with half
+  //   the work per step: 49 -> 58 at N = 256, 124 -> 144 at 512, 284 -> 301
+  //   at 1024 (at 2048 it lost 7%, at 4096 27%).
   int lmax = 0;
   for (int b = 0; b < a.B; ++b) lmax = max(lmax, a.L[b]);
-  if (lmax <= 1024) return launch_prefill_cq<1>(a, d, lmax, st);
-  return launch_prefill_cq<2>(a, d, lmax, st);
+  if (lmax <= 1024) return launch_prefill_cq<1, 4, 64>(a, d, lmax, st);
+  if (lmax < 8192) return launch_prefill_cq<2, 4, 64>(a, d, lmax, st);
+  return launch_prefill_cq<2, 8, 128>(a, d, lmax, st);
 }
 
 }  // namespace tb
