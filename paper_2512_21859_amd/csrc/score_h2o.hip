@@ -114,9 +114,29 @@ __device__ __forceinline__ void tile_products(const float (*qs)[D + 1], const fl
   }
 }
 
+// Block order (one-dimensional grid): workgroup i runs on XCD i % 8, and
+// XCD x takes the units x, x + 8, ... of (tile pair, batch, KV head), the G
+// query heads of a unit in G consecutive slots of it, so the blocks that
+// stream one KV head's keys share that XCD's L2 (L = 8192, 28 q / 4 kv
+// heads: 9689-9709 -> 9621-9626 us per call; the passes are bound by the
+// float64 products).  False for the padding of the last round.
+__device__ __forceinline__ bool h2o_block(const H2oArgs& a, int& p, int& h, int& b) {
+  const int G = a.Hq / a.Hkv;
+  const int wg = static_cast<int>(blockIdx.x);
+  const int slot = wg >> 3, unit = (slot / G) * 8 + (wg & 7);
+  const int g = unit % a.Hkv, rb = unit / a.Hkv;
+  b = rb % a.B;
+  p = rb / a.B;
+  h = g * G + slot % G;
+  int nt_max = 0;
+  for (int bb = 0; bb < a.B; ++bb) nt_max = max(nt_max, (a.L[bb] + kTile - 1) / kTile);
+  return p < (nt_max + 1) / 2;
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, 2) void h2o_rows_kernel(H2oArgs a) {
-  const int p = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  int p, h, b;
+  if (!h2o_block(a, p, h, b)) return;
   const int L = a.L[b], nt = (L + kTile - 1) / kTile;
   const int G = a.Hq / a.Hkv, g = h / G;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -187,7 +207,8 @@ __global__ __launch_bounds__(kThreads, 2) void h2o_rows_kernel(H2oArgs a) {
 
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, 2) void h2o_cols_kernel(H2oArgs a) {
-  const int p = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  int p, h, b;
+  if (!h2o_block(a, p, h, b)) return;
   const int L = a.L[b], nt = (L + kTile - 1) / kTile;
   const int G = a.Hq / a.Hkv, g = h / G;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -267,7 +288,8 @@ template <typename T, int D>
 hipError_t launch_typed(const H2oArgs& a, hipStream_t st) {
   int nt_max = 0;
   for (int b = 0; b < a.B; ++b) nt_max = max(nt_max, (a.L[b] + kTile - 1) / kTile);
-  const dim3 grid((nt_max + 1) / 2, a.Hq, a.B);
+  const int units = (nt_max + 1) / 2 * a.B * a.Hkv;          // (tile pair, batch, KV head)
+  const dim3 grid(((units + 7) / 8) * 8 * (a.Hq / a.Hkv));
   h2o_rows_kernel<T, D><<<grid, kThreads, 0, st>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
