@@ -103,3 +103,31 @@ def test_prefill_full_size_sampled_rows():
     _lib.tb_prefill_attn(q.to(DEV), pr["k"].to(DEV), pr["v"].to(DEV), L, out2)
     torch.cuda.synchronize()
     assert torch.equal(out, out2)
+
+
+@pytest.mark.parametrize("d,Hq,Hkv,L,w", [
+    # longest prompt >= 8192: the 8-wave, 256-row blocks with 128-key stages;
+    # ragged batch, tails that are not whole blocks or stages, d = 64 and 128
+    (64, 8, 2, [8300, 1000, 4097], 32),
+    (128, 7, 1, [300, 8193], 64),
+    (128, 12, 3, [9001], 16),
+])
+def test_prefill_long_ragged_sampled_rows(d, Hq, Hkv, L, w):
+    case(f"prefill long ragged d={d} Hq={Hq} Hkv={Hkv} L={L} w={w}: sampled rows")
+    wl = synth.custom(4400 + d + Hq, torch.bfloat16, len(L), L, Hq, Hkv, d, w, 1, 1)
+    pr, q, out, ws = _run(wl, L, w)
+    got = f64(out)
+    wst = ws.cpu().numpy()
+    worst = 0.0
+    for b, n in enumerate(L):
+        rows = sorted({r for r in (0, 1, 63, 64, 127, 128, 255, 256, 257, 4095, 4096,
+                                   8063, 8191, 8192, n - 129, n - 128, n - w, n - 2, n - 1)
+                       if 0 <= r < n})
+        ref = O.prefill_attention(f64(q[b]), f64(pr["k"][b]), f64(pr["v"][b]), n, rows)
+        worst = max(worst, float(np.abs(got[b][:, rows] - ref).max()))
+        assert np.all(got[b, :, n:] == 3.0), "rows past L were written"
+        st = O.prefill_window_stats(f64(q[b]), f64(pr["k"][b]), n, w)
+        assert np.all(np.abs(wst[b, ..., 0] - st[..., 0]) <= 1e-5 * (1 + np.abs(st[..., 0])))
+        assert np.all(np.abs(wst[b, ..., 1] / st[..., 1] - 1) <= 1e-4)
+    print(f"max abs error over sampled rows {worst:.2e}", flush=True)
+    assert worst <= TOL

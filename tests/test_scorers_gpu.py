@@ -182,6 +182,8 @@ def _h2o_gpu(q, k, L):
     (torch.bfloat16, 128, 14, 2, [1000, 257]),
     (torch.float32, 64, 4, 2, [300]),
     (torch.bfloat16, 64, 3, 3, [37, 64, 65]),
+    # 5 KV heads x 2 sequences: units that are not whole rounds of the 8 XCDs
+    (torch.bfloat16, 128, 10, 5, [700, 1300]),
 ])
 def test_h2o_scores_and_selection(dtype, d, Hq, Hkv, L):
     case(f"h2o dtype={dtype} d={d} Hq={Hq} Hkv={Hkv} L={L}")
