@@ -27,6 +27,7 @@ struct ScoreArgs {
   int32_t B, Lmax, Hq, Hkv, w, pool, R, n_tiles, row_chunks;
   int32_t pool_avg;       // 0: max-pool, 1: mean over the window (zeros outside the prefix)
   int32_t stream_e;       // set by launch_score: e written with streaming stores
+  int32_t pack_pairs;     // set by launch_score: row pairs P of packed K1 blocks, 0 if unpacked
   double scale;           // 1/sqrt(d)
   int32_t L[kMaxB];
 };

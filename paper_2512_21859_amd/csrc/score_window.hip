@@ -11,7 +11,10 @@
 // Four kernels, all with fixed-order reductions (no atomics):
 //   K1 score_tiles: block = (64-key tile, <=256 window rows) of one KV head,
 //      512 threads; wave w owns 32 rows x the 64 keys (waves whose rows are all
-//      padding skip the products).  Window queries (as fp32) and keys (as
+//      padding skip the products).  With 4, 6 or 7 row pairs and enough
+//      blocks, a block instead takes 8 consecutive units (32 rows x one tile,
+//      numbered tile-major) over at most two tiles, so no wave idles.
+//      Window queries (as fp32) and keys (as
 //      float64, converted once since every wave reads them) are staged in LDS
 //      in 32-wide d chunks, the next chunk's global loads in flight while the
 //      current one is multiplied; the float64 dot products run on the matrix
@@ -101,30 +104,50 @@ __device__ __forceinline__ float row16_max_f32(float x) {
 constexpr int kTilesThreads = 512;
 constexpr int kWaveRows = 32;      // window rows per wave in score_tiles
 
-template <typename T, int D>
+// Work unit of a wave: 32 window rows x one 64-key tile.  NS = 1: block =
+// (tile, 256-row chunk), wave w takes rows 32 w .. 32 w + 31 (waves past R
+// idle).  NS = 2 (R <= 256 with P = ceil(R / 32) row pairs, P in {4, 6, 7}):
+// the units are numbered tile-major, u = P t + p, and block j takes units
+// 8 j .. 8 j + 7, so every wave has one and the block's units span at most two
+// tiles, whose keys it stages together.  With one idle wave per block (R =
+// 224) the busiest SIMD of a CU carries as many waves as at R = 256 and the
+// block barriers pace every block by it; packing gives each block 8 busy waves.
+template <typename T, int D, int NS>
 __global__ __launch_bounds__(kTilesThreads, 2) void score_tiles_kernel(ScoreArgs a) {
-  const int tile = blockIdx.x / a.row_chunks, rc = blockIdx.x % a.row_chunks;
   const int g = blockIdx.y, b = blockIdx.z;
   const int L = a.L[b];
-  const int kbase = tile * kT;
-  if (kbase >= L) return;
-  const int G = a.Hq / a.Hkv, R = a.R, w = a.w;
-  const int row0 = rc * kRows;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int t0, tile, pair, row0;                       // block's first tile; this wave's unit
+  if constexpr (NS == 1) {
+    t0 = tile = blockIdx.x / a.row_chunks;
+    row0 = (blockIdx.x % a.row_chunks) * kRows;
+    pair = wave;
+  } else {
+    const int P = a.pack_pairs;
+    const int u = static_cast<int>(blockIdx.x) * 8 + wave;
+    t0 = static_cast<int>(blockIdx.x) * 8 / P;
+    tile = u / P;
+    pair = u % P;
+    row0 = 0;
+  }
+  if (t0 * kT >= L) return;                       // block-uniform
+  const int kbase = tile * kT;
+  const int G = a.Hq / a.Hkv, R = a.R, w = a.w;
   const int q4 = lane >> 4, r16 = lane & 15;
-  const bool active = row0 + kWaveRows * wave < R;    // wave-uniform: not all padding
+  // wave-uniform: the unit has real rows and real keys
+  const bool active = row0 + kWaveRows * pair < R && kbase < L;
 
   __shared__ float qs[kRows][kDC + 1];             // +1: conflict-free column reads
-  __shared__ double ks[kT][kDC + 1];             // keys staged as float64: every wave reads them
+  __shared__ double ks[NS * kT][kDC + 1];        // keys staged as float64: every wave reads them
   __shared__ int s_lim[kRows];                     // last key a row sees (-1: padding)
   if (tid < kRows) {
     const int r = row0 + tid;
     s_lim[tid] = r < R ? min(L - 1, L - w + r % w) : -1;
   }
 
-  // Staging: two threads per window row (16 elements each) and, for the first
-  // 256 threads, four threads per key (8 elements each).
+  // Staging: two threads per window row (16 elements each) and four threads
+  // per key (8 elements each; the first 256 threads when NS = 1).
   const int qrow = tid >> 1, qoff = (tid & 1) * 16;
   const bool qvalid = row0 + qrow < R;
   const T* qsrc = nullptr;
@@ -132,10 +155,10 @@ __global__ __launch_bounds__(kTilesThreads, 2) void score_tiles_kernel(ScoreArgs
     const int r = row0 + qrow, h = g * G + r / w, i = r % w;
     qsrc = static_cast<const T*>(a.q_win) + ((static_cast<size_t>(b) * a.Hq + h) * w + i) * D + qoff;
   }
-  const int kk = (tid & 255) >> 2, kdp = (tid & 3) * 8;
-  const bool kvalid = tid < 256 && kbase + kk < L;
+  const int kk = (tid & (NS * 256 - 1)) >> 2, kdp = (tid & 3) * 8;
+  const bool kvalid = tid < NS * 256 && t0 * kT + kk < L;
   const T* ksrc = static_cast<const T*>(a.k) +
-                  ((static_cast<size_t>(b) * a.Hkv + g) * a.Lmax + kbase + kk) * D + kdp;
+                  ((static_cast<size_t>(b) * a.Hkv + g) * a.Lmax + t0 * kT + kk) * D + kdp;
   float qv[16], kv[8];
   auto fetch = [&](int dc) {
     if (qvalid) {
@@ -155,7 +178,7 @@ __global__ __launch_bounds__(kTilesThreads, 2) void score_tiles_kernel(ScoreArgs
   auto stage = [&]() {
 #pragma unroll
     for (int e = 0; e < 16; ++e) qs[qrow][qoff + e] = qv[e];
-    if (tid < 256) {
+    if (tid < NS * 256) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) ks[kk][kdp + e] = static_cast<double>(kv[e]);
     }
@@ -181,9 +204,9 @@ __global__ __launch_bounds__(kTilesThreads, 2) void score_tiles_kernel(ScoreArgs
         double av[2], bv[4];
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
-          av[rt] = static_cast<double>(qs[kWaveRows * wave + 16 * rt + r16][dd]);
+          av[rt] = static_cast<double>(qs[kWaveRows * pair + 16 * rt + r16][dd]);
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) bv[kt] = ks[16 * kt + r16][dd];
+        for (int kt = 0; kt < 4; ++kt) bv[kt] = ks[(tile - t0) * kT + 16 * kt + r16][dd];
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
@@ -209,7 +232,7 @@ __global__ __launch_bounds__(kTilesThreads, 2) void score_tiles_kernel(ScoreArgs
   for (int rt = 0; rt < 2; ++rt) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int rl = kWaveRows * wave + 16 * rt + q4 + 4 * v;
+      const int rl = kWaveRows * pair + 16 * rt + q4 + 4 * v;
       const int lim = s_lim[rl];
       bool ok[4];
       float mx = -INFINITY;
@@ -399,13 +422,41 @@ hipError_t launch_score(const ScoreArgs& args, int d, bool bf16, hipStream_t st)
   ScoreArgs a = args;
   const double e_bytes = 4.0 * kT * a.R * a.n_tiles * a.Hkv * a.B;
   a.stream_e = e_bytes > 256.0 * (1 << 20);
-  const dim3 g1(a.n_tiles * a.row_chunks, a.Hkv, a.B);
-  if (bf16) {
-    if (d == 128) score_tiles_kernel<bf16_t, 128><<<g1, kTilesThreads, 0, st>>>(a);
-    else          score_tiles_kernel<bf16_t, 64><<<g1, kTilesThreads, 0, st>>>(a);
+  // Packed blocks (P = 4, 6 or 7 row pairs: waves would idle, and every run of
+  // 8 units spans at most two tiles) when packing lowers the blocks per CU and
+  // still leaves two per CU (two resident blocks overlap each other's barriers
+  // and staging).  Measured, d = 128, one scoring call, packed against not
+  // (us): P = 7, 4 KV heads: L = 32768 174 / 187 (8 -> 7 blocks per CU),
+  // 36864 198 / 210, 65536 352 / 369, but 8192 64.0 / 62.5, 16384 107 / 105,
+  // 24576 157 / 153, 28672 175 / 169 (blocks per CU unchanged); P = 6:
+  // 16384 85.0 / 99.7, 32768 152 / 184, 8192 60.1 / 59.2 (2 -> 2); P = 4:
+  // 16384 60.9 / 66.6, 32768 107 / 117, 8192 43.9 / 40.8 (one block per CU).
+  constexpr long long kCUs = 256;
+  const int P = (a.R + kWaveRows - 1) / kWaveRows;
+  const long long units = static_cast<long long>(a.Hkv) * a.B;
+  const long long plain = static_cast<long long>(a.n_tiles) * units;
+  const long long packed = (static_cast<long long>(P) * a.n_tiles + 7) / 8 * units;
+  const bool pack = a.row_chunks == 1 && (P == 4 || P == 6 || P == 7) && packed >= 2 * kCUs &&
+                    (packed + kCUs - 1) / kCUs < (plain + kCUs - 1) / kCUs;
+  a.pack_pairs = pack ? P : 0;
+  if (pack) {
+    const dim3 g1((P * a.n_tiles + 7) / 8, a.Hkv, a.B);
+    if (bf16) {
+      if (d == 128) score_tiles_kernel<bf16_t, 128, 2><<<g1, kTilesThreads, 0, st>>>(a);
+      else          score_tiles_kernel<bf16_t, 64, 2><<<g1, kTilesThreads, 0, st>>>(a);
+    } else {
+      if (d == 128) score_tiles_kernel<float, 128, 2><<<g1, kTilesThreads, 0, st>>>(a);
+      else          score_tiles_kernel<float, 64, 2><<<g1, kTilesThreads, 0, st>>>(a);
+    }
   } else {
-    if (d == 128) score_tiles_kernel<float, 128><<<g1, kTilesThreads, 0, st>>>(a);
-    else          score_tiles_kernel<float, 64><<<g1, kTilesThreads, 0, st>>>(a);
+    const dim3 g1(a.n_tiles * a.row_chunks, a.Hkv, a.B);
+    if (bf16) {
+      if (d == 128) score_tiles_kernel<bf16_t, 128, 1><<<g1, kTilesThreads, 0, st>>>(a);
+      else          score_tiles_kernel<bf16_t, 64, 1><<<g1, kTilesThreads, 0, st>>>(a);
+    } else {
+      if (d == 128) score_tiles_kernel<float, 128, 1><<<g1, kTilesThreads, 0, st>>>(a);
+      else          score_tiles_kernel<float, 64, 1><<<g1, kTilesThreads, 0, st>>>(a);
+    }
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;

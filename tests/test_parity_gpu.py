@@ -292,10 +292,39 @@ def test_select_exact_narrow_range():
     (torch.bfloat16, 64, 4, 64, 1, [129, 3000]),
     (torch.bfloat16, 128, 8, 40, 9, [2100]),          # 320 rows: two row chunks
     (torch.bfloat16, 128, 16, 64, 7, [700]),          # 1024 rows: four row chunks
+    # blocks with idle waves (too few blocks to pack): 6, 4 and 7 row pairs
+    (torch.bfloat16, 128, 6, 32, 7, [1000, 130]),     # 192 rows
+    (torch.bfloat16, 64, 5, 20, 3, [777]),            # 100 rows, the last pair partial
+    (torch.float32, 128, 7, 30, 5, [300, 2049]),      # 210 rows, the last pair partial
+    (torch.bfloat16, 128, 2, 64, 7, [65, 200, 4160]), # 128 rows, ragged batch
 ])
 def test_score_matches_oracle(dtype, d, G, w, pool, L):
-    case(f"score dtype={dtype} d={d} G={G} w={w} pool={pool} L={L}")
-    Hkv = 2
+    _score_case(dtype, d, G, w, pool, L, 2)
+
+
+def _k1_packs(R, Lmax, Hkv, B):
+    """Whether the library runs K1 with packed blocks (8 units of 32 rows x
+    64 keys per block over at most two key tiles) for this shape: 4, 6 or 7
+    row pairs, at least two packed blocks per CU and fewer blocks per CU than
+    unpacked (256 CUs)."""
+    P, nt, units = -(-R // 32), -(-Lmax // 64), Hkv * B
+    plain, packed = nt * units, -(-P * nt // 8) * units
+    return P in (4, 6, 7) and packed >= 512 and -(-packed // 256) < -(-plain // 256)
+
+
+@pytest.mark.parametrize("dtype,d,G,w,pool,Hkv,L", [
+    (torch.bfloat16, 128, 7, 32, 7, 8, [4600, 3001]),   # 224 rows: 7 row pairs
+    (torch.bfloat16, 64, 6, 32, 5, 8, [4096, 3333]),    # 192 rows: 6 pairs
+    (torch.float32, 128, 5, 20, 3, 4, [8200, 129]),     # 100 rows: 4 pairs, the last partial
+    (torch.bfloat16, 128, 7, 30, 7, 8, [5150, 999]),    # 210 rows: 7 pairs, the last partial
+])
+def test_score_packed_blocks_match_oracle(dtype, d, G, w, pool, Hkv, L):
+    assert _k1_packs(G * w, max(L), Hkv, len(L)), "shape does not take the packed blocks"
+    _score_case(dtype, d, G, w, pool, L, Hkv)
+
+
+def _score_case(dtype, d, G, w, pool, L, Hkv):
+    case(f"score dtype={dtype} d={d} G={G} w={w} pool={pool} Hkv={Hkv} L={L}")
     wl = synth.custom(700 + d + G + w, dtype, len(L), L, G * Hkv, Hkv, d, w, pool, 1)
     pr = synth.make_prompt(wl, L=L, pad_value=float("nan"))    # padding must never be read
     ev = Evictor(len(L), max(L), G * Hkv, Hkv, d, w, pool, keep_raw=True)
