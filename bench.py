@@ -719,7 +719,7 @@ def headline(torch, _lib, synth, Evictor, dev, steps, warmup, tokens=None):
         },
         "roofline": {
             "kernel": "tb_decode_attn: decode_mfma_kernel (split-K partials) + "
-                      "decode_merge_kernel / decode_merge_wave_kernel, one call per layer "
+                      "decode_merge_split_kernel (log-sum-exp merge), one call per layer "
                       "and token",
             "bound": "hbm",
             "achieved": round(achieved, 1),

@@ -24,10 +24,11 @@
 //     has one wave (the wave stores its partial from registers) or 2, 4 or 8
 //     (bf16: wave w takes every WAVES-th tile of the block from its w-th on;
 //     the block combines the waves through LDS).
-//   merge kernel, grid = (Hq, B): combines a query head's chunk partials by
-//     log-sum-exp in a fixed order, writes the output; the block of query
-//     head 0 advances kv_len[b].  One wave per query head when one round of
-//     loads covers the chunks, else a 256-thread block with an LDS tree.
+//   merge kernel: combines a query head's chunk partials by log-sum-exp in a
+//     fixed order, writes the output; the first block advances kv_len[b].
+//     d = 128 and up to 64 chunks: one wave per quarter head; d = 64 and up
+//     to 64 chunks: one wave per head; more chunks: a 256-thread block per
+//     head with an LDS tree.
 // bf16 runs on the matrix cores (v_mfma_f32_16x16x32_bf16), one wave per
 // 32-key block at a time:
 //   S^T[32 keys x 16 heads] = K[32 x d] . Q^T[d x 16]   (heads padded to 16)
@@ -637,6 +638,94 @@ __global__ __launch_bounds__(64) void decode_merge_wave_kernel(DecodeArgs a) {
   if (h == 0 && lane == 0) a.kv_len[b] = N;
 }
 
+// --------------------------------------------------------------------------
+// Merge by one wave per E4 float4 slices of a query head's output (grid =
+// (Hq * NQ, B), NQ = d / (4 E4) waves per head): lane = (chunk split sp of
+// 64 / E4, slice e4); each lane issues one round of KPT partials' loads (the
+// m, l of a partial are read by all NQ waves of its head), then the splits
+// are combined by cross-lane swaps in a fixed order (lower split first).
+// One round covers (64 / E4) * KPT chunks with no LDS and no barrier; more
+// chunks take more rounds.
+// --------------------------------------------------------------------------
+template <typename T, int D, int G, int E4, int KPT>
+__global__ __launch_bounds__(64) void decode_merge_split_kernel(DecodeArgs a) {
+  constexpr int NQ = D / 4 / E4;             // waves per query head
+  constexpr int SPL = 64 / E4;               // chunk splits per wave
+  const int h = blockIdx.x / NQ, qd = blockIdx.x % NQ, b = blockIdx.y;
+  const int Hkv = a.Hkv, Hq = Hkv * G;
+  const int g = h / G, hh = h % G;
+  const int lane = threadIdx.x, e4 = qd * E4 + lane % E4, sp = lane / E4;
+  const int N = a.seq_len[b];
+  const int n_used = a.n_chunks;
+  const size_t bg = static_cast<size_t>(b) * Hkv + g;
+  const float* base = a.part + (bg * a.n_chunks * G + hh) * (D + 4);
+  constexpr size_t CSTRIDE = static_cast<size_t>(G) * (D + 4);
+
+  float M = -INFINITY, L = 0.f;
+  float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int c0 = sp; c0 < n_used; c0 += SPL * KPT) {
+    float mm[KPT], ll[KPT];
+    float4 oo[KPT];
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) {
+      const int cc = c0 + k * SPL;
+      const float* pc = base + min(cc, n_used - 1) * CSTRIDE;
+      const float2 ml = *reinterpret_cast<const float2*>(pc + D);
+      oo[k] = *reinterpret_cast<const float4*>(pc + 4 * e4);
+      mm[k] = cc < n_used ? ml.x : -INFINITY;
+      ll[k] = cc < n_used ? ml.y : 0.f;
+    }
+    // keep every load above this point: they must all be in flight together
+    __builtin_amdgcn_sched_barrier(0);
+    float mx = M;
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) mx = fmaxf(mx, mm[k]);
+    if (mx == -INFINITY) continue;
+    const float corr = exp2f(M - mx);
+    L *= corr; O.x *= corr; O.y *= corr; O.z *= corr; O.w *= corr;
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) {
+      const float wgt = exp2f(mm[k] - mx);
+      L += wgt * ll[k];
+      O.x += wgt * oo[k].x; O.y += wgt * oo[k].y; O.z += wgt * oo[k].z; O.w += wgt * oo[k].w;
+    }
+    M = mx;
+  }
+  // splits s and s ^ (off / E4) meet at lanes l and l ^ off; both lanes combine
+  // (lower split, upper split) in that order, so they hold identical results
+#pragma unroll
+  for (int off = 32; off >= E4; off >>= 1) {
+    const float Mo = __shfl_xor(M, off), Lo = __shfl_xor(L, off);
+    const float4 Oo = make_float4(__shfl_xor(O.x, off), __shfl_xor(O.y, off),
+                                  __shfl_xor(O.z, off), __shfl_xor(O.w, off));
+    const bool upper = (lane & off) != 0;
+    const float Ma = upper ? Mo : M, La = upper ? Lo : L;
+    const float Mb = upper ? M : Mo, Lb = upper ? L : Lo;
+    const float4 Oa = upper ? Oo : O, Ob = upper ? O : Oo;
+    const float Mn = fmaxf(Ma, Mb);
+    if (Mn != -INFINITY) {
+      const float w1 = exp2f(Ma - Mn), w2 = exp2f(Mb - Mn);
+      L = La * w1 + Lb * w2;
+      O = make_float4(Oa.x * w1 + Ob.x * w2, Oa.y * w1 + Ob.y * w2,
+                      Oa.z * w1 + Ob.z * w2, Oa.w * w1 + Ob.w * w2);
+    }
+    M = Mn;
+  }
+  if (sp == 0) {
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    T* out = static_cast<T*>(a.out) + (static_cast<size_t>(b) * Hq + h) * D + 4 * e4;
+    if constexpr (sizeof(T) == 2) {
+      typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+      *reinterpret_cast<bf16x4*>(out) =
+          bf16x4{static_cast<__bf16>(O.x * inv), static_cast<__bf16>(O.y * inv),
+                 static_cast<__bf16>(O.z * inv), static_cast<__bf16>(O.w * inv)};
+    } else {
+      *reinterpret_cast<float4*>(out) = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
+    }
+  }
+  if (blockIdx.x == 0 && lane == 0) a.kv_len[b] = N;
+}
+
 constexpr int kMergeThreads = 256;
 constexpr int kMergePerThread = 8;
 
@@ -739,7 +828,17 @@ hipError_t launch_both(const DecodeArgs& a, hipStream_t st) {
   }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (a.n_chunks <= (256 / D) * kWaveMergePerLane)
+  // d = 128: one wave per quarter head (8 float4 slices), one round of loads
+  // for up to 64 chunks.  Measured on the 28-layer L = 32768 benchmark
+  // (tokens/s, two runs each, alternated): 2423-2425 against 2368-2369 with
+  // the whole-head wave (<= 32 chunks) and the 256-thread block with its LDS
+  // tree (33-64); 16 slices per wave 2414, 4 slices 2359-2360; at 32 chunks
+  // 207 against 211 us per token for the whole-head wave.
+  if (D == 128 && a.n_chunks <= 32)
+    decode_merge_split_kernel<T, D, G, 8, 4><<<dim3(a.Hkv * G * (D / 32), a.B), 64, 0, st>>>(a);
+  else if (D == 128 && a.n_chunks <= 64)
+    decode_merge_split_kernel<T, D, G, 8, 8><<<dim3(a.Hkv * G * (D / 32), a.B), 64, 0, st>>>(a);
+  else if (a.n_chunks <= (256 / D) * kWaveMergePerLane)
     decode_merge_wave_kernel<T, D, G><<<dim3(a.Hkv * G, a.B), 64, 0, st>>>(a);
   else
     decode_merge_kernel<T, D, G><<<dim3(a.Hkv * G, a.B), kMergeThreads, 0, st>>>(a);
