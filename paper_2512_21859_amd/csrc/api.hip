@@ -94,8 +94,11 @@ namespace tb {
 //   4-7 tiles, four waves 11.37-13.08 against 11.59-13.42 (two); 8 tiles,
 //   four waves 13.31 against 13.52 (eight); 9-16 tiles, eight waves 14.56-
 //   19.13 against 14.68-19.22 (four).
-// * Small caches (<= 2560 rows) keep at most 32 partials per KV head, which
-//   one wave per query head merges in a single round of loads.
+// * Small caches (<= 2048 rows) keep at most 32 partials per KV head (blocks
+//   of up to two tiles).  Measured with the quarter-head merge waves (us per
+//   layer-step or per 28-layer token, two runs each, alternated): 2304 rows
+//   6.85 against 7.10 with the cap (so the earlier 2560-row threshold was
+//   lowered), 1792 rows 206.9 against 207.3-207.8 us per token without it.
 // * Batches (B > 1) are usually ragged, and the plan sees only the capacity:
 //   blocks past a sequence's length exit at once, so small blocks (one wave,
 //   about 12 tiles) balance the real work across CUs.  On ragged batches and
@@ -117,7 +120,7 @@ DecodePlan decode_plan(int B, int Hkv, int cap, bool bf16) {
   }
   const long long tiles = std::max<long long>(1, cap / kVTile);
   long long C = std::max<long long>(1, 256 / units);
-  if (cap <= 2560) C = std::min<long long>(C, 32);
+  if (cap <= 2048) C = std::min<long long>(C, 32);
   C = std::min(C, tiles);
   constexpr long long kBatchTiles = 12;
   const bool batch = B > 1 && tiles / C > kBatchTiles;

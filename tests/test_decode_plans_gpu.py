@@ -26,7 +26,8 @@ def _gpu():
 # capacities (rows) and the block shape the plan gives 4 KV heads at each:
 # one block per CU (64 per KV head), the cap/32 tiles split evenly, one wave
 # per tile up to 8
-CAPS = [672,      # <= 2560 rows: 21 one-tile blocks per KV head, <= 32 partials
+CAPS = [672,      # <= 2048 rows: 21 one-tile blocks per KV head, <= 32 partials
+        2304,     # 72 tiles: 64 blocks of 1-2 tiles (past the 32-partial cap)
         2816,     # 64 blocks of 1-2 tiles, one wave
         4352,     # two-wave blocks of 2-3 tiles
         8448,     # four-wave blocks of 4-5 tiles
