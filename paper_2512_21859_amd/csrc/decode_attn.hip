@@ -24,11 +24,9 @@
 //     has one wave (the wave stores its partial from registers) or 2, 4 or 8
 //     (bf16: wave w takes every WAVES-th tile of the block from its w-th on;
 //     the block combines the waves through LDS).
-//   merge kernel: combines a query head's chunk partials by log-sum-exp in a
-//     fixed order, writes the output; the first block advances kv_len[b].
-//     d = 128 and up to 64 chunks: one wave per quarter head; d = 64 and up
-//     to 64 chunks: one wave per head; more chunks: a 256-thread block per
-//     head with an LDS tree.
+//   merge kernel, grid = (Hq * d / 32, B): one wave per 32 output values of a
+//     query head combines that head's chunk partials by log-sum-exp in a
+//     fixed order and writes them; the first wave advances kv_len[b].
 // bf16 runs on the matrix cores (v_mfma_f32_16x16x32_bf16), one wave per
 // 32-key block at a time:
 //   S^T[32 keys x 16 heads] = K[32 x d] . Q^T[d x 16]   (heads padded to 16)
@@ -537,115 +535,15 @@ __global__ __launch_bounds__(kValuThreads) void decode_valu_kernel(DecodeArgs a)
 }
 
 // --------------------------------------------------------------------------
-// Merge of the chunk partials of one query head.
-// grid = (Hq, B), block = 256 threads: thread (sp, e4) handles output
-// elements 4*e4 .. 4*e4+3 over the chunks c = sp, sp + S, ... (S = 256/(d/4)
-// interleaved splits, up to 8 chunks per thread per round).  A thread issues
-// all of a round's partial loads before using them (online max per thread),
-// then the splits are combined by a fixed-order tree in LDS.
-// Every chunk writes a partial (empty chunks carry m = -inf, l = 0), so the
-// merge runs over all of them and never waits for the length; the length is
-// only needed for the final kv_len store.
-// --------------------------------------------------------------------------
-// --------------------------------------------------------------------------
-// Merge by one wave per (query head, sequence), for up to 64 / (d/4) * 16
-// chunks (32 at d = 128): lane = (chunk split, float4 slice of o); every lane
-// issues its 16 partial loads at once, then the splits are combined by
-// cross-lane swaps in a fixed order (lower split first).  No LDS, no barrier;
-// measured faster than the block merge below whenever one round of loads
-// covers the chunks (21 chunks of the L = 8192 workload: 6.6 vs 7.1 us per
-// step), slower when it needs two.
-// --------------------------------------------------------------------------
-constexpr int kWaveMergePerLane = 16;
-
-template <typename T, int D, int G>
-__global__ __launch_bounds__(64) void decode_merge_wave_kernel(DecodeArgs a) {
-  constexpr int E4 = D / 4;                  // float4 slices of one head's o
-  constexpr int SPL = 64 / E4;               // chunk splits per wave
-  constexpr int KPT = kWaveMergePerLane;
-  const int h = blockIdx.x, b = blockIdx.y;
-  const int Hkv = a.Hkv, Hq = Hkv * G;
-  const int g = h / G, hh = h % G;
-  const int lane = threadIdx.x, e4 = lane % E4, sp = lane / E4;
-  const int N = a.seq_len[b];
-  const int n_used = a.n_chunks;
-  const size_t bg = static_cast<size_t>(b) * Hkv + g;
-  const float* base = a.part + (bg * a.n_chunks * G + hh) * (D + 4);
-  constexpr size_t CSTRIDE = static_cast<size_t>(G) * (D + 4);
-
-  float M = -INFINITY, L = 0.f;
-  float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int c0 = sp; c0 < n_used; c0 += SPL * KPT) {
-    float mm[KPT], ll[KPT];
-    float4 oo[KPT];
-#pragma unroll
-    for (int k = 0; k < KPT; ++k) {
-      const int cc = c0 + k * SPL;
-      const float* pc = base + min(cc, n_used - 1) * CSTRIDE;
-      const float2 ml = *reinterpret_cast<const float2*>(pc + D);
-      oo[k] = *reinterpret_cast<const float4*>(pc + 4 * e4);
-      mm[k] = cc < n_used ? ml.x : -INFINITY;
-      ll[k] = cc < n_used ? ml.y : 0.f;
-    }
-    // keep every load above this point: they must all be in flight together
-    __builtin_amdgcn_sched_barrier(0);
-    float mx = M;
-#pragma unroll
-    for (int k = 0; k < KPT; ++k) mx = fmaxf(mx, mm[k]);
-    if (mx == -INFINITY) continue;
-    const float corr = exp2f(M - mx);
-    L *= corr; O.x *= corr; O.y *= corr; O.z *= corr; O.w *= corr;
-#pragma unroll
-    for (int k = 0; k < KPT; ++k) {
-      const float wgt = exp2f(mm[k] - mx);
-      L += wgt * ll[k];
-      O.x += wgt * oo[k].x; O.y += wgt * oo[k].y; O.z += wgt * oo[k].z; O.w += wgt * oo[k].w;
-    }
-    M = mx;
-  }
-  // splits s and s ^ (off / E4) meet at lanes l and l ^ off; both lanes combine
-  // (lower split, upper split) in that order, so they hold identical results
-#pragma unroll
-  for (int off = 32; off >= E4; off >>= 1) {
-    const float Mo = __shfl_xor(M, off), Lo = __shfl_xor(L, off);
-    const float4 Oo = make_float4(__shfl_xor(O.x, off), __shfl_xor(O.y, off),
-                                  __shfl_xor(O.z, off), __shfl_xor(O.w, off));
-    const bool upper = (lane & off) != 0;
-    const float Ma = upper ? Mo : M, La = upper ? Lo : L;
-    const float Mb = upper ? M : Mo, Lb = upper ? L : Lo;
-    const float4 Oa = upper ? Oo : O, Ob = upper ? O : Oo;
-    const float Mn = fmaxf(Ma, Mb);
-    if (Mn != -INFINITY) {
-      const float w1 = exp2f(Ma - Mn), w2 = exp2f(Mb - Mn);
-      L = La * w1 + Lb * w2;
-      O = make_float4(Oa.x * w1 + Ob.x * w2, Oa.y * w1 + Ob.y * w2,
-                      Oa.z * w1 + Ob.z * w2, Oa.w * w1 + Ob.w * w2);
-    }
-    M = Mn;
-  }
-  if (sp == 0) {
-    const float inv = L > 0.f ? 1.f / L : 0.f;
-    T* out = static_cast<T*>(a.out) + (static_cast<size_t>(b) * Hq + h) * D + 4 * e4;
-    if constexpr (sizeof(T) == 2) {
-      typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
-      *reinterpret_cast<bf16x4*>(out) =
-          bf16x4{static_cast<__bf16>(O.x * inv), static_cast<__bf16>(O.y * inv),
-                 static_cast<__bf16>(O.z * inv), static_cast<__bf16>(O.w * inv)};
-    } else {
-      *reinterpret_cast<float4*>(out) = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
-    }
-  }
-  if (h == 0 && lane == 0) a.kv_len[b] = N;
-}
-
-// --------------------------------------------------------------------------
-// Merge by one wave per E4 float4 slices of a query head's output (grid =
-// (Hq * NQ, B), NQ = d / (4 E4) waves per head): lane = (chunk split sp of
-// 64 / E4, slice e4); each lane issues one round of KPT partials' loads (the
-// m, l of a partial are read by all NQ waves of its head), then the splits
-// are combined by cross-lane swaps in a fixed order (lower split first).
-// One round covers (64 / E4) * KPT chunks with no LDS and no barrier; more
-// chunks take more rounds.
+// Merge of the chunk partials of one query head, by one wave per E4 float4
+// slices of its output (grid = (Hq * NQ, B), NQ = d / (4 E4) waves per head):
+// lane = (chunk split sp of 64 / E4, slice e4); each lane issues one round of
+// KPT partials' loads (the m, l of a partial are read by all NQ waves of its
+// head), then the splits are combined by cross-lane swaps in a fixed order
+// (lower split first).  One round covers (64 / E4) * KPT chunks with no LDS
+// and no barrier; more chunks take more rounds.  Every chunk writes a partial
+// (empty chunks carry m = -inf, l = 0), so the merge runs over all of them and
+// never waits for the length; the length is only needed for the kv_len store.
 // --------------------------------------------------------------------------
 template <typename T, int D, int G, int E4, int KPT>
 __global__ __launch_bounds__(64) void decode_merge_split_kernel(DecodeArgs a) {
@@ -726,92 +624,6 @@ __global__ __launch_bounds__(64) void decode_merge_split_kernel(DecodeArgs a) {
   if (blockIdx.x == 0 && lane == 0) a.kv_len[b] = N;
 }
 
-constexpr int kMergeThreads = 256;
-constexpr int kMergePerThread = 8;
-
-template <typename T, int D, int G>
-__global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeArgs a) {
-  constexpr int E4 = D / 4;
-  constexpr int S = kMergeThreads / E4;
-  constexpr int KPT = kMergePerThread;
-  const int h = blockIdx.x, b = blockIdx.y;
-  const int Hkv = a.Hkv, Hq = Hkv * G;
-  const int g = h / G, hh = h % G;
-  const int tid = threadIdx.x, e4 = tid % E4, sp = tid / E4;
-  const int N = a.seq_len[b];
-  const int n_used = a.n_chunks;
-  const size_t bg = static_cast<size_t>(b) * Hkv + g;
-  const float* base = a.part + (bg * a.n_chunks * G + hh) * (D + 4);
-  constexpr size_t CSTRIDE = static_cast<size_t>(G) * (D + 4);
-
-  __shared__ float2 s_ml[S][E4];
-  __shared__ float4 s_o[S][E4];
-
-  float M = -INFINITY, L = 0.f;
-  float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int c0 = sp; c0 < n_used; c0 += S * KPT) {
-    float mm[KPT], ll[KPT];
-    float4 oo[KPT];
-    // unconditional loads (index clamped, value masked) so they issue back to back
-#pragma unroll
-    for (int k = 0; k < KPT; ++k) {
-      const int cc = c0 + k * S;
-      const float* pc = base + min(cc, n_used - 1) * CSTRIDE;
-      const float2 ml = *reinterpret_cast<const float2*>(pc + D);
-      oo[k] = *reinterpret_cast<const float4*>(pc + 4 * e4);
-      mm[k] = cc < n_used ? ml.x : -INFINITY;
-      ll[k] = cc < n_used ? ml.y : 0.f;
-    }
-    // keep every load above this point: they must all be in flight together
-    __builtin_amdgcn_sched_barrier(0);
-    float mx = M;
-#pragma unroll
-    for (int k = 0; k < KPT; ++k) mx = fmaxf(mx, mm[k]);
-    if (mx == -INFINITY) continue;
-    const float corr = exp2f(M - mx);
-    L *= corr; O.x *= corr; O.y *= corr; O.z *= corr; O.w *= corr;
-#pragma unroll
-    for (int k = 0; k < KPT; ++k) {
-      const float wgt = exp2f(mm[k] - mx);
-      L += wgt * ll[k];
-      O.x += wgt * oo[k].x; O.y += wgt * oo[k].y; O.z += wgt * oo[k].z; O.w += wgt * oo[k].w;
-    }
-    M = mx;
-  }
-  // fixed-order tree over the S splits
-#pragma unroll
-  for (int half = S / 2; half >= 1; half >>= 1) {
-    if (sp >= half && sp < 2 * half) { s_ml[sp][e4] = make_float2(M, L); s_o[sp][e4] = O; }
-    __syncthreads();
-    if (sp < half) {
-      const float2 ml2 = s_ml[sp + half][e4];
-      const float4 o2 = s_o[sp + half][e4];
-      const float Mn = fmaxf(M, ml2.x);
-      if (Mn != -INFINITY) {
-        const float w1 = exp2f(M - Mn), w2 = exp2f(ml2.x - Mn);
-        L = L * w1 + ml2.y * w2;
-        O.x = O.x * w1 + o2.x * w2; O.y = O.y * w1 + o2.y * w2;
-        O.z = O.z * w1 + o2.z * w2; O.w = O.w * w1 + o2.w * w2;
-        M = Mn;
-      }
-    }
-    __syncthreads();
-  }
-  if (sp == 0) {
-    const float inv = L > 0.f ? 1.f / L : 0.f;
-    T* out = static_cast<T*>(a.out) + (static_cast<size_t>(b) * Hq + h) * D + 4 * e4;
-    if constexpr (sizeof(T) == 2) {
-      typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
-      *reinterpret_cast<bf16x4*>(out) =
-          bf16x4{static_cast<__bf16>(O.x * inv), static_cast<__bf16>(O.y * inv),
-                 static_cast<__bf16>(O.z * inv), static_cast<__bf16>(O.w * inv)};
-    } else {
-      *reinterpret_cast<float4*>(out) = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
-    }
-  }
-  if (h == 0 && tid == 0) a.kv_len[b] = N;
-}
-
 template <typename T, int D, int G, bool PAGED>
 hipError_t launch_both(const DecodeArgs& a, hipStream_t st) {
   const dim3 grid(a.n_chunks, a.Hkv, a.B);
@@ -828,20 +640,20 @@ hipError_t launch_both(const DecodeArgs& a, hipStream_t st) {
   }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // d = 128: one wave per quarter head (8 float4 slices), one round of loads
-  // for up to 64 chunks.  Measured on the 28-layer L = 32768 benchmark
-  // (tokens/s, two runs each, alternated): 2423-2425 against 2368-2369 with
-  // the whole-head wave (<= 32 chunks) and the 256-thread block with its LDS
-  // tree (33-64); 16 slices per wave 2414, 4 slices 2359-2360; at 32 chunks
-  // 207 against 211 us per token for the whole-head wave.
-  if (D == 128 && a.n_chunks <= 32)
+  // 8 float4 slices per wave (a quarter of a head's output at d = 128, half
+  // at d = 64), one round of loads for up to 128 chunks.  Measured on the
+  // 28-layer L = 32768 benchmark (tokens/s, two runs each, alternated):
+  // 2423-2425 against 2368-2369 with one wave per whole head (<= 32 chunks)
+  // and a 256-thread block per head with an LDS tree (33-64); 16 slices per
+  // wave 2414, 4 slices 2359-2360.  Against those at other shapes (us per
+  // decode call): 128-256 chunks (1-2 KV heads, d = 128, 8192-32768 rows)
+  // 7.2-9.6 against 8.0-10.8; d = 64, 32-64 chunks 5.7-14.7 against 6.0-15.0.
+  if (a.n_chunks <= 32)
     decode_merge_split_kernel<T, D, G, 8, 4><<<dim3(a.Hkv * G * (D / 32), a.B), 64, 0, st>>>(a);
-  else if (D == 128 && a.n_chunks <= 64)
+  else if (a.n_chunks <= 64)
     decode_merge_split_kernel<T, D, G, 8, 8><<<dim3(a.Hkv * G * (D / 32), a.B), 64, 0, st>>>(a);
-  else if (a.n_chunks <= (256 / D) * kWaveMergePerLane)
-    decode_merge_wave_kernel<T, D, G><<<dim3(a.Hkv * G, a.B), 64, 0, st>>>(a);
   else
-    decode_merge_kernel<T, D, G><<<dim3(a.Hkv * G, a.B), kMergeThreads, 0, st>>>(a);
+    decode_merge_split_kernel<T, D, G, 8, 16><<<dim3(a.Hkv * G * (D / 32), a.B), 64, 0, st>>>(a);
   return hipGetLastError();
 }
 
