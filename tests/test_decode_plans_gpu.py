@@ -67,3 +67,38 @@ def test_single_sequence_plans(cap, d):
             ref = O.decode_step(q64[t, 0, g * G:(g + 1) * G], rk, rv)
             err = np.abs(got[t, 0, g * G:(g + 1) * G] - ref).max()
             assert err <= DECODE_TOL[torch.bfloat16], f"g={g} t={t}: max abs err {err}"
+
+
+@pytest.mark.parametrize("d", [128, 64])
+@pytest.mark.parametrize("Hkv,cap", [(1, 20000),    # 256 blocks of one KV head: 256 partials, two merge rounds
+                                     (2, 12032)])   # 128 partials per KV head, one round of 16 per lane
+def test_many_partial_plans(Hkv, cap, d):
+    print(f"\n[case] decode many partials Hkv={Hkv} cap={cap} d={d}", flush=True)
+    B, G, T = 1, 8, 2
+    Hq = G * Hkv
+    n0 = cap - 29
+    gen = torch.Generator().manual_seed(7 * cap + d + Hkv)
+    kc = torch.randn((B, Hkv, cap, d), generator=gen).to(torch.bfloat16)
+    vc = torch.randn((B, Hkv, cap, d), generator=gen).to(torch.bfloat16)
+    q = torch.randn((T, B, Hq, d), generator=gen).to(torch.bfloat16)
+    kn = torch.randn((T, B, Hkv, d), generator=gen).to(torch.bfloat16)
+    vn = torch.randn((T, B, Hkv, d), generator=gen).to(torch.bfloat16)
+    cache = _lib.KVCache(B, Hq, Hkv, cap, d, torch.bfloat16)
+    cache.k.copy_(kc)
+    cache.v.copy_(vc)
+    cache.kv_len.fill_(n0)
+    cache.host_len = [n0]
+    out = torch.empty((T, B, Hq, d), dtype=torch.bfloat16, device=DEV)
+    qd, knd, vnd = q.to(DEV), kn.to(DEV), vn.to(DEV)
+    for t in range(T):
+        cache.decode(qd[t], knd[t], vnd[t], out[t])
+    torch.cuda.synchronize()
+    assert cache.kv_len.cpu().tolist() == [n0 + T]
+    got, kc64, vc64, kn64, vn64, q64 = f64(out), f64(kc), f64(vc), f64(kn), f64(vn), f64(q)
+    for g in range(Hkv):
+        for t in range(T):
+            rk = np.concatenate([kc64[0, g, :n0], kn64[: t + 1, 0, g]])
+            rv = np.concatenate([vc64[0, g, :n0], vn64[: t + 1, 0, g]])
+            ref = O.decode_step(q64[t, 0, g * G:(g + 1) * G], rk, rv)
+            err = np.abs(got[t, 0, g * G:(g + 1) * G] - ref).max()
+            assert err <= DECODE_TOL[torch.bfloat16], f"g={g} t={t}: max abs err {err}"
