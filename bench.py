@@ -440,11 +440,13 @@ def cold_decode(torch, _lib, Evictor, dev, wl, q_win, k, v, qd, knd, vnd,
 
 def scorer_variants(torch, _lib, synth, Evictor, dev, reps=10):
     """Supplementary: scoring time of each scorer (max-pool window scores, the
-    mean-pooled variant, KNorm, and at L = 8192 H2O) at the L = 8192 and
-    L = 131072 shapes, from a graph of `reps` scoring calls (2 for H2O); KNorm's
-    bandwidth counts one read of K plus the fp32 scores written."""
+    mean-pooled variant, KNorm, and at L = 8192 H2O) at the L = 8192, one
+    layer of the L = 32768 and the L = 131072 shapes, from a graph of `reps`
+    scoring calls (2 for H2O); KNorm's bandwidth counts one read of K plus the
+    fp32 scores written; the window scorers' fp64 rate counts the window
+    products 2 Hq w L d over the whole scoring call."""
     out = {}
-    for wid in (2, 5):
+    for wid in (2, 3, 5):
         wl = synth.WORKLOADS[wid]
         B, Hq, Hkv, d, w, L = wl.B, wl.Hq, wl.Hkv, wl.d, wl.w, wl.L
         pr = synth.make_prompt(wl)
@@ -469,6 +471,9 @@ def scorer_variants(torch, _lib, synth, Evictor, dev, reps=10):
             torch.cuda.synchronize()
             us = _best_ms(torch, g.replay) * 1e3 / n
             row[scorer] = {"us": round(us, 2)}
+            if scorer in ("snapkv", "snapkv_avg"):
+                flops = 2 * Hq * w * L * d
+                row[scorer]["fp64_TFLOPs"] = round(flops / (us * 1e-6) / 1e12, 2)
             if scorer == "knorm":
                 nbytes = Hkv * L * d * 2 + Hkv * (L - w) * 4
                 row[scorer]["GBps"] = round(nbytes / (us * 1e-6) / 1e9, 1)
