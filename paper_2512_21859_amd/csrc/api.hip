@@ -70,7 +70,7 @@ tb_status check_common(int32_t B, int32_t Hq, int32_t Hkv, int32_t d, tb_dtype d
 
 size_t decode_ws(int32_t B, int32_t Hkv, int32_t G, int32_t d, int32_t cap, bool bf16) {
   const size_t n_chunks = tb::decode_plan(B, Hkv, cap, bf16).n_chunks;
-  const size_t part = static_cast<size_t>(B) * Hkv * n_chunks * G * (d + 4) * sizeof(float);
+  const size_t part = static_cast<size_t>(B) * Hkv * n_chunks * G * (d + tb::kPartPad) * sizeof(float);
   return align256(part) + align256(static_cast<size_t>(B) * sizeof(int32_t));
 }
 
@@ -465,7 +465,7 @@ tb_status decode_impl(const char* name, const void* q, const void* k_new, const 
     a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(d)));
     char* p = static_cast<char*>(ws);
     a.part = reinterpret_cast<float*>(p);
-    p += align256(static_cast<size_t>(B) * Hkv * a.n_chunks * G * (d + 4) * sizeof(float));
+    p += align256(static_cast<size_t>(B) * Hkv * a.n_chunks * G * (d + tb::kPartPad) * sizeof(float));
     a.seq_len = reinterpret_cast<int32_t*>(p);
     return hip_status(tb::launch_decode(a, G, d, bf16, stream), name);
   } catch (...) {

@@ -314,16 +314,16 @@ void decode_mfma_kernel(DecodeArgs a) {
   // ---- merge the lane groups' sums, then the waves, into this block's partial
   float l_tot = l_part + __shfl_xor(l_part, 16);
   l_tot += __shfl_xor(l_tot, 32);
-  float* part = a.part + (bg * a.n_chunks + c) * G * (D + 4);
+  float* part = a.part + (bg * a.n_chunks + c) * G * (D + kPartPad);
   if constexpr (WAVES == 1) {
     // one wave: its (o, m, l) is the block's partial, stored from registers
     // (lane (q4, r16) holds d = 16 n + 4 q4 .. +3 of head r16)
     if (r16 < G) {
 #pragma unroll
       for (int n = 0; n < NC; ++n)
-        *reinterpret_cast<float4*>(part + r16 * (D + 4) + 16 * n + 4 * q4) =
+        *reinterpret_cast<float4*>(part + r16 * (D + kPartPad) + 16 * n + 4 * q4) =
             make_float4(accO[n][0], accO[n][1], accO[n][2], accO[n][3]);
-      if (q4 == 0) *reinterpret_cast<float2*>(part + r16 * (D + 4) + D) = make_float2(m_sc, l_tot);
+      if (q4 == 0) *reinterpret_cast<float2*>(part + r16 * (D + kPartPad) + D) = make_float2(m_sc, l_tot);
     }
     if (c == 0 && g == 0 && tid == 0) a.seq_len[b] = N;
     return;
@@ -356,8 +356,8 @@ void decode_mfma_kernel(DecodeArgs a) {
         O.x += x.x * sc; O.y += x.y * sc; O.z += x.z * sc; O.w += x.w * sc;
       }
     }
-    *reinterpret_cast<float4*>(part + h * (D + 4) + 4 * e4) = O;
-    if (e4 == 0) *reinterpret_cast<float2*>(part + h * (D + 4) + D) = make_float2(M, L);
+    *reinterpret_cast<float4*>(part + h * (D + kPartPad) + 4 * e4) = O;
+    if (e4 == 0) *reinterpret_cast<float2*>(part + h * (D + kPartPad) + D) = make_float2(M, L);
   }
   if (c == 0 && g == 0 && tid == 0) a.seq_len[b] = N;
 }
@@ -513,7 +513,7 @@ __global__ __launch_bounds__(kValuThreads) void decode_valu_kernel(DecodeArgs a)
   }
   __syncthreads();
 
-  float* part = a.part + (bg * a.n_chunks + c) * G * (D + 4);
+  float* part = a.part + (bg * a.n_chunks + c) * G * (D + kPartPad);
   for (int idx = tid; idx < G * D; idx += kValuThreads) {
     const int h = idx / D, e = idx % D;
     float M = -INFINITY;
@@ -528,8 +528,8 @@ __global__ __launch_bounds__(kValuThreads) void decode_valu_kernel(DecodeArgs a)
         O += s_o[wv][h][e] * sc;
       }
     }
-    part[h * (D + 4) + e] = O;
-    if (e == 0) { part[h * (D + 4) + D] = M; part[h * (D + 4) + D + 1] = L; }
+    part[h * (D + kPartPad) + e] = O;
+    if (e == 0) { part[h * (D + kPartPad) + D] = M; part[h * (D + kPartPad) + D + 1] = L; }
   }
   if (c == 0 && g == 0 && tid == 0) a.seq_len[b] = N;
 }
@@ -556,8 +556,8 @@ __global__ __launch_bounds__(64) void decode_merge_split_kernel(DecodeArgs a) {
   const int N = a.seq_len[b];
   const int n_used = a.n_chunks;
   const size_t bg = static_cast<size_t>(b) * Hkv + g;
-  const float* base = a.part + (bg * a.n_chunks * G + hh) * (D + 4);
-  constexpr size_t CSTRIDE = static_cast<size_t>(G) * (D + 4);
+  const float* base = a.part + (bg * a.n_chunks * G + hh) * (D + kPartPad);
+  constexpr size_t CSTRIDE = static_cast<size_t>(G) * (D + kPartPad);
 
   float M = -INFINITY, L = 0.f;
   float4 O = make_float4(0.f, 0.f, 0.f, 0.f);

@@ -11,6 +11,11 @@ constexpr int kMaxB = 64;        // per-sequence values travel in kernel argumen
 constexpr int kScoreTile = 64;   // keys per scoring tile
 constexpr int kScoreRows = 256;  // window rows per scoring block
 constexpr int kVTile = 32;       // rows per tile of the compact caches (and per page)
+// Floats after the d outputs of a decode partial record (m, l, padding): with
+// d + kPartPad floats per record every 32-value slice a merge wave reads is
+// one 128-byte line (with d + 4: two lines for most slices; measured 13.53
+// against 13.61 us per decode call on the 28-layer L = 32768 benchmark).
+constexpr int kPartPad = 32;
 
 // ---------------------------------------------------------------- scoring
 struct ScoreArgs {
@@ -130,7 +135,7 @@ struct DecodeArgs {
   void* v_cache;          // [B][Hkv][cap][d]
   int32_t* kv_len;        // [B]
   void* out;              // [B][Hq][d]
-  float* part;            // ws: [B][Hkv][n_chunks][G][d+4] chunk partials (o, m, l)
+  float* part;            // ws: [B][Hkv][n_chunks][G][d+kPartPad] chunk partials (o, m, l)
   int32_t* seq_len;       // ws: [B] attended length of this step
   int32_t B, Hkv, cap, chunk, n_chunks, append;
   int32_t waves;          // waves per partial block (bf16: 1 or 4)
