@@ -461,6 +461,8 @@ tb_status decode_impl(const char* name, const void* q, const void* k_new, const 
     a.chunk = plan.chunk;
     a.n_chunks = plan.n_chunks;
     a.waves = plan.waves;
+    a.tiles_q = (cap / tb::kVTile) / plan.n_chunks;
+    a.tiles_r = (cap / tb::kVTile) % plan.n_chunks;
     a.append = k_new != nullptr;
     a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(d)));
     char* p = static_cast<char*>(ws);

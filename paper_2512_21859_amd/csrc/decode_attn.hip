@@ -18,8 +18,8 @@
 //     share of the 32-row tiles of KV head g of sequence b for all
 //     G = Hq/Hkv query heads of the group, so every K/V byte is read from HBM
 //     once per step, and writes one partial (m, l, o[G][d]).  bf16: the cap/32
-//     tiles are split as evenly as whole tiles allow (block c takes tiles
-//     [c T / C, (c + 1) T / C), T tiles, C blocks), so one block per CU covers
+//     tiles are split as evenly as whole tiles allow (T tiles, C blocks: the
+//     first T mod C blocks take one tile more), so one block per CU covers
 //     the cache with no CU left idle; fp32: blocks of `chunk` rows.  A block
 //     has one wave (the wave stores its partial from registers) or 2, 4 or 8
 //     (bf16: wave w takes every WAVES-th tile of the block from its w-th on;
@@ -112,9 +112,11 @@ void decode_mfma_kernel(DecodeArgs a) {
   const uint16_t* kn = static_cast<const uint16_t*>(a.k_new) + bg * D;
   const uint16_t* vn = static_cast<const uint16_t*>(a.v_new) + bg * D;
   const int cap = a.cap;
-  const int n_tiles = cap / kVT;
-  const int t_lo = static_cast<int>(static_cast<long long>(c) * n_tiles / a.n_chunks);
-  const int t_hi = static_cast<int>(static_cast<long long>(c + 1) * n_tiles / a.n_chunks);
+  // block c: tiles [c q + min(c, r), + q + (c < r)), q = n_tiles / n_chunks and
+  // r = n_tiles % n_chunks from the host (no device division before the first
+  // load)
+  const int t_lo = c * a.tiles_q + min(c, a.tiles_r);
+  const int t_hi = t_lo + a.tiles_q + (c < a.tiles_r ? 1 : 0);
   const int t_first = t_lo + wave;               // this wave: t_first, t_first + WAVES, ...
   // K tile row permutation: MFMA row r of tile t <-> key 8*(r/4) + 4*t + r%4.
   const int krow0 = 8 * (r16 >> 2) + (r16 & 3);

@@ -139,6 +139,7 @@ struct DecodeArgs {
   int32_t* seq_len;       // ws: [B] attended length of this step
   int32_t B, Hkv, cap, chunk, n_chunks, append;
   int32_t waves;          // waves per partial block (bf16: 1 or 4)
+  int32_t tiles_q, tiles_r;  // bf16: (cap / 32) / n_chunks and (cap / 32) % n_chunks
   const int32_t* table;   // paged caches (nullptr: contiguous); see CompactArgs
   int32_t max_pages, n_pages;
   float scale_log2;       // log2(e)/sqrt(d)
